@@ -1,0 +1,28 @@
+"""CPU oracle for the ESPACE projected linear layer.
+
+TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the benchmark's
+CPU-baseline leg may import this package; the library and its Python binding
+never do, and this package imports nothing from them.
+"""
+from .espace_ref import (  # noqa: F401
+    fold,
+    project,
+    expand,
+    projected_linear,
+    projected_linear_from_weights,
+    dense,
+    reconstruct,
+    rel_fro,
+    sampled_projected_linear,
+    sampled_dense,
+    autocorrelation,
+    principal_components,
+    normalized_autocorrelation,
+)
+from .brute import (  # noqa: F401
+    bf_fold,
+    bf_project,
+    bf_expand,
+    bf_dense,
+    bf_reconstruct,
+)

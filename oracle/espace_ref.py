@@ -1,0 +1,145 @@
+"""Plain float64 reference of the ESPACE projected linear layer.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+What the method computes (paper, Section 2.2, Eq. 3): a linear layer
+Y = WᵀX (Section 2.1, Eq. 1) is replaced at inference by
+    Y ≈ (PᵀW)ᵀ (PᵀX)
+with a static K×L matrix P of orthonormal columns; the folded weight PᵀW is
+computed once before deployment ("inference view", Section 2.2), and each call
+computes the projection PᵀX followed by the product with the folded weight.
+The result of the method for a given P is exactly (PᵀW)ᵀ(PᵀX); it is written
+out here with plain matrix products in float64.
+
+Paper orientation vs storage.  The paper writes W as K×N_p (used transposed),
+X as K×M_p (tokens as columns) and P as K×L.  Arrays here are stored
+row-major as
+    W[M][K]   = the paper's Wᵀ            (M output features)
+    X[N][K]   = the paper's Xᵀ            (N tokens, token-major)
+    Pt[L][K]  = the paper's Pᵀ
+    Wf[M][L]  = the paper's (PᵀW)ᵀ        (folded weight)
+    Z[N][L]   = the paper's (PᵀX)ᵀ        (projected activations)
+    Y[N][M]   = the paper's Yᵀ
+Every function below converts its arguments to the paper's orientation,
+evaluates the paper's expression, and converts the result back.
+"""
+import numpy as np
+
+
+def _f64(a):
+    return np.asarray(a, dtype=np.float64)
+
+
+# -- the inference path (Section 2.2, Eq. 3) ---------------------------------
+
+def fold(W, Pt):
+    """Folded weight, stored as Wf[M][L]: the paper's PᵀW (L×M), transposed.
+    Section 2.2 (inference view: PᵀW is pre-computed before deployment)."""
+    Wp = _f64(W).T            # K×M
+    P = _f64(Pt).T            # K×L
+    PtW = P.T @ Wp            # L×M
+    return np.ascontiguousarray(PtW.T)
+
+
+def project(Pt, X):
+    """Projected activations, stored as Z[N][L]: the paper's PᵀX (L×N),
+    transposed.  Section 2.2, Eq. 3 (right factor); Eq. 6 gives its entries as
+    the inner products <p_i, x>."""
+    Xp = _f64(X).T            # K×N
+    P = _f64(Pt).T            # K×L
+    PtX = P.T @ Xp            # L×N
+    return np.ascontiguousarray(PtX.T)
+
+
+def expand(Z, Wf):
+    """Y[N][M] from the projected activations and the folded weight: the
+    paper's (PᵀW)ᵀ(PᵀX), transposed.  Section 2.2, Eq. 3."""
+    PtX = _f64(Z).T           # L×N
+    PtW = _f64(Wf).T          # L×M
+    Yp = PtW.T @ PtX          # M×N
+    return np.ascontiguousarray(Yp.T)
+
+
+def projected_linear(X, Pt, Wf):
+    """One call of the layer given its folded weight: expand(project(X))."""
+    return expand(project(Pt, X), Wf)
+
+
+def projected_linear_from_weights(X, Pt, W):
+    """The method's result for weight W: (PᵀW)ᵀ(PᵀX), Eq. 3, folding included."""
+    return expand(project(Pt, X), fold(W, Pt))
+
+
+def dense(X, W):
+    """The layer without projection, Y = WᵀX (Section 2.1, Eq. 1), as Y[N][M]."""
+    Wp = _f64(W).T            # K×M
+    Xp = _f64(X).T            # K×N
+    return np.ascontiguousarray((Wp.T @ Xp).T)
+
+
+def reconstruct(Pt, X):
+    """X̃ = PPᵀX written as Eq. 6: x̃ = Σ_i <p_i, x> p_i for each token x,
+    returned token-major [N][K]."""
+    P = _f64(Pt).T            # K×L
+    Xp = _f64(X).T            # K×N
+    Xt = np.zeros_like(Xp)
+    for i in range(P.shape[1]):
+        p = P[:, i]
+        Xt += np.outer(p, p @ Xp)
+    return np.ascontiguousarray(Xt.T)
+
+
+def rel_fro(a, ref):
+    """Relative Frobenius error ||a - ref||_F / ||ref||_F in float64."""
+    a = _f64(a)
+    ref = _f64(ref)
+    den = np.linalg.norm(ref)
+    num = np.linalg.norm(a - ref)
+    return float(num / den) if den > 0 else float(num)
+
+
+# -- outputs at sampled positions (for layers too large to evaluate whole) ---
+
+def sampled_projected_linear(X, Pt, W, rows, cols):
+    """Y[rows][:, cols] of (PᵀW)ᵀ(PᵀX), computing only what those outputs need:
+    the folded-weight rows of the selected output features and the projections
+    of the selected tokens."""
+    rows = np.asarray(rows)
+    cols = np.asarray(cols)
+    Wf_sel = fold(_f64(W)[cols], Pt)          # [|cols|][L]
+    Z_sel = project(Pt, _f64(X)[rows])        # [|rows|][L]
+    return expand(Z_sel, Wf_sel)              # [|rows|][|cols|]
+
+
+def sampled_dense(X, W, rows, cols):
+    return dense(_f64(X)[np.asarray(rows)], _f64(W)[np.asarray(cols)])
+
+
+# -- calibration (Section 3.1, Eq. 5; Theorem 1; Corollary 1) -----------------
+
+def autocorrelation(batches):
+    """C_X averaged over calibration batches, Eq. 5: for each batch X_i (tokens
+    as rows here, K-vectors x), C_i = (Σ x xᵀ)/M_i, and C_X = (Σ_i C_i)/B."""
+    C = None
+    for Xi in batches:
+        Xp = _f64(Xi).T                       # K×M_i, tokens as columns
+        Ci = (Xp @ Xp.T) / Xp.shape[1]
+        C = Ci if C is None else C + Ci
+    return C / len(batches)
+
+
+def normalized_autocorrelation(batches):
+    """Ĉ_X of Corollary 1: the autocorrelation of L2-normalised tokens."""
+    normed = []
+    for Xi in batches:
+        Xi = _f64(Xi)
+        normed.append(Xi / np.linalg.norm(Xi, axis=1, keepdims=True))
+    return autocorrelation(normed)
+
+
+def principal_components(C, L):
+    """Theorem 1: P is the L principal eigenvectors of C (eigenvalues sorted in
+    decreasing order).  Returns (Pt[L][K], all eigenvalues descending)."""
+    d, V = np.linalg.eigh(_f64(C))
+    order = np.argsort(d)[::-1]
+    return np.ascontiguousarray(V[:, order[:L]].T), d[order]

@@ -1,0 +1,289 @@
+"""Checks that pin the CPU oracle to facts the paper and the mathematics fix.
+
+Each pin takes a namespace `o` exposing the oracle's functions and raises
+AssertionError when the oracle disagrees with the fact.  The pins do not
+re-type the oracle's formulas: they compare it with brute-force loop sums,
+with a different formula for the same quantity (Eq. 6 instead of Eq. 3),
+with special cases that reduce to a plain product, with exact results of
+permutation matrices, and with the identities of Theorem 1 and Proposition 1.
+"""
+import itertools
+
+import numpy as np
+
+from oracle import brute
+
+RTOL = 1e-12
+
+
+def _rng(seed):
+    return np.random.default_rng(np.random.SeedSequence([20241005, seed]))
+
+
+def _orthonormal(K, L, rng):
+    q, r = np.linalg.qr(rng.standard_normal((K, L)))
+    return q * np.sign(np.diag(r))[None, :]
+
+
+def _close(a, b, rtol=RTOL, what=""):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    assert a.shape == b.shape, f"{what}: shape {a.shape} != {b.shape}"
+    scale = max(np.abs(b).max(), 1e-300)
+    err = np.abs(a - b).max() / scale
+    assert err <= rtol, f"{what}: max rel err {err:.3e} > {rtol:.1e}"
+
+
+def _tiny_case(seed, K=7, M=5, L=3, N=4):
+    rng = _rng(seed)
+    W = rng.standard_normal((M, K))
+    X = rng.standard_normal((N, K))
+    Pt = _orthonormal(K, L, rng).T.copy()
+    return W, X, Pt
+
+
+# -- pins --------------------------------------------------------------------
+
+def pin_brute_force(o):
+    """Every product equals its entry-by-entry exactly rounded sum (math.fsum)
+    on tiny non-square shapes (Section 2.2, Eq. 3; Section 2.1, Eq. 1)."""
+    for seed, (K, M, L, N) in enumerate([(7, 5, 3, 4), (6, 9, 6, 2), (8, 3, 1, 5)]):
+        W, X, Pt = _tiny_case(seed, K, M, L, N)
+        Wf = o.fold(W, Pt)
+        Z = o.project(Pt, X)
+        _close(Wf, brute.bf_fold(W.tolist(), Pt.tolist()), what="fold")
+        _close(Z, brute.bf_project(Pt.tolist(), X.tolist()), what="project")
+        _close(o.expand(Z, Wf), brute.bf_expand(Z.tolist(), Wf.tolist()), what="expand")
+        _close(o.dense(X, W), brute.bf_dense(X.tolist(), W.tolist()), what="dense")
+        _close(o.reconstruct(Pt, X), brute.bf_reconstruct(Pt.tolist(), X.tolist()),
+               what="reconstruct")
+        # the composed layer against the loops composed by hand
+        Yb = brute.bf_expand(brute.bf_project(Pt.tolist(), X.tolist()),
+                             brute.bf_fold(W.tolist(), Pt.tolist()))
+        _close(o.projected_linear_from_weights(X, Pt, W), Yb, what="projected_linear")
+        _close(o.projected_linear(X, Pt, Wf), Yb, what="projected_linear(Wf)")
+
+
+def pin_associativity(o):
+    """(PᵀW)ᵀ(PᵀX) = Wᵀ(PPᵀX) (Eq. 3), with PPᵀX evaluated token by token as
+    Σ_i <p_i, x> p_i (Eq. 6) and the outer product as a plain dense layer."""
+    rng = _rng(100)
+    K, M, L, N = 48, 40, 12, 30
+    W = rng.standard_normal((M, K))
+    X = rng.standard_normal((N, K))
+    Pt = _orthonormal(K, L, rng).T.copy()
+    Y = o.projected_linear_from_weights(X, Pt, W)
+    Xt = brute.bf_reconstruct(Pt.tolist(), X.tolist())
+    Y2 = brute.bf_dense(Xt, W.tolist())
+    _close(Y, Y2, rtol=1e-11, what="associativity")
+
+
+def pin_full_rank_identity(o):
+    """L = K with orthonormal P gives PPᵀ = I, so the layer equals WᵀX
+    (Section 2.2: PPᵀ differs from the identity only when L < K)."""
+    rng = _rng(200)
+    K, M, N = 32, 20, 16
+    W = rng.standard_normal((M, K))
+    X = rng.standard_normal((N, K))
+    Pt = _orthonormal(K, K, rng).T.copy()
+    _close(o.projected_linear_from_weights(X, Pt, W),
+           brute.bf_dense(X.tolist(), W.tolist()), rtol=1e-11, what="L=K identity")
+
+
+def pin_rotation_invariance(o):
+    """Replacing P by P·R with R orthogonal (L×L) leaves the layer unchanged,
+    since (PR)(PR)ᵀ = PPᵀ; a mistake that breaks the pairing of the two P
+    factors changes the result."""
+    rng = _rng(300)
+    K, M, L, N = 24, 18, 9, 11
+    W = rng.standard_normal((M, K))
+    X = rng.standard_normal((N, K))
+    P = _orthonormal(K, L, rng)
+    R = _orthonormal(L, L, rng)
+    Y1 = o.projected_linear_from_weights(X, P.T.copy(), W)
+    Y2 = o.projected_linear_from_weights(X, (P @ R).T.copy(), W)
+    _close(Y1, Y2, rtol=1e-11, what="rotation invariance")
+
+
+def pin_selection_matrix(o):
+    """P whose columns are distinct signed unit vectors ±e_j: the folded weight
+    is exactly ±W[:, j] and the projection exactly ±X[:, j] (products with ±1
+    and sums of zeros are exact)."""
+    rng = _rng(400)
+    K, M, L, N = 16, 7, 5, 6
+    W = rng.standard_normal((M, K))
+    X = rng.standard_normal((N, K))
+    J = rng.permutation(K)[:L]
+    s = rng.choice([-1.0, 1.0], size=L)
+    Pt = np.zeros((L, K))
+    Pt[np.arange(L), J] = s
+    Wf = o.fold(W, Pt)
+    Z = o.project(Pt, X)
+    assert np.array_equal(Wf, W[:, J] * s[None, :]), "fold with selection P"
+    assert np.array_equal(Z, X[:, J] * s[None, :]), "project with selection P"
+    Y = o.expand(Z, Wf)
+    _close(Y, brute.bf_dense((X[:, J]).tolist(), (W[:, J]).tolist()), what="selection expand")
+
+
+def _hadamard(K):
+    H = np.array([[1.0]])
+    while H.shape[0] < K:
+        H = np.block([[H, H], [H, -H]])
+    return H
+
+
+def pin_hadamard(o):
+    """Sylvester-Hadamard/sqrt(K) is orthonormal; with L = K the layer is WᵀX,
+    and with L < K it keeps exactly the leading Hadamard directions."""
+    rng = _rng(500)
+    K, M, N = 64, 10, 9
+    W = rng.standard_normal((M, K))
+    X = rng.standard_normal((N, K))
+    H = _hadamard(K) / np.sqrt(K)
+    _close(o.projected_linear_from_weights(X, H.T.copy(), W),
+           brute.bf_dense(X.tolist(), W.tolist()), rtol=1e-11, what="Hadamard L=K")
+
+
+def pin_exact_rank_reconstruction(o):
+    """Tokens of exact rank r <= L: the top-L eigenvectors of the calibrated
+    autocorrelation span them, so PPᵀX = X and the layer equals WᵀX (consequence
+    of Theorem 1: the minimal mean squared error is then zero)."""
+    rng = _rng(600)
+    K, M, r, L, N = 40, 12, 6, 8, 50
+    basis = _orthonormal(K, r, rng)
+    X = (rng.standard_normal((N, r)) @ basis.T)
+    W = rng.standard_normal((M, K))
+    C = o.autocorrelation([X[:25], X[25:]])
+    Pt, d = o.principal_components(C, L)
+    _close(o.reconstruct(Pt, X), X, rtol=1e-10, what="rank<=L reconstruction")
+    _close(o.projected_linear_from_weights(X, Pt, W),
+           brute.bf_dense(X.tolist(), W.tolist()), rtol=1e-10, what="rank<=L layer")
+
+
+def pin_tail_eigenvalue_identity(o):
+    """From the proof of Theorem 1: the MSE of the projection equals
+    E||x||² − Σ_{i<=L} p_iᵀ C_X p_i, which for the principal eigenvectors is the
+    sum of the discarded eigenvalues: (1/N)||X − PPᵀX||² = Σ_{i>L} d_i."""
+    rng = _rng(700)
+    K, L, N = 20, 7, 300
+    A = rng.standard_normal((K, K)) * (1.0 / np.arange(1, K + 1))[None, :]
+    X = rng.standard_normal((N, K)) @ A.T
+    C = o.autocorrelation([X])
+    Pt, d = o.principal_components(C, L)
+    mse = np.sum((X - o.reconstruct(Pt, X)) ** 2) / N
+    tail = float(np.sum(d[L:]))
+    assert abs(mse - tail) <= 1e-10 * max(tail, 1e-300), f"tail identity {mse} vs {tail}"
+    # and the eigenvalues are those of the batch second moment, in decreasing order
+    assert np.all(np.diff(d) <= 1e-12), "eigenvalues not in decreasing order"
+    brute_C = np.array([[sum(X[n, i] * X[n, j] for n in range(N)) / N for j in range(K)]
+                        for i in range(K)])
+    _close(C, brute_C, rtol=1e-12, what="autocorrelation")
+
+
+def pin_batch_average(o):
+    """Eq. 5: C_X is the average over calibration batches of X_i X_iᵀ / M_i;
+    with batches of unequal size that is not the pooled second moment."""
+    rng = _rng(750)
+    K = 5
+    b1 = rng.standard_normal((3, K))
+    b2 = rng.standard_normal((9, K)) * 2.0
+    C = o.autocorrelation([b1, b2])
+    C1 = np.array([[sum(b1[n, i] * b1[n, j] for n in range(3)) / 3 for j in range(K)]
+                   for i in range(K)])
+    C2 = np.array([[sum(b2[n, i] * b2[n, j] for n in range(9)) / 9 for j in range(K)]
+                   for i in range(K)])
+    _close(C, (C1 + C2) / 2, rtol=1e-12, what="batch average")
+
+
+def pin_theorem1_brute_force(o):
+    """Theorem 1 on tiny inputs: no random orthonormal P (K <= 6) attains a
+    lower empirical MSE than the top-L eigenvectors of C_X; Corollary 1 likewise
+    for the normalised MSE with the normalised autocorrelation."""
+    rng = _rng(800)
+    for K, L in ((4, 2), (6, 3), (5, 1)):
+        X = rng.standard_normal((60, K)) @ rng.standard_normal((K, K))
+        X[:5] *= 20.0  # a few large outliers, so MSE and NMSE optima differ
+        Pt, _ = o.principal_components(o.autocorrelation([X]), L)
+        Pn, _ = o.principal_components(o.normalized_autocorrelation([X]), L)
+
+        def mse(Ptr):
+            return np.mean(np.sum((X - o.reconstruct(Ptr, X)) ** 2, axis=1))
+
+        def nmse(Ptr):
+            e = np.sum((X - o.reconstruct(Ptr, X)) ** 2, axis=1)
+            return np.mean(e / np.sum(X ** 2, axis=1))
+
+        best, bestn = mse(Pt), nmse(Pn)
+        for _ in range(2000):
+            Pr = _orthonormal(K, L, rng).T.copy()
+            assert mse(Pr) >= best - 1e-12, "random P beats Theorem 1"
+            assert nmse(Pr) >= bestn - 1e-12, "random P beats Corollary 1"
+        # coordinate subspaces too (exhaustive over column subsets)
+        for J in itertools.combinations(range(K), L):
+            Pc = np.zeros((L, K))
+            Pc[np.arange(L), list(J)] = 1.0
+            assert mse(Pc) >= best - 1e-12
+
+
+def pin_norm_and_bound(o):
+    """Proposition 1 (proof, Appendix A.3): ||x̃|| <= ||x|| for every token, and
+    per sample (y − ỹ)² <= 2||w||²||x||² − 2<w,x><w,x̃>, with y from the dense
+    layer and ỹ from the projected one."""
+    rng = _rng(900)
+    K, M, L, N = 12, 6, 4, 25
+    W = rng.standard_normal((M, K))
+    X = rng.standard_normal((N, K))
+    Pt = _orthonormal(K, L, rng).T.copy()
+    Xt = o.reconstruct(Pt, X)
+    assert np.all(np.sum(Xt ** 2, 1) <= np.sum(X ** 2, 1) * (1 + 1e-12)), "||x~|| > ||x||"
+    Y = np.asarray(o.dense(X, W))
+    Yt = np.asarray(o.projected_linear_from_weights(X, Pt, W))
+    wx = X @ W.T
+    wxt = Xt @ W.T
+    bound = 2 * np.sum(W ** 2, 1)[None, :] * np.sum(X ** 2, 1)[:, None] - 2 * wx * wxt
+    assert np.all((Y - Yt) ** 2 <= bound + 1e-9), "Proposition 1 bound violated"
+    # the projected layer is the dense layer applied to x̃
+    _close(Yt, wxt, rtol=1e-11, what="projected = dense(x~)")
+
+
+def pin_sampled(o):
+    """Outputs at sampled positions equal the same entries of the whole layer."""
+    rng = _rng(1000)
+    K, M, L, N = 30, 26, 10, 19
+    W = rng.standard_normal((M, K))
+    X = rng.standard_normal((N, K))
+    Pt = _orthonormal(K, L, rng).T.copy()
+    rows = np.array([0, 5, 18, 7])
+    cols = np.array([25, 0, 3, 11, 12])
+    Yb = np.array(brute.bf_expand(brute.bf_project(Pt.tolist(), X.tolist()),
+                                  brute.bf_fold(W.tolist(), Pt.tolist())))
+    _close(o.sampled_projected_linear(X, Pt, W, rows, cols), Yb[np.ix_(rows, cols)],
+           what="sampled projected")
+    _close(o.sampled_dense(X, W, rows, cols),
+           np.array(brute.bf_dense(X.tolist(), W.tolist()))[np.ix_(rows, cols)],
+           what="sampled dense")
+
+
+def pin_rel_fro(o):
+    """Relative Frobenius error on values with a known answer."""
+    ref = np.array([[3.0, 0.0], [0.0, 4.0]])
+    a = ref + np.array([[0.0, 0.0], [0.0, 0.5]])
+    assert abs(o.rel_fro(a, ref) - 0.1) < 1e-15
+    assert o.rel_fro(ref, ref) == 0.0
+
+
+ALL_PINS = [
+    pin_brute_force,
+    pin_associativity,
+    pin_full_rank_identity,
+    pin_rotation_invariance,
+    pin_selection_matrix,
+    pin_hadamard,
+    pin_exact_rank_reconstruction,
+    pin_tail_eigenvalue_identity,
+    pin_batch_average,
+    pin_theorem1_brute_force,
+    pin_norm_and_bound,
+    pin_sampled,
+    pin_rel_fro,
+]

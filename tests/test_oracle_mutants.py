@@ -1,0 +1,115 @@
+"""Plant plausible mistakes in the oracle (on the CPU) and check that the pins
+catch every one of them: a dropped term, a wrong sign, a transposed operand,
+the wrong end of the spectrum, a missing normalisation."""
+import types
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import espace_ref as R
+from tests import oracle_pins
+
+
+def _base():
+    return {k: getattr(oracle, k) for k in dir(oracle) if not k.startswith("_")}
+
+
+def _fold_transposed_p(W, Pt):
+    # uses Pt as if it were P (K×L); only shape-valid when L == K
+    return np.asarray(W, float) @ np.asarray(Pt, float)
+
+
+def _project_drops_last(Pt, X):
+    Z = R.project(Pt, X)
+    Z[:, -1] = 0.0
+    return Z
+
+
+def _expand_sign(Z, Wf):
+    return -R.expand(Z, Wf)
+
+
+def _expand_transposed(Z, Wf):
+    Z = np.asarray(Z, float)
+    Wf = np.asarray(Wf, float)
+    return (Z @ Wf.T)[:, ::-1].copy()
+
+
+def _dense_transposed(X, W):
+    return np.asarray(X, float) @ np.asarray(W, float)[::-1].T
+
+
+def _pc_ascending(C, L):
+    d, V = np.linalg.eigh(np.asarray(C, float))
+    return np.ascontiguousarray(V[:, :L].T), d
+
+
+def _autocorr_unscaled(batches):
+    C = None
+    for Xi in batches:
+        Xi = np.asarray(Xi, float)
+        Ci = Xi.T @ Xi
+        C = Ci if C is None else C + Ci
+    return C / len(batches)
+
+
+def _autocorr_pooled(batches):
+    X = np.concatenate([np.asarray(b, float) for b in batches])
+    return X.T @ X / X.shape[0]
+
+
+def _reconstruct_drops_term(Pt, X):
+    return R.reconstruct(np.asarray(Pt)[:-1], X) if len(Pt) > 1 else 0 * np.asarray(X, float)
+
+
+def _normalized_plain(batches):
+    return R.autocorrelation(batches)
+
+
+def _fold_skips_projection(W, Pt):
+    W = np.asarray(W, float)
+    L = len(Pt)
+    return W[:, :L].copy()
+
+
+MUTANTS = {
+    "fold uses Pt for P": {"fold": _fold_transposed_p},
+    "fold ignores P": {"fold": _fold_skips_projection},
+    "project drops a component": {"project": _project_drops_last},
+    "expand flips sign": {"expand": _expand_sign},
+    "expand permutes outputs": {"expand": _expand_transposed},
+    "dense permutes weights": {"dense": _dense_transposed},
+    "smallest eigenvectors": {"principal_components": _pc_ascending},
+    "autocorrelation without 1/M": {"autocorrelation": _autocorr_unscaled},
+    "autocorrelation pooled, not batch-averaged": {"autocorrelation": _autocorr_pooled},
+    "reconstruct drops a term": {"reconstruct": _reconstruct_drops_term},
+    "normalised autocorrelation not normalised": {"normalized_autocorrelation": _normalized_plain},
+}
+
+
+def _caught(ns):
+    for pin in oracle_pins.ALL_PINS:
+        try:
+            pin(ns)
+        except Exception:
+            return pin.__name__
+    return None
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name):
+    fns = _base()
+    fns.update(MUTANTS[name])
+    if "fold" in MUTANTS[name] or "project" in MUTANTS[name] or "expand" in MUTANTS[name]:
+        # keep the composed helpers consistent with the mutated step
+        f, p, e = fns["fold"], fns["project"], fns["expand"]
+        fns["projected_linear_from_weights"] = lambda X, Pt, W: e(p(Pt, X), f(W, Pt))
+        fns["projected_linear"] = lambda X, Pt, Wf: e(p(Pt, X), Wf)
+        fns["sampled_projected_linear"] = (
+            lambda X, Pt, W, rows, cols: e(p(Pt, np.asarray(X)[rows]), f(np.asarray(W)[cols], Pt)))
+    if "dense" in MUTANTS[name]:
+        d = fns["dense"]
+        fns["sampled_dense"] = lambda X, W, rows, cols: d(np.asarray(X)[rows], np.asarray(W)[cols])
+    ns = types.SimpleNamespace(**fns)
+    assert _caught(ns) is not None, f"mutant '{name}' passes every pin"
