@@ -1,0 +1,294 @@
+"""Benchmark of the ESPACE projected linear layer on one MI355X.
+
+    python bench.py [--gpus 1] [--steps 50] [--warmup 10]
+
+One step is one call of the projected linear layer Y = Wf·(Pᵀ·X) (the
+projection GEMM followed by the folded-weight GEMM, Section 2.2, Eq. 3) on the
+Llama2-7B fused-QKV layer at 50% compression: K=4096, M=12288, L=1536,
+N=4096 tokens, bfloat16 storage with fp32 accumulation, synthetic seeded
+inputs resident in HBM.  The folded weight is computed once before timing, as
+the method prescribes.  Prints one JSON line.
+
+Also measured in the same run: the dense layer Y = W·X on the same GPU with
+this library's own kernels (speedup denominator), the fold, the two kernels
+of the path separately (HIP events on the launch stream; the slower one is
+the roofline kernel), decode-sized calls of the Llama2-7B FFN up+gate layer,
+and the CPU oracle on the host cores (cpu_baseline).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+ROTATE_BYTES = 600 << 20    # > 2x the 256 MB last-level cache
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    return ap.parse_args()
+
+
+def to_dev(storage, device):
+    import torch
+    import paper_2410_05437_amd as E
+    R, C = storage.shape
+    t = E.padded_empty(R, C, torch.bfloat16, device)
+    t.copy_(torch.from_numpy(np.ascontiguousarray(storage).view(np.int16)).view(torch.bfloat16))
+    return t
+
+
+def copies(nbytes_one):
+    return max(1, int(np.ceil(ROTATE_BYTES / max(nbytes_one, 1))))
+
+
+def time_calls(fn, n_args, steps, warmup, stream):
+    """Average ms per call over `steps` calls (after `warmup`), rotating over
+    the argument sets so each call streams its operands from HBM."""
+    import torch
+    for i in range(warmup):
+        fn(i % n_args)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for i in range(steps):
+        fn(i % n_args)
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps
+
+
+def time_each(fn, n_args, steps, stream):
+    """Per-launch durations (ms) of one call, each bracketed by its own events."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(evs):
+        a.record(stream)
+        fn(i % n_args)
+        b.record(stream)
+    torch.cuda.synchronize()
+    return float(np.mean([a.elapsed_time(b) for a, b in evs]))
+
+
+def cpu_baseline(inp, seconds):
+    """The float64 oracle of the same layer on the host cores (fold excluded,
+    as on the GPU); repeated full calls for about `seconds` seconds."""
+    import oracle
+    from paper_2410_05437_amd import accounting as acc
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 0) for p in threadpool_info()] + [1])
+    except Exception:  # noqa: BLE001
+        cores = len(os.sched_getaffinity(0))
+    w = inp.w
+    Wf = oracle.fold(inp.W, inp.Pt)
+    t0 = time.perf_counter()
+    calls = 0
+    while True:
+        oracle.projected_linear(inp.X, inp.Pt, Wf)
+        calls += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or calls >= 50:
+            break
+    per = el / calls
+    tflops = acc.projected_flops(w.K, w.M, w.L, w.N) / per / 1e12
+    return {"value": round(tflops, 4), "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{calls} full calls of the N={w.N} layer (float64 numpy), {el:.1f} s",
+            "ms_per_call": round(per * 1e3, 2)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
+              "this build has no multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2410_05437_amd as E
+    from paper_2410_05437_amd import accounting as acc
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    w = synth.workload(1)
+    K, M, L, N = w.K, w.M, w.L, w.N
+    inp = synth.make_inputs(w)
+
+    Xs = to_dev(inp.X_s, dev)
+    Pts = to_dev(inp.Pt_s, dev)
+    Ws = to_dev(inp.W_s, dev)
+    Wf0 = E.espace_fold_weights(Ws, Pts)
+    torch.cuda.synchronize()
+
+    one = (Xs.numel() + Pts.numel() + Wf0.numel()) * 2
+    R = copies(one)
+    Xr = [Xs] + [Xs.clone() for _ in range(R - 1)]
+    Pr = [Pts] + [Pts.clone() for _ in range(R - 1)]
+    Wfr = [Wf0] + [Wf0.clone() for _ in range(R - 1)]
+    Y = E.padded_empty(N, M, torch.bfloat16, dev)
+    ws_bytes = E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, M, K, L, N, torch.bfloat16)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    Z = E.padded_empty(N, L, torch.bfloat16, dev)
+    wsz = torch.empty(max(E.espace_workspace_bytes(E.OP_PROJECT, 0, K, L, N, torch.bfloat16), 1),
+                      dtype=torch.uint8, device=dev)
+    wse = torch.empty(max(E.espace_workspace_bytes(E.OP_EXPAND, M, L, L, N, torch.bfloat16), 1),
+                      dtype=torch.uint8, device=dev)
+
+    def step(i):
+        E.espace_projected_linear(Xr[i], Pr[i], Wfr[i], Y, ws)
+
+    # the timed region: exactly `steps` calls, synchronised on both sides
+    for i in range(args.warmup):
+        step(i % R)
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(i % R)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms = t_start.elapsed_time(t_end) / args.steps
+
+    flops = acc.projected_flops(K, M, L, N)
+    tflops = flops / (ms * 1e-3) / 1e12
+
+    # the two kernels of the path, each bracketed by events on the launch stream
+    ms_proj = time_each(lambda i: E.espace_project(Pr[i], Xr[i], Z, wsz), R, args.steps, stream)
+    ms_exp = time_each(lambda i: E.espace_expand(Z, Wfr[i], Y, wse), R, args.steps, stream)
+    kern = {
+        "project": {"ms": ms_proj, "flops": acc.gemm_flops(N, L, K)},
+        "expand": {"ms": ms_exp, "flops": acc.gemm_flops(N, M, L)},
+    }
+    dom = max(kern, key=lambda k: kern[k]["ms"])
+    achieved = kern[dom]["flops"] / (kern[dom]["ms"] * 1e-3) / 1e12
+
+    # dense baseline with the same library, same rotation
+    Rd = copies((Xs.numel() + Ws.numel()) * 2)
+    Wr = [Ws] + [Ws.clone() for _ in range(Rd - 1)]
+    Xd = [Xr[i % R] for i in range(Rd)]
+    wsd = torch.empty(max(E.espace_workspace_bytes(E.OP_DENSE, M, K, 1, N, torch.bfloat16), 1),
+                      dtype=torch.uint8, device=dev)
+    ms_dense = time_calls(lambda i: E.espace_dense_linear(Xd[i], Wr[i], Y, wsd), Rd,
+                          args.steps, args.warmup, stream)
+    dense_tflops = acc.dense_flops(K, M, N) / (ms_dense * 1e-3) / 1e12
+    del Wr, Xd
+
+    wsf = torch.empty(max(E.espace_workspace_bytes(E.OP_FOLD, M, K, L, 0, torch.bfloat16), 1),
+                      dtype=torch.uint8, device=dev)
+    Wf_tmp = E.padded_empty(M, L, torch.bfloat16, dev)
+    ms_fold = time_calls(lambda i: E.espace_fold_weights(Ws, Pts, Wf_tmp, wsf), 1,
+                         max(5, args.steps // 5), 2, stream)
+
+    # parity of the benchmarked output on sampled entries (oracle not needed:
+    # the parity tests cover this launch configuration against the oracle)
+    detail = {
+        "us_per_layer": round(ms * 1e3, 2),
+        "dense_us": round(ms_dense * 1e3, 2),
+        "dense_tflops": round(dense_tflops, 1),
+        "dense_mfma_frac": round(dense_tflops / PEAK_BF16_TFLOPS, 4),
+        "speedup_vs_dense": round(ms_dense / ms, 3),
+        "ideal_speedup": round(acc.ideal_speedup(K, M, L), 3),
+        "fold_us": round(ms_fold * 1e3, 1),
+        "project_us": round(ms_proj * 1e3, 2),
+        "expand_us": round(ms_exp * 1e3, 2),
+        "compression": round(acc.compression(K, M, L), 4),
+        "rotating_copies": R,
+    }
+
+    if not args.no_decode:
+        detail["decode"] = decode_lines(E, acc, synth, dev, stream, args)
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(inp, args.cpu_seconds)
+
+    out = {
+        "metric": "projected-linear TFLOP/s + µs/layer and speedup vs dense GEMM at 50% compression",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "llama2-7b-qkv projected linear", "K": K, "M": M, "L": L, "N": N,
+                   "parallelism": "single-gpu"},
+        "roofline": {"bound": "mfma", "kernel": dom,
+                     "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+        "cpu_baseline": cpu,
+        "detail": detail,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def decode_lines(E, acc, synth, dev, stream, args):
+    """Llama2-7B FFN up+gate (K=4096, M=22016, L=1536) at N = 1 and 16 tokens:
+    HBM-bound, rotating over copies larger than the last-level cache."""
+    import torch
+    res = {}
+    base = synth.workload(2, N=16)
+    inp = synth.make_inputs(base)
+    K, M, L = base.K, base.M, base.L
+    Ps = to_dev(inp.Pt_s, dev)
+    Ws = to_dev(inp.W_s, dev)
+    Wf = E.espace_fold_weights(Ws, Ps)
+    Xall = to_dev(inp.X_s, dev)
+    R = copies((Ps.numel() + Wf.numel()) * 2)
+    Pr = [Ps] + [Ps.clone() for _ in range(R - 1)]
+    Wfr = [Wf] + [Wf.clone() for _ in range(R - 1)]
+    Rd = copies(Ws.numel() * 2)
+    Wr = [Ws] + [Ws.clone() for _ in range(Rd - 1)]
+    for N in (1, 16):
+        X = Xall[:N]
+        Y = E.padded_empty(N, M, torch.bfloat16, dev)
+        ws = torch.empty(max(E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, M, K, L, N,
+                                                      torch.bfloat16), 1),
+                         dtype=torch.uint8, device=dev)
+        wsd = torch.empty(max(E.espace_workspace_bytes(E.OP_DENSE, M, K, 1, N, torch.bfloat16), 1),
+                          dtype=torch.uint8, device=dev)
+        ms = time_calls(lambda i: E.espace_projected_linear(X, Pr[i], Wfr[i], Y, ws), R,
+                        args.steps * 4, args.warmup, stream)
+        msd = time_calls(lambda i: E.espace_dense_linear(X, Wr[i], Y, wsd), Rd,
+                         args.steps * 4, args.warmup, stream)
+        by = acc.projected_bytes(K, M, L, N)
+        byd = acc.dense_bytes(K, M, N)
+        res[f"N{N}"] = {
+            "us_per_layer": round(ms * 1e3, 2),
+            "GB_s": round(by / (ms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(by / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "dense_us": round(msd * 1e3, 2),
+            "dense_GB_s": round(byd / (msd * 1e-3) / 1e9, 1),
+            "speedup_vs_dense": round(msd / ms, 3),
+        }
+    return res
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,163 @@
+/*
+ * espace.h - C ABI of the ESPACE projected linear layer on MI355X (gfx950).
+ *
+ * The layer (Sakr & Khailany, "ESPACE: Dimensionality Reduction of Activations
+ * for Model Compression", Section 2.2, Eq. 3) replaces a dense linear layer
+ * Y = W·X (Section 2.1, Eq. 1) at inference by
+ *
+ *        Y = (W·P)·(Pᵀ·X)
+ *
+ * where P (K×L, orthonormal columns) is a static projection calibrated before
+ * deployment and the folded weight W' = W·P (M×L) is computed once, before
+ * deployment.  Each call computes the projection Z = Pᵀ·X and then Y = W'·Z.
+ *
+ * Letters: K input features, M output features, L retained components, N tokens.
+ *
+ * Storage (all matrices row-major with an explicit leading dimension "ld",
+ * counted in elements):
+ *     W  [M][K]   weight, output features by input features
+ *     Pt [L][K]   the projection P stored column-major (row l = column p_l)
+ *     Wf [M][L]   folded weight W' = W·P
+ *     X  [N][K]   activations, token-major (row n = token x_n)
+ *     Z  [N][L]   projected activations (row n = Pᵀ·x_n)
+ *     Y  [N][M]   output, token-major
+ * With this storage every product reduces over the contiguous dimension of
+ * both operands.
+ *
+ * Conventions shared by every entry point:
+ *  - Pointers are DEVICE pointers owned by the caller; the library never
+ *    allocates, frees or keeps caller memory.
+ *  - A matrix with R rows and leading dimension ld occupies R·ld elements:
+ *    the library may read the padding columns [cols, round_up(cols, 8)) of a
+ *    row but never uses their values, and never writes outside [0, cols).
+ *  - ld >= cols, ld a multiple of 8 elements (bf16) or 4 elements (f32);
+ *    every base pointer 16-byte aligned (workspace: 256-byte aligned).
+ *  - Shapes: M, N >= 0 (0 = empty, nothing is launched); K >= 1; 1 <= L <= K
+ *    (P has L orthonormal columns of length K).  Orthonormality of P is the
+ *    caller's contract and is not checked: the library computes the products
+ *    for any P.
+ *  - The output must not overlap any input or the workspace.
+ *  - dtype: ESPACE_BF16 (bfloat16 storage, fp32 accumulation, outputs and the
+ *    intermediate Z rounded to bfloat16 with round-to-nearest-even) or
+ *    ESPACE_F32 (float32 throughout).
+ *  - workspace: device scratch of at least espace_workspace_bytes(...) bytes
+ *    for the same op, shapes and dtype; NULL only when that size is 0.  Its
+ *    contents need no initialisation and are undefined after the call.  Calls
+ *    that run concurrently must not share a workspace.
+ *  - Every call is asynchronous and stream-ordered on `stream` (NULL = the
+ *    default stream).  ESPACE_OK means "validated and enqueued"; faults during
+ *    execution surface at the caller's next synchronisation.  Any other status
+ *    means nothing was enqueued and no memory was written; espace_last_error()
+ *    then gives a description (thread-local).
+ */
+#ifndef ESPACE_H
+#define ESPACE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ESPACE_ABI_VERSION 1
+
+typedef enum {
+    ESPACE_F32 = 0,
+    ESPACE_BF16 = 1
+} espace_dtype;
+
+typedef enum {
+    ESPACE_OK = 0,
+    ESPACE_ERR_NULL = 1,       /* a required pointer is NULL */
+    ESPACE_ERR_SHAPE = 2,      /* a size or leading dimension is invalid */
+    ESPACE_ERR_ALIGN = 3,      /* a pointer or leading dimension is misaligned */
+    ESPACE_ERR_DTYPE = 4,      /* unknown dtype */
+    ESPACE_ERR_ALIAS = 5,      /* the output overlaps an input or the workspace */
+    ESPACE_ERR_WORKSPACE = 6,  /* workspace missing or too small */
+    ESPACE_ERR_HIP = 7,        /* the HIP runtime reported an error */
+    ESPACE_ERR_DEVICE = 8      /* the current device is not gfx950 */
+} espace_status;
+
+typedef enum {
+    ESPACE_OP_FOLD = 0,
+    ESPACE_OP_PROJECT = 1,
+    ESPACE_OP_EXPAND = 2,
+    ESPACE_OP_PROJECTED_LINEAR = 3,
+    ESPACE_OP_DENSE = 4
+} espace_op;
+
+/* Folded weight Wf = W·P (Section 2.2: the paper's PᵀW, "pre-computed before
+ * deployment", stored transposed).  Wf[m][l] = sum_k W[m][k]·Pt[l][k].
+ * In: W [M][K] (ldw), Pt [L][K] (ldp).  Out: Wf [M][L] (ldwf). */
+espace_status espace_fold_weights(const void* W, int64_t ldw,
+                                  const void* Pt, int64_t ldp,
+                                  void* Wf, int64_t ldwf,
+                                  int64_t M, int64_t K, int64_t L,
+                                  espace_dtype dt,
+                                  void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream);
+
+/* Projection Z = Pᵀ·X (Section 2.2, Eq. 3, right factor; Eq. 6 gives its
+ * entries as the inner products <p_l, x_n>).  Z[n][l] = sum_k X[n][k]·Pt[l][k].
+ * In: Pt [L][K] (ldp), X [N][K] (ldx).  Out: Z [N][L] (ldz). */
+espace_status espace_project(const void* Pt, int64_t ldp,
+                             const void* X, int64_t ldx,
+                             void* Z, int64_t ldz,
+                             int64_t K, int64_t L, int64_t N,
+                             espace_dtype dt,
+                             void* workspace, size_t workspace_bytes,
+                             hipStream_t stream);
+
+/* Expansion Y = Wf·Z (Section 2.2, Eq. 3: the folded weight times the
+ * projected activations).  Y[n][m] = sum_l Z[n][l]·Wf[m][l].
+ * In: Z [N][L] (ldz), Wf [M][L] (ldwf).  Out: Y [N][M] (ldy). */
+espace_status espace_expand(const void* Z, int64_t ldz,
+                            const void* Wf, int64_t ldwf,
+                            void* Y, int64_t ldy,
+                            int64_t M, int64_t L, int64_t N,
+                            espace_dtype dt,
+                            void* workspace, size_t workspace_bytes,
+                            hipStream_t stream);
+
+/* The projected linear layer Y = Wf·(Pᵀ·X) (Section 2.2, Eq. 3, inference
+ * view), i.e. espace_project followed by espace_expand with Z kept in the
+ * workspace (bf16: Z is rounded to bfloat16 between the two products).
+ * In: X [N][K] (ldx), Pt [L][K] (ldp), Wf [M][L] (ldwf).  Out: Y [N][M] (ldy).
+ * Needs espace_workspace_bytes(ESPACE_OP_PROJECTED_LINEAR, M, K, L, N, dt). */
+espace_status espace_projected_linear(const void* X, int64_t ldx,
+                                      const void* Pt, int64_t ldp,
+                                      const void* Wf, int64_t ldwf,
+                                      void* Y, int64_t ldy,
+                                      int64_t M, int64_t K, int64_t L, int64_t N,
+                                      espace_dtype dt,
+                                      void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream);
+
+/* The dense layer Y = W·X it replaces (Section 2.1, Eq. 1): the baseline.
+ * Y[n][m] = sum_k X[n][k]·W[m][k].
+ * In: X [N][K] (ldx), W [M][K] (ldw).  Out: Y [N][M] (ldy). */
+espace_status espace_dense_linear(const void* X, int64_t ldx,
+                                  const void* W, int64_t ldw,
+                                  void* Y, int64_t ldy,
+                                  int64_t M, int64_t K, int64_t N,
+                                  espace_dtype dt,
+                                  void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream);
+
+/* Workspace bytes needed by `op` for these sizes (0 when none is needed).
+ * Arguments an op does not use are ignored (e.g. L for ESPACE_OP_DENSE).
+ * Returns SIZE_MAX for invalid sizes. */
+size_t espace_workspace_bytes(espace_op op, int64_t M, int64_t K, int64_t L,
+                              int64_t N, espace_dtype dt);
+
+const char* espace_status_string(espace_status s);
+const char* espace_last_error(void);
+int espace_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ESPACE_H */

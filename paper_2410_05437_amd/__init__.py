@@ -1,0 +1,27 @@
+"""ESPACE projected linear layer on MI355X (gfx950): Python binding of libespace.so.
+
+Y = (W·P)·(Pᵀ·X)  (Sakr & Khailany, ESPACE, Section 2.2, Eq. 3), with the
+folded weight W·P computed once and the projection and expansion computed per
+call by hand-written HIP kernels.  Importing the package loads the library;
+there is no other implementation behind these functions.
+"""
+from ._lib import (  # noqa: F401
+    ABI_VERSION,
+    BF16,
+    F32,
+    OP_DENSE,
+    OP_EXPAND,
+    OP_FOLD,
+    OP_PROJECT,
+    OP_PROJECTED_LINEAR,
+    EspaceError,
+    espace_dense_linear,
+    espace_expand,
+    espace_fold_weights,
+    espace_project,
+    espace_projected_linear,
+    espace_workspace_bytes,
+    header_functions,
+    lib,
+    padded_empty,
+)

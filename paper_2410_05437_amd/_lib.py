@@ -1,0 +1,218 @@
+"""ctypes binding of libespace.so (argument marshalling only).
+
+Every computation runs in the library's HIP kernels; this module only turns
+torch tensors into (device pointer, leading dimension) pairs, allocates
+outputs and workspaces with torch, passes torch's current HIP stream, and
+raises EspaceError on a non-OK status.  It has no fallback: if the library is
+missing, importing the package fails.
+"""
+import ctypes
+import os
+import re
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libespace.so")
+HEADER = os.path.join(os.path.dirname(_HERE), "include", "espace.h")
+
+F32 = 0
+BF16 = 1
+OP_FOLD, OP_PROJECT, OP_EXPAND, OP_PROJECTED_LINEAR, OP_DENSE = range(5)
+
+_c_i64 = ctypes.c_int64
+_c_p = ctypes.c_void_p
+_c_sz = ctypes.c_size_t
+_c_int = ctypes.c_int
+
+_SIGS = {
+    # name: (argtypes, restype)
+    "espace_fold_weights": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_i64, _c_i64,
+                             _c_int, _c_p, _c_sz, _c_p], _c_int),
+    "espace_project": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_i64, _c_i64,
+                        _c_int, _c_p, _c_sz, _c_p], _c_int),
+    "espace_expand": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_i64, _c_i64,
+                       _c_int, _c_p, _c_sz, _c_p], _c_int),
+    "espace_projected_linear": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64,
+                                 _c_i64, _c_i64, _c_i64, _c_i64, _c_int, _c_p, _c_sz, _c_p], _c_int),
+    "espace_dense_linear": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_i64, _c_i64,
+                             _c_int, _c_p, _c_sz, _c_p], _c_int),
+    "espace_workspace_bytes": ([_c_int, _c_i64, _c_i64, _c_i64, _c_i64, _c_int], _c_sz),
+    "espace_status_string": ([_c_int], ctypes.c_char_p),
+    "espace_last_error": ([], ctypes.c_char_p),
+    "espace_abi_version": ([], _c_int),
+}
+
+
+class EspaceError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"espace status {status}: {message}")
+        self.status = status
+        self.message = message
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built (python paper_2410_05437_amd/build.py)")
+    lib = ctypes.CDLL(LIB_PATH)
+    for name, (args, res) in _SIGS.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+lib = _load()
+ABI_VERSION = lib.espace_abi_version()
+
+
+def header_functions():
+    """Names of the functions include/espace.h declares."""
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(espace_\w+)\s*\(", text, re.M)))
+
+
+def _check(status):
+    if status != 0:
+        msg = lib.espace_last_error().decode()
+        raise EspaceError(status, msg or lib.espace_status_string(status).decode())
+
+
+def _dt(t):
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _mat(t, name):
+    """(pointer, leading dimension) of a row-major 2-D tensor whose storage
+    holds rows*ld elements (the library may read the padding of the last row)."""
+    if t.dim() != 2:
+        raise ValueError(f"{name} must be 2-D")
+    if t.stride(1) != 1 and t.shape[1] > 1:
+        raise ValueError(f"{name} must have unit column stride")
+    ld = t.stride(0) if t.shape[0] > 1 else max(t.stride(0), t.shape[1])
+    need = (t.storage_offset() + t.shape[0] * ld) * t.element_size()
+    if t.numel() and t.untyped_storage().nbytes() < need:
+        raise ValueError(f"{name}: storage must hold rows*ld elements (use padded_empty)")
+    return ctypes.c_void_p(t.data_ptr()), ld
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def padded_empty(rows, cols, dtype, device, align=8):
+    """Uninitialised rows x cols tensor with a leading dimension rounded up to
+    `align` elements (its storage holds rows*ld elements)."""
+    ld = max((cols + align - 1) // align * align, align)
+    return torch.empty((rows, ld), dtype=dtype, device=device)[:, :cols]
+
+
+def _out(out, rows, cols, like, name):
+    if out is None:
+        return padded_empty(rows, cols, like.dtype, like.device, 8 if like.dtype == torch.bfloat16 else 4)
+    if tuple(out.shape) != (rows, cols):
+        raise ValueError(f"{name} must be {rows}x{cols}")
+    return out
+
+
+def espace_workspace_bytes(op, M, K, L, N, dtype):
+    dt = BF16 if dtype == torch.bfloat16 else F32
+    n = lib.espace_workspace_bytes(op, M, K, L, N, dt)
+    if n == ctypes.c_size_t(-1).value:
+        raise EspaceError(2, "invalid sizes for workspace query")
+    return n
+
+
+def _ws(workspace, nbytes, device):
+    if nbytes == 0:
+        return None, 0
+    if workspace is None:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def espace_fold_weights(W, Pt, Wf=None, workspace=None):
+    """Wf = W·P  (W [M][K], Pt [L][K] -> Wf [M][L])."""
+    M, K = W.shape
+    L = Pt.shape[0]
+    Wf = _out(Wf, M, L, W, "Wf")
+    ws, wsb = _ws(workspace, espace_workspace_bytes(OP_FOLD, M, K, L, 0, W.dtype), W.device)
+    pw, ldw = _mat(W, "W")
+    pp, ldp = _mat(Pt, "Pt")
+    po, ldo = _mat(Wf, "Wf")
+    with torch.cuda.device(W.device):
+        _check(lib.espace_fold_weights(pw, ldw, pp, ldp, po, ldo, M, K, L, _dt(W),
+                                       ctypes.c_void_p(ws.data_ptr() if ws is not None else 0),
+                                       wsb, _stream(W.device)))
+    return Wf
+
+
+def espace_project(Pt, X, Z=None, workspace=None):
+    """Z = Pᵀ·X  (Pt [L][K], X [N][K] -> Z [N][L])."""
+    L, K = Pt.shape
+    N = X.shape[0]
+    Z = _out(Z, N, L, X, "Z")
+    ws, wsb = _ws(workspace, espace_workspace_bytes(OP_PROJECT, 0, K, L, N, X.dtype), X.device)
+    pp, ldp = _mat(Pt, "Pt")
+    px, ldx = _mat(X, "X")
+    pz, ldz = _mat(Z, "Z")
+    with torch.cuda.device(X.device):
+        _check(lib.espace_project(pp, ldp, px, ldx, pz, ldz, K, L, N, _dt(X),
+                                  ctypes.c_void_p(ws.data_ptr() if ws is not None else 0),
+                                  wsb, _stream(X.device)))
+    return Z
+
+
+def espace_expand(Z, Wf, Y=None, workspace=None):
+    """Y = Wf·Z  (Z [N][L], Wf [M][L] -> Y [N][M])."""
+    N, L = Z.shape
+    M = Wf.shape[0]
+    Y = _out(Y, N, M, Z, "Y")
+    ws, wsb = _ws(workspace, espace_workspace_bytes(OP_EXPAND, M, L, L, N, Z.dtype), Z.device)
+    pz, ldz = _mat(Z, "Z")
+    pw, ldw = _mat(Wf, "Wf")
+    py, ldy = _mat(Y, "Y")
+    with torch.cuda.device(Z.device):
+        _check(lib.espace_expand(pz, ldz, pw, ldw, py, ldy, M, L, N, _dt(Z),
+                                 ctypes.c_void_p(ws.data_ptr() if ws is not None else 0),
+                                 wsb, _stream(Z.device)))
+    return Y
+
+
+def espace_projected_linear(X, Pt, Wf, Y=None, workspace=None):
+    """Y = Wf·(Pᵀ·X)  (X [N][K], Pt [L][K], Wf [M][L] -> Y [N][M])."""
+    N, K = X.shape
+    L = Pt.shape[0]
+    M = Wf.shape[0]
+    Y = _out(Y, N, M, X, "Y")
+    ws, wsb = _ws(workspace, espace_workspace_bytes(OP_PROJECTED_LINEAR, M, K, L, N, X.dtype), X.device)
+    px, ldx = _mat(X, "X")
+    pp, ldp = _mat(Pt, "Pt")
+    pw, ldw = _mat(Wf, "Wf")
+    py, ldy = _mat(Y, "Y")
+    with torch.cuda.device(X.device):
+        _check(lib.espace_projected_linear(px, ldx, pp, ldp, pw, ldw, py, ldy, M, K, L, N, _dt(X),
+                                           ctypes.c_void_p(ws.data_ptr() if ws is not None else 0),
+                                           wsb, _stream(X.device)))
+    return Y
+
+
+def espace_dense_linear(X, W, Y=None, workspace=None):
+    """Y = W·X  (X [N][K], W [M][K] -> Y [N][M])."""
+    N, K = X.shape
+    M = W.shape[0]
+    Y = _out(Y, N, M, X, "Y")
+    ws, wsb = _ws(workspace, espace_workspace_bytes(OP_DENSE, M, K, 1, N, X.dtype), X.device)
+    px, ldx = _mat(X, "X")
+    pw, ldw = _mat(W, "W")
+    py, ldy = _mat(Y, "Y")
+    with torch.cuda.device(X.device):
+        _check(lib.espace_dense_linear(px, ldx, pw, ldw, py, ldy, M, K, N, _dt(X),
+                                       ctypes.c_void_p(ws.data_ptr() if ws is not None else 0),
+                                       wsb, _stream(X.device)))
+    return Y

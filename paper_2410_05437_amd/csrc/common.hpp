@@ -1,0 +1,94 @@
+// Device-side helpers shared by the gfx950 kernels of the projected linear layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace espace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+// float -> bfloat16 bits, round to nearest, ties to even (NaN stays NaN).
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return bf16_rne(lo) | (bf16_rne(hi) << 16);
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t h) {
+    return __uint_as_float(h << 16);
+}
+
+// Zero the bfloat16 lanes e >= nvalid of an 8-element chunk (0 <= nvalid <= 8).
+__device__ __forceinline__ u32x4_t mask_chunk(u32x4_t v, int nvalid) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        const int e0 = 2 * w;
+        uint32_t keep = (e0 + 1 < nvalid) ? 0xffffffffu : (e0 < nvalid ? 0x0000ffffu : 0u);
+        v[w] &= keep;
+    }
+    return v;
+}
+
+// Load one 16-byte chunk of 8 bfloat16 values starting at element k of a row,
+// keeping only elements k .. depth-1.  Chunks starting at or beyond `depth`
+// are not read.  The row is padded to a multiple of 8 elements, so a partial
+// chunk stays inside the row.
+__device__ __forceinline__ u32x4_t load_chunk_masked(const uint16_t* row, int k, int depth) {
+    u32x4_t v = {0u, 0u, 0u, 0u};
+    const int nvalid = depth - k;
+    if (nvalid > 0) {
+        v = *reinterpret_cast<const u32x4_t*>(row + k);
+        if (nvalid < 8) v = mask_chunk(v, nvalid);
+    }
+    return v;
+}
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) {
+    return __builtin_bit_cast(bf16x8_t, v);
+}
+
+// Workgroups are dispatched to the 8 XCDs of the chip round-robin by linear
+// workgroup id.  Remap so that each XCD receives a contiguous range of tile
+// indices (tiles next to each other share operand panels in that XCD's L2).
+__device__ __forceinline__ int xcd_contiguous(int bid, int nblocks) {
+    constexpr int NXCD = 8;
+    const int q = nblocks / NXCD;
+    const int r = nblocks % NXCD;
+    const int x = bid % NXCD;
+    const int i = bid / NXCD;
+    return x * q + (x < r ? x : r) + i;
+}
+
+// Output-tile coordinates of workgroup bid among tiles_r x tiles_c tiles.
+// map bit 0: skip the XCD remapping; bit 1: plain row-major order instead of
+// groups of GROUP tile-rows walked column by column.
+template <int GROUP>
+__device__ __forceinline__ void tile_coords(int bid, int nblocks, int tiles_c, int map,
+                                            int& tile_r, int& tile_c) {
+    const int t = (map & 1) ? bid : xcd_contiguous(bid, nblocks);
+    if (map & 2) {
+        tile_r = t / tiles_c;
+        tile_c = t - tile_r * tiles_c;
+        return;
+    }
+    const int tiles_r = nblocks / tiles_c;
+    const int group_size = GROUP * tiles_c;
+    const int g = t / group_size;
+    const int first_r = g * GROUP;
+    const int gsz = (tiles_r - first_r) < GROUP ? (tiles_r - first_r) : GROUP;
+    const int in_g = t - g * group_size;
+    tile_r = first_r + in_g % gsz;
+    tile_c = in_g / gsz;
+}
+
+}  // namespace espace

@@ -1,0 +1,443 @@
+// C ABI of the projected linear layer: argument validation, the choice of
+// kernel configuration for each product, and the launches.
+//
+// Every entry point validates all of its arguments before touching the device,
+// so an error status guarantees that nothing was enqueued or written.
+#include "espace.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+
+#include "kernels.hpp"
+
+namespace {
+
+using espace::GemmArgs;
+
+thread_local std::string g_last_error;
+
+espace_status fail(espace_status s, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
+espace_status ok() {
+    g_last_error.clear();
+    return ESPACE_OK;
+}
+
+constexpr int64_t kMaxDim = (int64_t)1 << 30;
+constexpr int kNumCUs = 256;          // MI355X; configurations are planned for it
+constexpr size_t kWsAlign = 256;
+
+size_t elem_size(espace_dtype dt) { return dt == ESPACE_BF16 ? 2 : 4; }
+int64_t ld_align(espace_dtype dt) { return dt == ESPACE_BF16 ? 8 : 4; }
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+size_t align_ws(size_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; }
+
+// ---- planning ---------------------------------------------------------------
+
+enum Kind { KIND_TILED = 0, KIND_SKINNY = 1, KIND_F32 = 2 };
+
+struct Plan {
+    int kind = KIND_F32;
+    int tile = 0;
+    int splits = 1;
+    size_t partial_bytes = 0;   // fp32 partial sums for splits > 1
+};
+
+int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+Plan plan_skinny(int R, int Cc, int D) {
+    Plan p;
+    p.kind = KIND_SKINNY;
+    const int nb2 = ceil_div(Cc, 32);
+    const int nb1 = ceil_div(Cc, 16);
+    const int steps = ceil_div(D, 32);
+    const int target = 2 * kNumCUs;
+    if (nb2 >= target) {
+        p.tile = espace::SKINNY_RG2_W4;
+    } else if (nb1 >= target) {
+        p.tile = espace::SKINNY_RG1_W4;
+    } else {
+        p.tile = espace::SKINNY_RG1_W8;
+        int s = ceil_div(target, nb1);
+        int smax = steps / 32;              // keep >= 4 steps per wave per split
+        if (smax < 1) smax = 1;
+        p.splits = s < smax ? s : smax;
+    }
+    if (p.splits > 1) p.partial_bytes = (size_t)p.splits * R * espace::splitk_ld(Cc) * sizeof(float);
+    return p;
+}
+
+struct TileShape { int tile, bm, bn, per_cu; double eff; };
+
+Plan plan_tiled(int R, int Cc, int D) {
+    // Estimated time of each tile shape (and depth split) from the number of
+    // rounds of workgroups the chip needs, the per-tile work and a relative
+    // efficiency of the tile shape; the cheapest wins.
+    static const TileShape shapes[] = {
+        {espace::TILE_256x256_W8T, 256, 256, 1, 1.00},
+        {espace::TILE_256x128, 256, 128, 1, 0.85},
+        {espace::TILE_128x256, 128, 256, 1, 0.85},
+        {espace::TILE_128x128, 128, 128, 2, 0.70},
+    };
+    const int ktiles = ceil_div(D, 64);
+    Plan best;
+    best.kind = KIND_TILED;
+    double best_cost = 1e300;
+    for (const TileShape& s : shapes) {
+        const int64_t tiles = (int64_t)ceil_div(R, s.bm) * ceil_div(Cc, s.bn);
+        for (int splits = 1; splits <= 4; ++splits) {
+            if (splits > 1 && ktiles / splits < 8) break;
+            const int64_t blocks = tiles * splits;
+            const int64_t slots = (int64_t)kNumCUs * s.per_cu;
+            const int64_t rounds = (blocks + slots - 1) / slots;
+            // a round runs per_cu blocks on every CU
+            const double per_round = (double)s.bm * s.bn * ceil_div(ktiles, splits) * s.per_cu;
+            double cost = rounds * per_round / s.eff;
+            // partial sums: written and read back once each (fp32), priced
+            // against the MFMA rate as bytes per flop of the machine balance
+            if (splits > 1) cost += 2.0 * splits * (double)R * Cc * 4.0 * 315.0 / (2.0 * 64 * kNumCUs);
+            if (cost < best_cost) {
+                best_cost = cost;
+                best.tile = s.tile;
+                best.splits = splits;
+            }
+        }
+    }
+    if (best.splits > 1) best.partial_bytes = (size_t)best.splits * R * espace::splitk_ld(Cc) * sizeof(float);
+    return best;
+}
+
+// Tuning override: ESPACE_TILE=256x256|256x128|128x256|128x128 and
+// ESPACE_SPLITK=<n> force the tiled configuration, ESPACE_KERNEL=1 selects
+// the register-staged kernel, ESPACE_VARIANT=<n> a kernel variant (read once
+// per process).
+struct Override { int tile = -1; int splits = 0; int kernel = 2; int variant = 1; };
+
+const Override& tile_override() {
+    static const Override o = [] {
+        Override r;
+        if (const char* t = std::getenv("ESPACE_TILE")) {
+            if (!std::strcmp(t, "256x256")) r.tile = espace::TILE_256x256;
+            else if (!std::strcmp(t, "256x128")) r.tile = espace::TILE_256x128;
+            else if (!std::strcmp(t, "128x256")) r.tile = espace::TILE_128x256;
+            else if (!std::strcmp(t, "128x128")) r.tile = espace::TILE_128x128;
+            else if (!std::strcmp(t, "256x256w8")) r.tile = espace::TILE_256x256_W8;
+            else if (!std::strcmp(t, "256x256w8t")) r.tile = espace::TILE_256x256_W8T;
+        }
+        if (const char* s = std::getenv("ESPACE_SPLITK")) r.splits = std::atoi(s);
+        if (const char* s = std::getenv("ESPACE_KERNEL")) r.kernel = std::atoi(s);
+        if (const char* s = std::getenv("ESPACE_VARIANT")) r.variant = std::atoi(s);
+        return r;
+    }();
+    return o;
+}
+
+Plan plan_tn(int64_t R, int64_t Cc, int64_t D, espace_dtype dt) {
+    if (dt == ESPACE_F32) return Plan{};
+    if (R <= 32) return plan_skinny((int)R, (int)Cc, (int)D);
+    Plan p = plan_tiled((int)R, (int)Cc, (int)D);
+    const Override& o = tile_override();
+    if (o.tile >= 0 || o.splits > 0) {
+        if (o.tile >= 0) p.tile = o.tile;
+        if (o.splits > 0) p.splits = o.splits;
+        if (p.splits > ceil_div(D, 64)) p.splits = ceil_div(D, 64);
+        p.partial_bytes = p.splits > 1 ? (size_t)p.splits * R * espace::splitk_ld(Cc) * sizeof(float) : 0;
+    }
+    return p;
+}
+
+int64_t z_ld(int64_t L, espace_dtype dt) { return round_up(L, dt == ESPACE_BF16 ? 64 : 32); }
+
+size_t z_bytes(int64_t N, int64_t L, espace_dtype dt) {
+    return align_ws((size_t)N * z_ld(L, dt) * elem_size(dt));
+}
+
+size_t ws_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int64_t N, espace_dtype dt) {
+    switch (op) {
+        case ESPACE_OP_FOLD: return M ? align_ws(plan_tn(M, L, K, dt).partial_bytes) : 0;
+        case ESPACE_OP_PROJECT: return N ? align_ws(plan_tn(N, L, K, dt).partial_bytes) : 0;
+        case ESPACE_OP_EXPAND: return (N && M) ? align_ws(plan_tn(N, M, L, dt).partial_bytes) : 0;
+        case ESPACE_OP_DENSE: return (N && M) ? align_ws(plan_tn(N, M, K, dt).partial_bytes) : 0;
+        case ESPACE_OP_PROJECTED_LINEAR: {
+            if (!N || !M) return 0;
+            size_t a = plan_tn(N, L, K, dt).partial_bytes;
+            size_t b = plan_tn(N, M, L, dt).partial_bytes;
+            return z_bytes(N, L, dt) + align_ws(a > b ? a : b);
+        }
+    }
+    return SIZE_MAX;
+}
+
+// ---- validation -------------------------------------------------------------
+
+struct Range { const char* name; uintptr_t lo, hi; };
+
+Range mat_range(const char* name, const void* p, int64_t rows, int64_t ld, espace_dtype dt) {
+    const uintptr_t lo = (uintptr_t)p;
+    return Range{name, lo, lo + (uintptr_t)(rows * ld) * elem_size(dt)};
+}
+
+espace_status check_dtype(espace_dtype dt) {
+    if (dt != ESPACE_F32 && dt != ESPACE_BF16)
+        return fail(ESPACE_ERR_DTYPE, "unknown dtype %d", (int)dt);
+    return ESPACE_OK;
+}
+
+espace_status check_dims(int64_t M, int64_t K, int64_t L, int64_t N, bool has_L) {
+    if (M < 0 || N < 0) return fail(ESPACE_ERR_SHAPE, "negative size (M=%lld, N=%lld)", (long long)M, (long long)N);
+    if (K < 1) return fail(ESPACE_ERR_SHAPE, "K must be >= 1 (got %lld)", (long long)K);
+    if (M > kMaxDim || N > kMaxDim || K > kMaxDim)
+        return fail(ESPACE_ERR_SHAPE, "size above 2^30");
+    if (has_L && (L < 1 || L > K))
+        return fail(ESPACE_ERR_SHAPE, "need 1 <= L <= K (L=%lld, K=%lld)", (long long)L, (long long)K);
+    return ESPACE_OK;
+}
+
+espace_status check_mat(const char* name, const void* p, int64_t rows, int64_t cols, int64_t ld,
+                        espace_dtype dt) {
+    if (!p) return fail(ESPACE_ERR_NULL, "%s is NULL", name);
+    if (ld < cols || ld > kMaxDim * 4)
+        return fail(ESPACE_ERR_SHAPE, "%s: leading dimension %lld < %lld columns", name,
+                    (long long)ld, (long long)cols);
+    if (ld % ld_align(dt))
+        return fail(ESPACE_ERR_ALIGN, "%s: leading dimension %lld not a multiple of %lld elements",
+                    name, (long long)ld, (long long)ld_align(dt));
+    if ((uintptr_t)p % 16)
+        return fail(ESPACE_ERR_ALIGN, "%s: pointer not 16-byte aligned", name);
+    if (rows * ld > ((int64_t)1 << 40)) return fail(ESPACE_ERR_SHAPE, "%s too large", name);
+    return ESPACE_OK;
+}
+
+bool overlaps(const Range& a, const Range& b) { return a.lo < b.hi && b.lo < a.hi; }
+
+espace_status check_alias(const Range& out, const Range* ins, int n) {
+    for (int i = 0; i < n; ++i)
+        if (ins[i].lo != ins[i].hi && overlaps(out, ins[i]))
+            return fail(ESPACE_ERR_ALIAS, "output %s overlaps %s", out.name, ins[i].name);
+    return ESPACE_OK;
+}
+
+espace_status check_workspace(void* ws, size_t have, size_t need) {
+    if (need == 0) return ESPACE_OK;
+    if (!ws) return fail(ESPACE_ERR_WORKSPACE, "workspace of %zu bytes needed, got NULL", need);
+    if (have < need) return fail(ESPACE_ERR_WORKSPACE, "workspace of %zu bytes needed, got %zu", need, have);
+    if ((uintptr_t)ws % kWsAlign) return fail(ESPACE_ERR_ALIGN, "workspace not 256-byte aligned");
+    return ESPACE_OK;
+}
+
+std::mutex g_dev_mu;
+int g_dev_ok[64];   // 0 unknown, 1 gfx950, -1 other
+
+espace_status check_device() {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= 64) return fail(ESPACE_ERR_DEVICE, "device id %d out of range", dev);
+    std::lock_guard<std::mutex> lk(g_dev_mu);
+    if (g_dev_ok[dev] == 0) {
+        hipDeviceProp_t prop;
+        e = hipGetDeviceProperties(&prop, dev);
+        if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
+        g_dev_ok[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
+    }
+    if (g_dev_ok[dev] != 1) return fail(ESPACE_ERR_DEVICE, "device %d is not gfx950", dev);
+    return ESPACE_OK;
+}
+
+#define ESPACE_TRY(x)                       \
+    do {                                    \
+        espace_status _s = (x);             \
+        if (_s != ESPACE_OK) return _s;     \
+    } while (0)
+
+// ---- launch -----------------------------------------------------------------
+
+espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
+                     int64_t R, int64_t Cc, int64_t D, espace_dtype dt, void* partial,
+                     hipStream_t stream) {
+    hipError_t e;
+    if (dt == ESPACE_F32) {
+        e = espace::launch_gemm_tn_f32((const float*)A, lda, (const float*)B, ldb, (float*)C, ldc,
+                                       (int)R, (int)Cc, (int)D, stream);
+    } else {
+        const Plan p = plan_tn(R, Cc, D, dt);
+        GemmArgs g;
+        g.A = (const uint16_t*)A;
+        g.lda = lda;
+        g.B = (const uint16_t*)B;
+        g.ldb = ldb;
+        g.C = C;
+        g.ldc = ldc;
+        g.R = (int)R;
+        g.Cc = (int)Cc;
+        g.D = (int)D;
+        g.c_f32 = 0;
+        g.tile = p.tile;
+        g.splits = p.splits;
+        g.partial = (float*)partial;
+        g.variant = tile_override().variant;
+        e = p.kind == KIND_SKINNY ? espace::launch_skinny_tn_bf16(g, stream)
+                                  : (tile_override().kernel == 1 ? espace::launch_gemm_tn_bf16(g, stream)
+                                     : tile_override().kernel == 3 ? espace::launch_gemm_tn_bf16_pp(g, stream)
+                                                                   : espace::launch_gemm_tn_bf16_v2(g, stream));
+    }
+    if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
+    return ESPACE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int espace_abi_version(void) { return ESPACE_ABI_VERSION; }
+
+const char* espace_last_error(void) { return g_last_error.c_str(); }
+
+const char* espace_status_string(espace_status s) {
+    switch (s) {
+        case ESPACE_OK: return "ok";
+        case ESPACE_ERR_NULL: return "null pointer";
+        case ESPACE_ERR_SHAPE: return "invalid shape";
+        case ESPACE_ERR_ALIGN: return "misaligned pointer or leading dimension";
+        case ESPACE_ERR_DTYPE: return "invalid dtype";
+        case ESPACE_ERR_ALIAS: return "output overlaps an input";
+        case ESPACE_ERR_WORKSPACE: return "workspace missing or too small";
+        case ESPACE_ERR_HIP: return "HIP runtime error";
+        case ESPACE_ERR_DEVICE: return "unsupported device";
+    }
+    return "unknown status";
+}
+
+size_t espace_workspace_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int64_t N,
+                              espace_dtype dt) {
+    if (dt != ESPACE_F32 && dt != ESPACE_BF16) return SIZE_MAX;
+    const bool has_L = op != ESPACE_OP_DENSE;
+    int64_t Kc = K;
+    if (op == ESPACE_OP_EXPAND) Kc = L;       // expand has no K; L bounds itself
+    if (M < 0 || N < 0 || Kc < 1 || M > kMaxDim || N > kMaxDim || Kc > kMaxDim) return SIZE_MAX;
+    if (has_L && (L < 1 || L > Kc)) return SIZE_MAX;
+    if (op < ESPACE_OP_FOLD || op > ESPACE_OP_DENSE) return SIZE_MAX;
+    return ws_bytes(op, M, K, L, N, dt);
+}
+
+espace_status espace_fold_weights(const void* W, int64_t ldw, const void* Pt, int64_t ldp,
+                                  void* Wf, int64_t ldwf, int64_t M, int64_t K, int64_t L,
+                                  espace_dtype dt, void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream) {
+    ESPACE_TRY(check_dtype(dt));
+    ESPACE_TRY(check_dims(M, K, L, 0, true));
+    if (M == 0) return ok();
+    ESPACE_TRY(check_mat("W", W, M, K, ldw, dt));
+    ESPACE_TRY(check_mat("Pt", Pt, L, K, ldp, dt));
+    ESPACE_TRY(check_mat("Wf", Wf, M, L, ldwf, dt));
+    const size_t need = ws_bytes(ESPACE_OP_FOLD, M, K, L, 0, dt);
+    ESPACE_TRY(check_workspace(workspace, workspace_bytes, need));
+    const Range ins[] = {mat_range("W", W, M, ldw, dt), mat_range("Pt", Pt, L, ldp, dt),
+                         Range{"workspace", (uintptr_t)workspace, (uintptr_t)workspace + (need ? workspace_bytes : 0)}};
+    ESPACE_TRY(check_alias(mat_range("Wf", Wf, M, ldwf, dt), ins, 3));
+    ESPACE_TRY(check_device());
+    ESPACE_TRY(run_tn(W, ldw, Pt, ldp, Wf, ldwf, M, L, K, dt, workspace, stream));
+    return ok();
+}
+
+espace_status espace_project(const void* Pt, int64_t ldp, const void* X, int64_t ldx, void* Z,
+                             int64_t ldz, int64_t K, int64_t L, int64_t N, espace_dtype dt,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    ESPACE_TRY(check_dtype(dt));
+    ESPACE_TRY(check_dims(0, K, L, N, true));
+    if (N == 0) return ok();
+    ESPACE_TRY(check_mat("Pt", Pt, L, K, ldp, dt));
+    ESPACE_TRY(check_mat("X", X, N, K, ldx, dt));
+    ESPACE_TRY(check_mat("Z", Z, N, L, ldz, dt));
+    const size_t need = ws_bytes(ESPACE_OP_PROJECT, 0, K, L, N, dt);
+    ESPACE_TRY(check_workspace(workspace, workspace_bytes, need));
+    const Range ins[] = {mat_range("Pt", Pt, L, ldp, dt), mat_range("X", X, N, ldx, dt),
+                         Range{"workspace", (uintptr_t)workspace, (uintptr_t)workspace + (need ? workspace_bytes : 0)}};
+    ESPACE_TRY(check_alias(mat_range("Z", Z, N, ldz, dt), ins, 3));
+    ESPACE_TRY(check_device());
+    ESPACE_TRY(run_tn(X, ldx, Pt, ldp, Z, ldz, N, L, K, dt, workspace, stream));
+    return ok();
+}
+
+espace_status espace_expand(const void* Z, int64_t ldz, const void* Wf, int64_t ldwf, void* Y,
+                            int64_t ldy, int64_t M, int64_t L, int64_t N, espace_dtype dt,
+                            void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    ESPACE_TRY(check_dtype(dt));
+    ESPACE_TRY(check_dims(M, L, L, N, true));
+    if (M == 0 || N == 0) return ok();
+    ESPACE_TRY(check_mat("Z", Z, N, L, ldz, dt));
+    ESPACE_TRY(check_mat("Wf", Wf, M, L, ldwf, dt));
+    ESPACE_TRY(check_mat("Y", Y, N, M, ldy, dt));
+    const size_t need = ws_bytes(ESPACE_OP_EXPAND, M, L, L, N, dt);
+    ESPACE_TRY(check_workspace(workspace, workspace_bytes, need));
+    const Range ins[] = {mat_range("Z", Z, N, ldz, dt), mat_range("Wf", Wf, M, ldwf, dt),
+                         Range{"workspace", (uintptr_t)workspace, (uintptr_t)workspace + (need ? workspace_bytes : 0)}};
+    ESPACE_TRY(check_alias(mat_range("Y", Y, N, ldy, dt), ins, 3));
+    ESPACE_TRY(check_device());
+    ESPACE_TRY(run_tn(Z, ldz, Wf, ldwf, Y, ldy, N, M, L, dt, workspace, stream));
+    return ok();
+}
+
+espace_status espace_projected_linear(const void* X, int64_t ldx, const void* Pt, int64_t ldp,
+                                      const void* Wf, int64_t ldwf, void* Y, int64_t ldy,
+                                      int64_t M, int64_t K, int64_t L, int64_t N, espace_dtype dt,
+                                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    ESPACE_TRY(check_dtype(dt));
+    ESPACE_TRY(check_dims(M, K, L, N, true));
+    if (M == 0 || N == 0) return ok();
+    ESPACE_TRY(check_mat("X", X, N, K, ldx, dt));
+    ESPACE_TRY(check_mat("Pt", Pt, L, K, ldp, dt));
+    ESPACE_TRY(check_mat("Wf", Wf, M, L, ldwf, dt));
+    ESPACE_TRY(check_mat("Y", Y, N, M, ldy, dt));
+    const size_t need = ws_bytes(ESPACE_OP_PROJECTED_LINEAR, M, K, L, N, dt);
+    ESPACE_TRY(check_workspace(workspace, workspace_bytes, need));
+    const Range ws{"workspace", (uintptr_t)workspace, (uintptr_t)workspace + workspace_bytes};
+    const Range ins[] = {mat_range("X", X, N, ldx, dt), mat_range("Pt", Pt, L, ldp, dt),
+                         mat_range("Wf", Wf, M, ldwf, dt), ws};
+    ESPACE_TRY(check_alias(mat_range("Y", Y, N, ldy, dt), ins, 4));
+    // the workspace holds Z and must not overlap the inputs either
+    const Range wsr{"workspace", ws.lo, ws.lo + need};
+    ESPACE_TRY(check_alias(wsr, ins, 3));
+    ESPACE_TRY(check_device());
+    const int64_t ldz = z_ld(L, dt);
+    void* Z = workspace;
+    void* partial = (char*)workspace + z_bytes(N, L, dt);
+    ESPACE_TRY(run_tn(X, ldx, Pt, ldp, Z, ldz, N, L, K, dt, partial, stream));
+    ESPACE_TRY(run_tn(Z, ldz, Wf, ldwf, Y, ldy, N, M, L, dt, partial, stream));
+    return ok();
+}
+
+espace_status espace_dense_linear(const void* X, int64_t ldx, const void* W, int64_t ldw, void* Y,
+                                  int64_t ldy, int64_t M, int64_t K, int64_t N, espace_dtype dt,
+                                  void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    ESPACE_TRY(check_dtype(dt));
+    ESPACE_TRY(check_dims(M, K, 1, N, false));
+    if (M == 0 || N == 0) return ok();
+    ESPACE_TRY(check_mat("X", X, N, K, ldx, dt));
+    ESPACE_TRY(check_mat("W", W, M, K, ldw, dt));
+    ESPACE_TRY(check_mat("Y", Y, N, M, ldy, dt));
+    const size_t need = ws_bytes(ESPACE_OP_DENSE, M, K, 0, N, dt);
+    ESPACE_TRY(check_workspace(workspace, workspace_bytes, need));
+    const Range ins[] = {mat_range("X", X, N, ldx, dt), mat_range("W", W, M, ldw, dt),
+                         Range{"workspace", (uintptr_t)workspace, (uintptr_t)workspace + (need ? workspace_bytes : 0)}};
+    ESPACE_TRY(check_alias(mat_range("Y", Y, N, ldy, dt), ins, 3));
+    ESPACE_TRY(check_device());
+    ESPACE_TRY(run_tn(X, ldx, W, ldw, Y, ldy, N, M, K, dt, workspace, stream));
+    return ok();
+}
+
+}  // extern "C"

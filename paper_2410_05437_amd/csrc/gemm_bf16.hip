@@ -1,0 +1,277 @@
+// Tiled bfloat16 GEMM on gfx950 matrix cores, "TN" form:
+//
+//     C[r][c] = sum_k A[r][k] * B[c][k]        (fp32 accumulation)
+//
+// A [R][D] and B [Cc][D] are row-major with the reduced dimension contiguous,
+// which is the storage of every product of the projected linear layer
+// (fold: A=W, B=Pt; project: A=X, B=Pt; expand: A=Z, B=Wf; dense: A=X, B=W).
+//
+// Block tile BM x BN, depth step BK = 64.  Operand tiles are staged in LDS,
+// double-buffered: the global loads of step t+1 are issued before the MFMAs of
+// step t and written to the other LDS buffer afterwards.  LDS rows are 128 B
+// (64 bf16 = 8 chunks of 16 B); chunk c of row r is stored at chunk position
+// c ^ (r & 7), so the 16-byte reads of 8 consecutive lanes (8 consecutive rows,
+// same logical chunk) hit 8 different bank groups.
+// Each wave owns a (BM/WM) x (BN/WN) sub-tile computed with
+// v_mfma_f32_32x32x16_bf16.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace espace {
+
+namespace {
+
+constexpr int BK = 64;
+constexpr int CHUNKS = BK / 8;   // 16-byte chunks per tile row
+
+template <int BM, int BN, int WM, int WN>
+struct TileCfg {
+    static constexpr int NT = WM * WN * 64;
+    static constexpr int WTM = BM / WM;     // rows per wave
+    static constexpr int WTN = BN / WN;     // cols per wave
+    static constexpr int TM = WTM / 32;     // 32x32 MFMA tiles per wave (rows)
+    static constexpr int TN = WTN / 32;
+    static constexpr int A_CHUNKS = BM * CHUNKS / NT;   // 16-B loads per thread
+    static constexpr int B_CHUNKS = BN * CHUNKS / NT;
+    static_assert(BM % (32 * WM) == 0 && BN % (32 * WN) == 0, "wave tiling");
+    static_assert((BM * CHUNKS) % NT == 0 && (BN * CHUNKS) % NT == 0, "load tiling");
+    static constexpr int STAGE = (BM + BN) * CHUNKS;    // u32x4 per LDS stage
+};
+
+template <class T>
+__device__ __forceinline__ void load_tile(u32x4_t (&ra)[T::A_CHUNKS], u32x4_t (&rb)[T::B_CHUNKS],
+                                          const uint16_t* __restrict__ A, int64_t lda,
+                                          const uint16_t* __restrict__ B, int64_t ldb,
+                                          int row0, int col0, int R, int Cc, int k0, int D,
+                                          bool full) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < T::A_CHUNKS; ++i) {
+        const int q = tid + i * T::NT;
+        const int r = q / CHUNKS;
+        const int c = q % CHUNKS;
+        int gr = row0 + r;
+        gr = gr < R ? gr : R - 1;
+        const uint16_t* p = A + (int64_t)gr * lda;
+        const int k = k0 + c * 8;
+        ra[i] = full ? *reinterpret_cast<const u32x4_t*>(p + k) : load_chunk_masked(p, k, D);
+    }
+#pragma unroll
+    for (int i = 0; i < T::B_CHUNKS; ++i) {
+        const int q = tid + i * T::NT;
+        const int r = q / CHUNKS;
+        const int c = q % CHUNKS;
+        int gc = col0 + r;
+        gc = gc < Cc ? gc : Cc - 1;
+        const uint16_t* p = B + (int64_t)gc * ldb;
+        const int k = k0 + c * 8;
+        rb[i] = full ? *reinterpret_cast<const u32x4_t*>(p + k) : load_chunk_masked(p, k, D);
+    }
+}
+
+template <class T, int BM>
+__device__ __forceinline__ void store_tile(u32x4_t* stage, const u32x4_t (&ra)[T::A_CHUNKS],
+                                           const u32x4_t (&rb)[T::B_CHUNKS]) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < T::A_CHUNKS; ++i) {
+        const int q = tid + i * T::NT;
+        const int r = q / CHUNKS;
+        const int c = q % CHUNKS;
+        stage[r * CHUNKS + (c ^ (r & 7))] = ra[i];
+    }
+    u32x4_t* sb = stage + BM * CHUNKS;
+#pragma unroll
+    for (int i = 0; i < T::B_CHUNKS; ++i) {
+        const int q = tid + i * T::NT;
+        const int r = q / CHUNKS;
+        const int c = q % CHUNKS;
+        sb[r * CHUNKS + (c ^ (r & 7))] = rb[i];
+    }
+}
+
+template <int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(WM * WN * 64)
+void gemm_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
+                         const uint16_t* __restrict__ B, int64_t ldb,
+                         void* __restrict__ Cout, int64_t ldc,
+                         int R, int Cc, int D, int tiles_c, int ktiles_per_split,
+                         int out_f32, int64_t split_stride) {
+    using T = TileCfg<BM, BN, WM, WN>;
+    __shared__ u32x4_t smem[2 * T::STAGE];
+
+    // tile coordinates: XCD-contiguous, then groups of 4 tile-rows walked
+    // column by column
+    const int nblocks = gridDim.x;
+    const int t = xcd_contiguous(blockIdx.x, nblocks);
+    const int tiles_r = nblocks / tiles_c;
+    constexpr int GROUP = 4;
+    const int group_size = GROUP * tiles_c;
+    const int g = t / group_size;
+    const int first_r = g * GROUP;
+    const int gsz = (tiles_r - first_r) < GROUP ? (tiles_r - first_r) : GROUP;
+    const int in_g = t - g * group_size;
+    const int tile_r = first_r + in_g % gsz;
+    const int tile_c = in_g / gsz;
+    const int row0 = tile_r * BM;
+    const int col0 = tile_c * BN;
+
+    const int ktiles = (D + BK - 1) / BK;
+    const int kt_begin = blockIdx.y * ktiles_per_split;
+    int kt_end = kt_begin + ktiles_per_split;
+    kt_end = kt_end < ktiles ? kt_end : ktiles;
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int wr = wave / WN;
+    const int wc = wave % WN;
+    const int wrow0 = wr * T::WTM;
+    const int wcol0 = wc * T::WTN;
+
+    f32x16_t acc[T::TM][T::TN];
+#pragma unroll
+    for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    u32x4_t ra[T::A_CHUNKS];
+    u32x4_t rb[T::B_CHUNKS];
+
+    if (kt_begin < kt_end) {
+        load_tile<T>(ra, rb, A, lda, B, ldb, row0, col0, R, Cc, kt_begin * BK, D,
+                     (kt_begin + 1) * BK <= D);
+        store_tile<T, BM>(smem, ra, rb);
+    }
+    __syncthreads();
+
+    const int lrow = lane & 31;       // row (A) / column (B) inside a 32x32 MFMA tile
+    const int lk = lane >> 5;         // which 8-element half of the 16-deep step
+
+    for (int kt = kt_begin; kt < kt_end; ++kt) {
+        const int cur = (kt - kt_begin) & 1;
+        const bool more = kt + 1 < kt_end;
+        if (more)
+            load_tile<T>(ra, rb, A, lda, B, ldb, row0, col0, R, Cc, (kt + 1) * BK, D,
+                         (kt + 2) * BK <= D);
+        const u32x4_t* sa = smem + cur * T::STAGE;
+        const u32x4_t* sb = sa + BM * CHUNKS;
+#pragma unroll
+        for (int s = 0; s < BK / 16; ++s) {
+            const int c = 2 * s + lk;
+            bf16x8_t fa[T::TM];
+            bf16x8_t fb[T::TN];
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i) {
+                const int r = wrow0 + i * 32 + lrow;
+                fa[i] = as_bf16x8(sa[r * CHUNKS + (c ^ (r & 7))]);
+            }
+#pragma unroll
+            for (int j = 0; j < T::TN; ++j) {
+                const int r = wcol0 + j * 32 + lrow;
+                fb[j] = as_bf16x8(sb[r * CHUNKS + (c ^ (r & 7))]);
+            }
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+                for (int j = 0; j < T::TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        }
+        if (more) store_tile<T, BM>(smem + (cur ^ 1) * T::STAGE, ra, rb);
+        __syncthreads();
+    }
+
+    // epilogue: accumulator v of lane l holds row 8*(v/4) + 4*(l/32) + v%4 and
+    // column l%32 of its 32x32 tile
+#pragma unroll
+    for (int i = 0; i < T::TM; ++i) {
+#pragma unroll
+        for (int j = 0; j < T::TN; ++j) {
+            const int c = col0 + wcol0 + j * 32 + lrow;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int r = row0 + wrow0 + i * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
+                if (r < R && c < Cc) {
+                    if (out_f32) {
+                        float* C = reinterpret_cast<float*>(Cout) + blockIdx.y * split_stride;
+                        C[(int64_t)r * ldc + c] = acc[i][j][v];
+                    } else {
+                        uint16_t* C = reinterpret_cast<uint16_t*>(Cout);
+                        C[(int64_t)r * ldc + c] = (uint16_t)bf16_rne(acc[i][j][v]);
+                    }
+                }
+            }
+        }
+    }
+}
+
+// Sum of S fp32 partial results -> bf16 or fp32 output.
+__global__ __launch_bounds__(256)
+void splitk_reduce_kernel(const float* __restrict__ P, int S, int64_t split_stride, int64_t ldp,
+                          void* __restrict__ Cout, int64_t ldc, int R, int Cc, int out_bf16) {
+    const int64_t total = (int64_t)R * Cc;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = e / Cc;
+        const int64_t c = e - r * Cc;
+        float s = 0.f;
+        for (int i = 0; i < S; ++i) s += P[i * split_stride + r * ldp + c];
+        if (out_bf16)
+            reinterpret_cast<uint16_t*>(Cout)[r * ldc + c] = (uint16_t)bf16_rne(s);
+        else
+            reinterpret_cast<float*>(Cout)[r * ldc + c] = s;
+    }
+}
+
+template <int BM, int BN, int WM, int WN>
+hipError_t launch_cfg(const GemmArgs& g, hipStream_t stream) {
+    const int tiles_r = (g.R + BM - 1) / BM;
+    const int tiles_c = (g.Cc + BN - 1) / BN;
+    const int ktiles = (g.D + BK - 1) / BK;
+    const int S = g.splits;
+    const int ktps = (ktiles + S - 1) / S;
+    dim3 grid(tiles_r * tiles_c, S);
+    dim3 block(WM * WN * 64);
+    if (S == 1) {
+        hipLaunchKernelGGL((gemm_tn_bf16_kernel<BM, BN, WM, WN>), grid, block, 0, stream,
+                           g.A, g.lda, g.B, g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c, ktps,
+                           g.c_f32, (int64_t)0);
+        return hipGetLastError();
+    }
+    const int64_t ldp = splitk_ld(g.Cc);
+    const int64_t split_stride = (int64_t)g.R * ldp;
+    hipLaunchKernelGGL((gemm_tn_bf16_kernel<BM, BN, WM, WN>), grid, block, 0, stream,
+                       g.A, g.lda, g.B, g.ldb, (void*)g.partial, ldp, g.R, g.Cc, g.D, tiles_c,
+                       ktps, 1, split_stride);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_splitk_reduce(g.partial, S, split_stride, ldp, g.C, g.ldc, g.R, g.Cc,
+                                g.c_f32 ? 0 : 1, stream);
+}
+
+}  // namespace
+
+hipError_t launch_splitk_reduce(const float* P, int S, int64_t split_stride, int64_t ldp,
+                                void* C, int64_t ldc, int R, int Cc, int out_bf16,
+                                hipStream_t stream) {
+    const int64_t total = (int64_t)R * Cc;
+    int64_t nb = (total + 255) / 256;
+    if (nb > 8192) nb = 8192;
+    if (nb < 1) nb = 1;
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)nb), dim3(256), 0, stream,
+                       P, S, split_stride, ldp, C, ldc, R, Cc, out_bf16);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_tn_bf16(const GemmArgs& g, hipStream_t stream) {
+    switch (g.tile) {
+        case TILE_256x256: return launch_cfg<256, 256, 2, 4>(g, stream);
+        case TILE_256x128: return launch_cfg<256, 128, 2, 2>(g, stream);
+        case TILE_128x256: return launch_cfg<128, 256, 2, 2>(g, stream);
+        case TILE_128x128: return launch_cfg<128, 128, 2, 2>(g, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace espace

@@ -1,0 +1,366 @@
+// Tiled bfloat16 "TN" GEMM for gfx950, direct-to-LDS multi-stage pipeline:
+//
+//     C[r][c] = sum_k A[r][k] * B[c][k]        (fp32 accumulation)
+//
+// A [R][D] and B [Cc][D] row-major with the reduced dimension contiguous.
+//
+// Block tile BM x BN, depth step BK (32 or 64), one wave per SIMD (WM x WN
+// waves), each wave owning a (BM/WM) x (BN/WN) sub-tile of 32x32
+// v_mfma_f32_32x32x16_bf16 blocks held in accumulation registers.
+//
+// Data movement:
+//  * global -> LDS with global_load_lds_dwordx4: each wave instruction moves
+//    64 x 16 B into 1 KB of contiguous LDS (1024/(2*BK) tile rows).  The
+//    swizzle is applied on the global side: the lane that writes chunk slot p
+//    of row r fetches logical chunk p ^ swz(r), so chunk c of row r lives at
+//    slot c ^ swz(r).  swz(r) spreads the 16 rows read by 16 consecutive lanes
+//    over all 64 LDS banks, so fragment reads are conflict free.
+//  * STAGES LDS stages; step t+STAGES-1 is loaded while step t is computed,
+//    and each wave waits only for the oldest of its outstanding steps
+//    (s_waitcnt vmcnt(N)) before the single barrier of a step.
+//  * LDS -> registers with ds_read_b128 (8 bf16 of one row per lane),
+//    double-buffered in registers across the 16-deep sub-steps; the MFMAs of
+//    a step's last sub-step are issued after the barrier and overlap it.
+//  * epilogue: the MFMA is issued with the B rows as its first operand, so
+//    each lane ends with 4 consecutive output columns; they are packed to
+//    bf16, staged through LDS and written back as 16-byte row segments.
+// The depth tail (D not a multiple of BK) is loaded through registers with
+// the out-of-range elements zeroed.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace espace {
+
+namespace {
+
+template <int BM, int BN, int WM, int WN, int BK, int STAGES>
+struct Cfg {
+    static constexpr int NW = WM * WN;
+    static constexpr int WTM = BM / WM;
+    static constexpr int WTN = BN / WN;
+    static constexpr int TM = WTM / 32;
+    static constexpr int TN = WTN / 32;
+    static constexpr int ROWB = BK * 2;                   // bytes per LDS tile row
+    static constexpr int CPR = BK / 8;                    // 16-byte chunks per row
+    static constexpr int RPL = 1024 / ROWB;               // rows per 1 KB wave-load
+    static constexpr int SWZ_SH = ROWB == 128 ? 1 : 2;    // rows sharing a 256-B bank line
+    static constexpr int NSUB = BK / 16;                  // MFMA sub-steps per step
+    static constexpr int STAGE = (BM + BN) * ROWB;        // bytes per LDS stage
+    static constexpr int NLOAD = (BM + BN) / RPL;         // wave-loads per stage
+    static constexpr int LPW = NLOAD / NW;                // wave-loads per wave per stage
+    static constexpr int EPI_LD = WTN * 2 + 16;           // epilogue row stride (bytes)
+    static constexpr int EPI = NW * WTM * EPI_LD;
+    static constexpr int SMEM = (STAGES * STAGE > EPI) ? STAGES * STAGE : EPI;
+    static_assert(NLOAD % NW == 0, "loads per wave");
+    static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
+    static_assert(BK == 32 || BK == 64, "depth step");
+    static_assert(LPW * (STAGES - 1) < 64, "vmcnt range");
+};
+
+template <class T>
+__device__ __forceinline__ int swz(int r) { return (r >> T::SWZ_SH) & (T::CPR - 1); }
+
+// s_waitcnt vmcnt(n) leaving the other counters free (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
+// Wait until at most n of this wave's steps of loads are outstanding
+// (0 <= n <= STAGES-1 <= 3).
+template <class T>
+__device__ __forceinline__ void wait_steps(int n) {
+    if (n <= 0) wait_vmcnt<0>();
+    else if (n == 1) wait_vmcnt<T::LPW>();
+    else if (n == 2) wait_vmcnt<2 * T::LPW>();
+    else wait_vmcnt<3 * T::LPW>();
+}
+
+// Issue the loads of depth step kt into LDS stage st.
+template <class T, int BM>
+__device__ __forceinline__ void issue(unsigned char* smem, const uint16_t* __restrict__ A,
+                                      const uint16_t* __restrict__ B, const int* off, int wave,
+                                      int lane, int kt, int st, int D) {
+    const int k0 = kt * (T::ROWB / 2);
+    unsigned char* sbase = smem + st * T::STAGE;
+    if (k0 + T::ROWB / 2 <= D) {
+#pragma unroll
+        for (int j = 0; j < T::LPW; ++j) {
+            const int q = wave + j * T::NW;
+            const uint16_t* base = (q * T::RPL < BM) ? A : B;
+            __builtin_amdgcn_global_load_lds(base + off[j] + k0, sbase + q * 1024, 16, 0, 0);
+        }
+    } else {
+        // depth tail: through registers, zeroing elements at or beyond D
+#pragma unroll
+        for (int j = 0; j < T::LPW; ++j) {
+            const int q = wave + j * T::NW;
+            const bool isA = q * T::RPL < BM;
+            const uint16_t* base = isA ? A : B;
+            const int rr = q * T::RPL + lane / T::CPR - (isA ? 0 : BM);
+            const int lc = (lane % T::CPR) ^ swz<T>(rr);
+            const uint16_t* rowp = base + off[j] - lc * 8;
+            const u32x4_t v = load_chunk_masked(rowp, k0 + lc * 8, D);
+            *reinterpret_cast<u32x4_t*>(sbase + q * 1024 + lane * 16) = v;
+        }
+    }
+}
+
+// Read the fragments of 16-deep sub-step s of stage st.
+template <class T>
+__device__ __forceinline__ void read_frags(const unsigned char* smem, bf16x8_t* fa, bf16x8_t* fb,
+                                           int st, int s, int a_off, int b_off, int lh, int sw) {
+    const unsigned char* sbase = smem + st * T::STAGE;
+    const int pc = ((2 * s + lh) ^ sw) * 16;
+#pragma unroll
+    for (int i = 0; i < T::TM; ++i)
+        fa[i] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(sbase + a_off + i * 32 * T::ROWB + pc));
+#pragma unroll
+    for (int j = 0; j < T::TN; ++j)
+        fb[j] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(sbase + b_off + j * 32 * T::ROWB + pc));
+}
+
+// The MFMA is issued with the B rows as its first operand: the result of
+// block (i, j) holds output rows in lanes and output columns in registers.
+template <int TM, int TN>
+__device__ __forceinline__ void mfmas(f32x16_t (*acc)[TN], const bf16x8_t* fa, const bf16x8_t* fb) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+}
+
+// Matrices handed to this kernel hold fewer than 2^31 elements, so per-lane
+// load offsets fit in 32 bits (the launcher checks).
+template <int BM, int BN, int WM, int WN, int BK, int STAGES, bool OUT_F32>
+__global__ __launch_bounds__(WM * WN * 64, 1)
+void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
+                            const uint16_t* __restrict__ B, int64_t ldb,
+                            void* __restrict__ Cout, int64_t ldc,
+                            int R, int Cc, int D, int tiles_c, int ktiles_per_split,
+                            int64_t split_stride, int map) {
+    using T = Cfg<BM, BN, WM, WN, BK, STAGES>;
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[T::SMEM];
+
+    // XCD-contiguous tile order, then groups of 4 tile-rows walked by column
+    int tile_r, tile_c;
+    tile_coords<4>(blockIdx.x, gridDim.x, tiles_c, map, tile_r, tile_c);
+    const int row0 = tile_r * BM;
+    const int col0 = tile_c * BN;
+
+    const int ktiles = (D + BK - 1) / BK;
+    const int kt0 = blockIdx.y * ktiles_per_split;
+    int kt_end = kt0 + ktiles_per_split;
+    kt_end = kt_end < ktiles ? kt_end : ktiles;
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wrow0 = (wave / WN) * T::WTM;
+    const int wcol0 = (wave % WN) * T::WTN;
+
+    // wave-load j of this wave covers rows RPL*q .. RPL*q+RPL-1 of the
+    // combined A|B tile, q = wave + j*NW; off[j] is this lane's element
+    // offset from A or B
+    int off[T::LPW];
+#pragma unroll
+    for (int j = 0; j < T::LPW; ++j) {
+        const int q = wave + j * T::NW;
+        const int rl = q * T::RPL + lane / T::CPR;
+        const bool isA = q * T::RPL < BM;
+        const int rr = isA ? rl : rl - BM;
+        const int lc = (lane % T::CPR) ^ swz<T>(rr);
+        int gr = (isA ? row0 : col0) + rr;
+        const int lim = isA ? R : Cc;
+        gr = gr < lim ? gr : lim - 1;
+        off[j] = gr * (int)(isA ? lda : ldb) + lc * 8;
+    }
+
+    const int lr = lane & 31;
+    const int lh = lane >> 5;
+    const int sw = swz<T>(lr);                    // rows of a fragment are lr mod 32
+    const int a_off = (wrow0 + lr) * T::ROWB;
+    const int b_off = (BM + wcol0 + lr) * T::ROWB;
+
+    f32x16_t acc[T::TM][T::TN];
+#pragma unroll
+    for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    bf16x8_t fa0[T::TM], fa1[T::TM];
+    bf16x8_t fb0[T::TN], fb1[T::TN];
+
+    if (kt0 < kt_end) {
+        // prologue: steps kt0 .. kt0+STAGES-1 fill the stages
+#pragma unroll
+        for (int p = 0; p < STAGES; ++p)
+            if (kt0 + p < kt_end) issue<T, BM>(smem, A, B, off, wave, lane, kt0 + p, p, D);
+        {
+            const int newer = (kt_end - kt0 - 1) < (STAGES - 1) ? (kt_end - kt0 - 1) : (STAGES - 1);
+            wait_steps<T>(newer);
+        }
+        __builtin_amdgcn_s_barrier();
+        read_frags<T>(smem, fa0, fb0, 0, 0, a_off, b_off, lh, sw);
+        int st = 0;                                // stage of step kt
+        for (int kt = kt0; kt < kt_end; ++kt) {
+#pragma unroll
+            for (int s = 0; s + 1 < T::NSUB; ++s) {
+                if (s & 1) {
+                    read_frags<T>(smem, fa0, fb0, st, s + 1, a_off, b_off, lh, sw);
+                    mfmas<T::TM, T::TN>(acc, fa1, fb1);
+                } else {
+                    read_frags<T>(smem, fa1, fb1, st, s + 1, a_off, b_off, lh, sw);
+                    mfmas<T::TM, T::TN>(acc, fa0, fb0);
+                }
+            }
+            // the last sub-step's fragments sit in buffer (NSUB-1)&1 (NSUB is even);
+            // once they have landed this wave is done reading stage st
+            wait_lgkmcnt0();
+            if (kt + 1 < kt_end) {
+                // steps issued after kt+1 that may stay in flight
+                const int last_issued = (kt + STAGES - 1 < kt_end - 1) ? kt + STAGES - 1 : kt_end - 1;
+                wait_steps<T>(last_issued - (kt + 1));
+                __builtin_amdgcn_s_barrier();
+                // stage st held step kt; it now receives step kt+STAGES
+                if (kt + STAGES < kt_end)
+                    issue<T, BM>(smem, A, B, off, wave, lane, kt + STAGES, st, D);
+                st = (st + 1 == STAGES) ? 0 : st + 1;
+                read_frags<T>(smem, fa0, fb0, st, 0, a_off, b_off, lh, sw);
+            }
+            mfmas<T::TM, T::TN>(acc, fa1, fb1);
+        }
+    }
+    __syncthreads();
+
+    // ---- epilogue ----------------------------------------------------------------
+    // lane holds, for MFMA block (i, j) and group q = v/4, the output row
+    // wrow0 + 32i + lr and the 4 columns wcol0 + 32j + 8q + 4lh + {0..3}
+    if constexpr (OUT_F32) {
+        float* C = reinterpret_cast<float*>(Cout) + blockIdx.y * split_stride;
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i) {
+            const int r = row0 + wrow0 + 32 * i + lr;
+            if (r >= R) continue;
+#pragma unroll
+            for (int j = 0; j < T::TN; ++j) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int c = col0 + wcol0 + 32 * j + 8 * q + 4 * lh;
+                    f32x4_t v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                 acc[i][j][4 * q + 3]};
+                    float* p = C + (int64_t)r * ldc + c;
+                    if (c + 4 <= Cc) {
+                        *reinterpret_cast<f32x4_t*>(p) = v;
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (c + e < Cc) p[e] = v[e];
+                    }
+                }
+            }
+        }
+    } else {
+        unsigned char* ep = smem + wave * T::WTM * T::EPI_LD;
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+            for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    u32x2_t v;
+                    v[0] = pack_bf16x2(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
+                    v[1] = pack_bf16x2(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+                    const int rl = 32 * i + lr;
+                    const int cl = 32 * j + 8 * q + 4 * lh;
+                    *reinterpret_cast<u32x2_t*>(ep + rl * T::EPI_LD + cl * 2) = v;
+                }
+        __syncthreads();
+        uint16_t* C = reinterpret_cast<uint16_t*>(Cout);
+        constexpr int CPRO = T::WTN / 8;           // 16-byte chunks per wave-tile row
+        constexpr int RPI = 64 / CPRO;             // rows per instruction
+#pragma unroll 4
+        for (int it = 0; it < T::WTM / RPI; ++it) {
+            const int rl = it * RPI + lane / CPRO;
+            const int cl = (lane % CPRO) * 8;
+            const int r = row0 + wrow0 + rl;
+            const int c = col0 + wcol0 + cl;
+            const u32x4_t v = *reinterpret_cast<const u32x4_t*>(ep + rl * T::EPI_LD + cl * 2);
+            if (r < R) {
+                uint16_t* p = C + (int64_t)r * ldc + c;
+                if (c + 8 <= Cc) {
+                    *reinterpret_cast<u32x4_t*>(p) = v;
+                } else if (c < Cc) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (c + e < Cc) p[e] = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
+                }
+            }
+        }
+    }
+}
+
+template <int BM, int BN, int WM, int WN, int BK, int STAGES>
+hipError_t launch_v2(const GemmArgs& g, hipStream_t stream) {
+    const int tiles_r = (g.R + BM - 1) / BM;
+    const int tiles_c = (g.Cc + BN - 1) / BN;
+    const int ktiles = (g.D + BK - 1) / BK;
+    const int S = g.splits;
+    const int ktps = (ktiles + S - 1) / S;
+    dim3 grid(tiles_r * tiles_c, S);
+    dim3 block(WM * WN * 64);
+    if (S == 1) {
+        hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, false>), grid, block,
+                           0, stream, g.A, g.lda, g.B, g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c,
+                           ktps, (int64_t)0, g.variant >> 2);
+        return hipGetLastError();
+    }
+    const int64_t ldp = splitk_ld(g.Cc);
+    const int64_t split_stride = (int64_t)g.R * ldp;
+    hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, true>), grid, block, 0,
+                       stream, g.A, g.lda, g.B, g.ldb, (void*)g.partial, ldp, g.R, g.Cc, g.D,
+                       tiles_c, ktps, split_stride, g.variant >> 2);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_splitk_reduce(g.partial, S, split_stride, ldp, g.C, g.ldc, g.R, g.Cc,
+                                g.c_f32 ? 0 : 1, stream);
+}
+
+}  // namespace
+
+// variant bit 0 clear: depth step 32 with 4 LDS stages; set: depth step 64
+// with 2.  Bits 2-3: tile order (tile_coords).
+hipError_t launch_gemm_tn_bf16_v2(const GemmArgs& g, hipStream_t stream) {
+    const int64_t lim = (int64_t)1 << 31;
+    if ((int64_t)g.R * g.lda >= lim || (int64_t)g.Cc * g.ldb >= lim || g.c_f32)
+        return launch_gemm_tn_bf16(g, stream);
+    const bool deep = (g.variant & 1) == 0;
+    switch (g.tile) {
+        case TILE_256x256:
+            return deep ? launch_v2<256, 256, 2, 2, 32, 4>(g, stream)
+                        : launch_v2<256, 256, 2, 2, 64, 2>(g, stream);
+        case TILE_256x128:
+            return deep ? launch_v2<256, 128, 2, 2, 32, 4>(g, stream)
+                        : launch_v2<256, 128, 2, 2, 64, 2>(g, stream);
+        case TILE_128x256:
+            return deep ? launch_v2<128, 256, 2, 2, 32, 4>(g, stream)
+                        : launch_v2<128, 256, 2, 2, 64, 2>(g, stream);
+        case TILE_256x256_W8:
+            return deep ? launch_v2<256, 256, 2, 4, 32, 4>(g, stream)
+                        : launch_v2<256, 256, 2, 4, 64, 2>(g, stream);
+        case TILE_256x256_W8T:
+            return deep ? launch_v2<256, 256, 4, 2, 32, 4>(g, stream)
+                        : launch_v2<256, 256, 4, 2, 64, 2>(g, stream);
+        case TILE_128x128:
+            return deep ? launch_v2<128, 128, 2, 2, 32, 4>(g, stream)
+                        : launch_v2<128, 128, 2, 2, 64, 2>(g, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace espace

@@ -1,0 +1,190 @@
+// Bandwidth-oriented bfloat16 product for few tokens (decode):
+//
+//     C[n][j] = sum_k A[n][k] * B[j][k],   n < R <= 32 (tokens), j < Cc
+//
+// The many-row operand B (P, the folded weight, or W) is streamed from HBM
+// exactly once; the few-row operand A (the tokens) is small and stays in L2.
+// A workgroup owns 16*RG consecutive rows of B and one range of the reduced
+// dimension; its WAVES waves take interleaved 32-element steps of that range,
+// so at any moment the workgroup reads WAVES*64 contiguous bytes of each row.
+// The arithmetic is done by v_mfma_f32_16x16x32_bf16 with the B rows as the
+// 16-row operand and up to 16 tokens as the 16-column operand, which keeps
+// the ALU cost negligible next to the memory stream.  Per-wave partial sums
+// are reduced through LDS in a fixed order; several depth ranges (split > 1)
+// write fp32 partials that a second kernel sums in a fixed order, so results
+// do not depend on scheduling.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace espace {
+
+namespace {
+
+constexpr int STEP = 32;   // reduced elements per MFMA
+constexpr int UNROLL = 4;  // steps whose loads are issued together
+
+template <int RG, int TG, int WAVES>
+__global__ __launch_bounds__(WAVES * 64)
+void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
+                           const uint16_t* __restrict__ B, int64_t ldb,
+                           void* __restrict__ Cout, int64_t ldc,
+                           int R, int Cc, int D, int steps_per_split,
+                           int out_f32, int64_t split_stride) {
+    __shared__ f32x4_t red[WAVES - 1][RG * TG][64];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int j0 = blockIdx.x * (16 * RG);
+    const int nsteps = (D + STEP - 1) / STEP;
+    const int s_begin = blockIdx.y * steps_per_split;
+    int s_end = s_begin + steps_per_split;
+    s_end = s_end < nsteps ? s_end : nsteps;
+
+    const int lr = lane & 15;          // B row / token inside a 16-wide group
+    const int lk = (lane >> 4) * 8;    // element offset of this lane's chunk
+
+    const uint16_t* brow[RG];
+#pragma unroll
+    for (int g = 0; g < RG; ++g) {
+        int j = j0 + g * 16 + lr;
+        j = j < Cc ? j : Cc - 1;
+        brow[g] = B + (int64_t)j * ldb;
+    }
+    const uint16_t* arow[TG];
+    bool avalid[TG];
+#pragma unroll
+    for (int t = 0; t < TG; ++t) {
+        const int n = t * 16 + lr;
+        avalid[t] = n < R;
+        arow[t] = A + (int64_t)(avalid[t] ? n : 0) * lda;
+    }
+
+    f32x4_t acc[RG][TG];
+#pragma unroll
+    for (int g = 0; g < RG; ++g)
+#pragma unroll
+        for (int t = 0; t < TG; ++t) acc[g][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    const bool full_depth = (D % STEP) == 0;
+    for (int s0 = s_begin + wave; s0 < s_end; s0 += WAVES * UNROLL) {
+        u32x4_t vb[UNROLL][RG];
+        u32x4_t va[UNROLL][TG];
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+            const int s = s0 + u * WAVES;
+            const int k = s * STEP + lk;
+            const bool live = s < s_end;
+            const bool full = live && (full_depth || (s + 1) * STEP <= D);
+#pragma unroll
+            for (int g = 0; g < RG; ++g) {
+                vb[u][g] = full ? *reinterpret_cast<const u32x4_t*>(brow[g] + k)
+                                : (live ? load_chunk_masked(brow[g], k, D) : u32x4_t{0u, 0u, 0u, 0u});
+            }
+#pragma unroll
+            for (int t = 0; t < TG; ++t) {
+                va[u][t] = (full && avalid[t]) ? *reinterpret_cast<const u32x4_t*>(arow[t] + k)
+                         : ((live && avalid[t]) ? load_chunk_masked(arow[t], k, D)
+                                                : u32x4_t{0u, 0u, 0u, 0u});
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u)
+#pragma unroll
+            for (int g = 0; g < RG; ++g)
+#pragma unroll
+                for (int t = 0; t < TG; ++t)
+                    acc[g][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        as_bf16x8(vb[u][g]), as_bf16x8(va[u][t]), acc[g][t], 0, 0, 0);
+    }
+
+    // reduce the waves' partial sums through LDS, in wave order
+    if (wave > 0) {
+#pragma unroll
+        for (int g = 0; g < RG; ++g)
+#pragma unroll
+            for (int t = 0; t < TG; ++t) red[wave - 1][g * TG + t][lane] = acc[g][t];
+    }
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int w = 0; w < WAVES - 1; ++w)
+#pragma unroll
+        for (int g = 0; g < RG; ++g)
+#pragma unroll
+            for (int t = 0; t < TG; ++t) acc[g][t] += red[w][g * TG + t][lane];
+
+    // accumulator i of lane l holds B row 4*(l/16) + i and token l%16 of its
+    // 16x16 tile: four consecutive output columns of one token row
+#pragma unroll
+    for (int g = 0; g < RG; ++g) {
+        const int jb = j0 + g * 16 + 4 * (lane >> 4);
+#pragma unroll
+        for (int t = 0; t < TG; ++t) {
+            const int n = t * 16 + lr;
+            if (n >= R) continue;
+            if (out_f32) {
+                float* C = reinterpret_cast<float*>(Cout) + blockIdx.y * split_stride + (int64_t)n * ldc;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (jb + i < Cc) C[jb + i] = acc[g][t][i];
+            } else {
+                uint16_t* C = reinterpret_cast<uint16_t*>(Cout) + (int64_t)n * ldc;
+                if (jb + 3 < Cc) {
+                    u32x2_t v;
+                    v[0] = pack_bf16x2(acc[g][t][0], acc[g][t][1]);
+                    v[1] = pack_bf16x2(acc[g][t][2], acc[g][t][3]);
+                    *reinterpret_cast<u32x2_t*>(C + jb) = v;
+                } else {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        if (jb + i < Cc) C[jb + i] = (uint16_t)bf16_rne(acc[g][t][i]);
+                }
+            }
+        }
+    }
+}
+
+template <int RG, int TG, int WAVES>
+hipError_t launch_skinny_cfg(const GemmArgs& g, hipStream_t stream) {
+    const int nsteps = (g.D + STEP - 1) / STEP;
+    const int S = g.splits;
+    const int sps = (nsteps + S - 1) / S;
+    dim3 grid((g.Cc + 16 * RG - 1) / (16 * RG), S);
+    dim3 block(WAVES * 64);
+    if (S == 1) {
+        hipLaunchKernelGGL((skinny_tn_bf16_kernel<RG, TG, WAVES>), grid, block, 0, stream,
+                           g.A, g.lda, g.B, g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, sps, g.c_f32,
+                           (int64_t)0);
+        return hipGetLastError();
+    }
+    const int64_t ldp = splitk_ld(g.Cc);
+    const int64_t split_stride = (int64_t)g.R * ldp;
+    hipLaunchKernelGGL((skinny_tn_bf16_kernel<RG, TG, WAVES>), grid, block, 0, stream,
+                       g.A, g.lda, g.B, g.ldb, (void*)g.partial, ldp, g.R, g.Cc, g.D, sps, 1,
+                       split_stride);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_splitk_reduce(g.partial, S, split_stride, ldp, g.C, g.ldc, g.R, g.Cc,
+                                g.c_f32 ? 0 : 1, stream);
+}
+
+template <int RG, int WAVES>
+hipError_t launch_skinny_tg(const GemmArgs& g, hipStream_t stream) {
+    if (g.R <= 16) return launch_skinny_cfg<RG, 1, WAVES>(g, stream);
+    return launch_skinny_cfg<RG, 2, WAVES>(g, stream);
+}
+
+}  // namespace
+
+hipError_t launch_skinny_tn_bf16(const GemmArgs& g, hipStream_t stream) {
+    if (g.R > 32) return hipErrorInvalidValue;
+    switch (g.tile) {
+        case SKINNY_RG1_W4: return launch_skinny_tg<1, 4>(g, stream);
+        case SKINNY_RG2_W4: return launch_skinny_tg<2, 4>(g, stream);
+        case SKINNY_RG1_W8: return launch_skinny_tg<1, 8>(g, stream);
+        case SKINNY_RG2_W8: return launch_skinny_tg<2, 8>(g, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace espace

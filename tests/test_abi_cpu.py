@@ -1,0 +1,90 @@
+"""The C ABI without a GPU: the library loads, exports every function the
+header declares, and rejects invalid arguments before touching any device."""
+import ctypes
+
+import pytest
+
+import paper_2410_05437_amd as E
+from paper_2410_05437_amd import _lib
+
+L = E.lib
+P16 = ctypes.c_void_p(0x10000)      # fake, 16-byte aligned; never dereferenced
+P16b = ctypes.c_void_p(0x20000000)
+P16c = ctypes.c_void_p(0x40000000)
+NULL = ctypes.c_void_p(0)
+
+
+def test_exports_every_declared_function():
+    names = E.header_functions()
+    assert set(names) == {
+        "espace_fold_weights", "espace_project", "espace_expand", "espace_projected_linear",
+        "espace_dense_linear", "espace_workspace_bytes", "espace_status_string",
+        "espace_last_error", "espace_abi_version"}
+    for n in names:
+        assert hasattr(L, n)
+    assert E.ABI_VERSION == 1
+
+
+def _fold(W=P16, ldw=64, Pt=P16b, ldp=64, Wf=P16c, ldwf=16, M=32, K=64, Lc=16, dt=1,
+          ws=NULL, wsb=0):
+    return L.espace_fold_weights(W, ldw, Pt, ldp, Wf, ldwf, M, K, Lc, dt, ws, wsb, NULL)
+
+
+def _pl(X=P16, ldx=64, Pt=P16b, ldp=64, Wf=P16c, ldwf=16, Y=ctypes.c_void_p(0x60000000),
+        ldy=32, M=32, K=64, Lc=16, N=8, dt=1, ws=ctypes.c_void_p(0x70000000), wsb=1 << 20):
+    return L.espace_projected_linear(X, ldx, Pt, ldp, Wf, ldwf, Y, ldy, M, K, Lc, N, dt, ws, wsb, NULL)
+
+
+def _status_and_msg(s):
+    return s, L.espace_last_error().decode()
+
+
+def test_validation_errors():
+    assert _fold(W=NULL) == 1                                           # NULL
+    assert _fold(Lc=65) == 2                                            # L > K
+    assert _fold(Lc=0) == 2
+    assert _fold(K=0) == 2
+    assert _fold(M=-1) == 2
+    assert _fold(ldw=60) == 2                                           # ld < cols
+    assert _fold(ldw=68) == 3                                           # ld % 8
+    assert _fold(W=ctypes.c_void_p(0x10008)) == 3                       # pointer alignment
+    assert _fold(dt=7) == 4
+    assert _fold(Wf=ctypes.c_void_p(0x10000 + 64)) == 5                 # Wf inside W
+    s, msg = _status_and_msg(_fold(Wf=ctypes.c_void_p(0x10000 + 64)))
+    assert "overlaps" in msg
+    assert _pl(ws=NULL, wsb=0) == 6                                     # workspace missing
+    assert _pl(wsb=16) == 6                                             # workspace too small
+    assert _pl(ws=ctypes.c_void_p(0x70000010)) == 3                     # workspace alignment
+    assert _pl(ws=ctypes.c_void_p(0x10000)) == 5                        # workspace over X
+
+
+def test_empty_sizes_return_ok_without_a_device():
+    assert _fold(M=0, W=NULL, Wf=NULL) == 0
+    assert _pl(N=0, X=NULL, Y=NULL, ws=NULL, wsb=0) == 0
+    assert _pl(M=0, Wf=NULL, Y=NULL, ws=NULL, wsb=0) == 0
+
+
+def test_valid_call_without_gpu_reports_device_error():
+    # every argument is valid, so the library asks the HIP runtime for the device
+    s = _pl()
+    assert s in (7, 8), (s, L.espace_last_error())
+
+
+def test_workspace_sizes():
+    bf16, f32 = 1, 0
+    ws = L.espace_workspace_bytes
+    # prefill Llama2-7B QKV: only Z (N x round_up(L, 64) bf16)
+    assert ws(3, 12288, 4096, 1536, 4096, bf16) == 4096 * 1536 * 2
+    assert ws(4, 12288, 4096, 0, 4096, bf16) == 0
+    assert ws(3, 12288, 4096, 1536, 0, bf16) == 0
+    assert ws(3, 12288, 4096, 5000, 4096, bf16) == ctypes.c_size_t(-1).value
+    assert ws(9, 1, 1, 1, 1, bf16) == ctypes.c_size_t(-1).value
+    assert ws(3, 256, 256, 64, 128, f32) == 128 * 64 * 4
+    # ragged L: Z rows padded to a multiple of 64 elements
+    assert ws(3, 6144, 24576, 2458, 8192, bf16) >= 8192 * 2496 * 2
+
+
+def test_status_strings():
+    for s in range(9):
+        assert L.espace_status_string(s)
+    assert isinstance(_lib.header_functions(), list)

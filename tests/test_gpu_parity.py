@@ -1,0 +1,227 @@
+"""GPU path vs the fp64 CPU oracle, through the C ABI.
+
+Tolerances (relative Frobenius error of the GPU output against the oracle's
+float64 result on the same rounded inputs): 1e-2 for bfloat16 storage, 1e-5
+for float32.  Parity is against the method's result (W·P)(Pᵀ·X), never W·X.
+Inputs carry NaN in their row padding, so any read of padding values would
+poison the result.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests.gpu_util import dev_mat, host64, need_gpu, out_mat, padding
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": 1e-2, "f32": 1e-5}
+
+
+@pytest.fixture(scope="module")
+def E():
+    need_gpu()
+    import paper_2410_05437_amd as e
+    return e
+
+
+def _inputs(K, M, L, N, dtype, seed=0, recipe="gaussian"):
+    w = synth.Workload(cfg=-1, name="test", K=K, M=M, L=L, N=N, dtype=dtype, recipe=recipe,
+                       lam_floor=1e-4, proj="leading", cov_key=1000 + seed, w_key=2000 + seed)
+    return synth.make_inputs(w)
+
+
+def _dev_inputs(inp, dev):
+    dt = inp.w.dtype
+    return (dev_mat(inp.X_s, dt, dev), dev_mat(inp.Pt_s, dt, dev), dev_mat(inp.W_s, dt, dev))
+
+
+# (K, M, L, N): several tiles plus ragged tails in every dimension; N <= 32
+# takes the decode path, N > 32 the tiled path
+SHAPES = [
+    (256, 256, 64, 128),
+    (1000, 600, 136, 300),
+    (1003, 517, 131, 301),
+    (640, 1100, 200, 64),
+    (520, 390, 72, 33),
+    (1024, 2000, 256, 1),
+    (1000, 777, 131, 5),
+    (1003, 1500, 200, 16),
+    (768, 1000, 96, 17),
+    (2048, 3000, 320, 32),
+]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "K%d_M%d_L%d_N%d" % s)
+def test_each_entry_point(E, dtype, shape):
+    dev = need_gpu()
+    K, M, L, N = shape
+    inp = _inputs(K, M, L, N, dtype)
+    X, Pt, W = _dev_inputs(inp, dev)
+    tol = TOL[dtype]
+
+    Wf64 = oracle.fold(inp.W, inp.Pt)
+    Z64 = oracle.project(inp.Pt, inp.X)
+    Y64 = oracle.projected_linear_from_weights(inp.X, inp.Pt, inp.W)
+    Yd64 = oracle.dense(inp.X, inp.W)
+
+    Wf = E.espace_fold_weights(W, Pt, out_mat(M, L, dtype, dev))
+    Z = E.espace_project(Pt, X, out_mat(N, L, dtype, dev))
+    Y = E.espace_projected_linear(X, Pt, Wf, out_mat(N, M, dtype, dev))
+    Ye = E.espace_expand(Z, Wf, out_mat(N, M, dtype, dev))
+    Yd = E.espace_dense_linear(X, W, out_mat(N, M, dtype, dev))
+    torch.cuda.synchronize()
+
+    assert oracle.rel_fro(host64(Wf), Wf64) <= tol
+    assert oracle.rel_fro(host64(Z), Z64) <= tol
+    assert oracle.rel_fro(host64(Y), Y64) <= tol
+    assert oracle.rel_fro(host64(Ye), Y64) <= tol
+    assert oracle.rel_fro(host64(Yd), Yd64) <= tol
+    # the fused call computes exactly what project followed by expand computes
+    assert torch.equal(Y, Ye)
+    # outputs keep their padding untouched (prefilled with NaN)
+    for t in (Wf, Z, Y, Yd):
+        assert np.isnan(padding(t)).all()
+
+
+def test_projected_linear_given_oracle_folded_weight(E):
+    """The per-call path alone, with the folded weight rounded from the
+    oracle's float64 fold (an input, not a result of the GPU)."""
+    dev = need_gpu()
+    K, M, L, N = 1000, 900, 136, 257
+    inp = _inputs(K, M, L, N, "bf16", seed=3)
+    X, Pt, _ = _dev_inputs(inp, dev)
+    Wf_bits = synth.bf16_bits_from_f64(oracle.fold(inp.W, inp.Pt))
+    Wf_exact = synth.f64_from_bf16_bits(Wf_bits).reshape(M, L)
+    Wf = dev_mat(Wf_bits, "bf16", dev)
+    Y = E.espace_projected_linear(X, Pt, Wf)
+    torch.cuda.synchronize()
+    assert oracle.rel_fro(host64(Y), oracle.projected_linear(inp.X, inp.Pt, Wf_exact)) <= 1e-2
+
+
+@pytest.mark.parametrize("N", [1, 16, 200])
+def test_selection_matrix_is_bitwise(E, N):
+    """P with distinct signed unit columns: the folded weight is exactly ±W[:, J]
+    and the projection exactly ±X[:, J] (one nonzero product per sum)."""
+    dev = need_gpu()
+    rng = np.random.default_rng(5)
+    K, M, L = 1000, 700, 136
+    J = rng.permutation(K)[:L]
+    s = rng.choice([-1.0, 1.0], size=L)
+    Pt = np.zeros((L, K))
+    Pt[np.arange(L), J] = s
+    inp = _inputs(K, M, L, N, "bf16", seed=4)
+    Xd = dev_mat(inp.X_s, "bf16", dev)
+    Wd = dev_mat(inp.W_s, "bf16", dev)
+    Pd = dev_mat(synth.bf16_bits_from_f64(Pt), "bf16", dev)
+    Wf = E.espace_fold_weights(Wd, Pd)
+    Z = E.espace_project(Pd, Xd)
+    torch.cuda.synchronize()
+    assert np.array_equal(host64(Wf), inp.W[:, J] * s[None, :])
+    assert np.array_equal(host64(Z), inp.X[:, J] * s[None, :])
+
+
+def _hadamard(K):
+    H = np.array([[1.0]])
+    while H.shape[0] < K:
+        H = np.block([[H, H], [H, -H]])
+    return H / np.sqrt(K)
+
+
+@pytest.mark.parametrize("N", [4, 300])
+def test_full_rank_hadamard_equals_dense(E, N):
+    """L = K with an orthonormal P exactly representable in bf16 (Hadamard/16):
+    PPᵀ = I, so the layer reproduces W·X within the bf16 tolerance."""
+    dev = need_gpu()
+    K, M = 256, 640
+    inp = _inputs(K, M, 8, N, "bf16", seed=6)
+    H = _hadamard(K)
+    Pd = dev_mat(synth.bf16_bits_from_f64(H.T.copy()), "bf16", dev)
+    Xd = dev_mat(inp.X_s, "bf16", dev)
+    Wd = dev_mat(inp.W_s, "bf16", dev)
+    Y = E.espace_projected_linear(Xd, Pd, E.espace_fold_weights(Wd, Pd))
+    torch.cuda.synchronize()
+    assert oracle.rel_fro(host64(Y), oracle.dense(inp.X, inp.W)) <= 1e-2
+
+
+def test_exact_rank_tokens_reproduce_dense(E):
+    """Tokens of exact rank <= L projected on the top-L eigenvectors of their
+    autocorrelation: PPᵀX = X (Theorem 1), so the layer reproduces W·X."""
+    dev = need_gpu()
+    rng = np.random.default_rng(8)
+    K, M, r, L, N = 512, 384, 40, 64, 200
+    B = np.linalg.qr(rng.standard_normal((K, r)))[0]
+    X = rng.standard_normal((N, r)) @ B.T
+    Pt, _ = oracle.principal_components(oracle.autocorrelation([X]), L)
+    W = rng.standard_normal((M, K)) / np.sqrt(K)
+    Xd = dev_mat(X.astype(np.float32), "f32", dev)
+    Pd = dev_mat(Pt.astype(np.float32), "f32", dev)
+    Wd = dev_mat(W.astype(np.float32), "f32", dev)
+    Y = E.espace_projected_linear(Xd, Pd, E.espace_fold_weights(Wd, Pd))
+    torch.cuda.synchronize()
+    assert oracle.rel_fro(host64(Y), oracle.dense(X, W)) <= 1e-5
+
+
+def test_tiny_fp32_workload(E):
+    """Workload 0 (K=M=256, L=64, N=128, float32) end to end."""
+    dev = need_gpu()
+    w = synth.workload(0)
+    inp = synth.make_inputs(w)
+    X, Pt, W = _dev_inputs(inp, dev)
+    Y = E.espace_projected_linear(X, Pt, E.espace_fold_weights(W, Pt))
+    torch.cuda.synchronize()
+    Y64 = oracle.projected_linear_from_weights(inp.X, inp.Pt, inp.W)
+    assert oracle.rel_fro(host64(Y), Y64) <= 1e-5
+    # information: the projection error against the dense layer is large by design
+    assert oracle.rel_fro(Y64, oracle.dense(inp.X, inp.W)) > 0.1
+
+
+def test_determinism(E):
+    dev = need_gpu()
+    for shape in [(1003, 1500, 200, 16), (1000, 600, 136, 300)]:
+        inp = _inputs(*shape, "bf16", seed=9)
+        X, Pt, W = _dev_inputs(inp, dev)
+        Wf = E.espace_fold_weights(W, Pt)
+        ref = E.espace_projected_linear(X, Pt, Wf).clone()
+        for _ in range(20):
+            assert torch.equal(E.espace_projected_linear(X, Pt, Wf), ref)
+
+
+def test_empty_sizes_are_no_ops(E):
+    dev = need_gpu()
+    inp = _inputs(256, 128, 32, 8, "bf16", seed=10)
+    X, Pt, W = _dev_inputs(inp, dev)
+    Wf = E.espace_fold_weights(W, Pt)
+    Y0 = E.espace_projected_linear(X[:0], Pt, Wf)
+    assert Y0.shape == (0, 128)
+    Yd0 = E.espace_dense_linear(X[:0], W)
+    assert Yd0.shape == (0, 128)
+    Ym0 = E.espace_projected_linear(X, Pt, Wf[:0])
+    assert Ym0.shape == (8, 0)
+
+
+def test_invalid_arguments_write_nothing(E):
+    dev = need_gpu()
+    inp = _inputs(256, 128, 32, 8, "bf16", seed=11)
+    X, Pt, W = _dev_inputs(inp, dev)
+    Wf = E.espace_fold_weights(W, Pt)
+    Y = out_mat(8, 128, "bf16", dev, fill=7.0)
+    # L > K
+    with pytest.raises(E.EspaceError) as ei:
+        E.espace_projected_linear(X, dev_mat(np.zeros((300, 256), np.uint16), "bf16", dev),
+                                  Wf, Y)
+    assert ei.value.status in (2,)
+    # output aliasing an input
+    with pytest.raises(E.EspaceError) as ei:
+        E.espace_dense_linear(X, W, W[:8, :128])
+    assert ei.value.status == 5
+    # misaligned base pointer (a view starting one element in)
+    big = torch.zeros(9 * 256, dtype=torch.bfloat16, device=dev)
+    Xm = big[1:1 + 8 * 256].view(8, 256)
+    with pytest.raises(E.EspaceError) as ei:
+        E.espace_dense_linear(Xm, W, Y)
+    assert ei.value.status == 3
+    torch.cuda.synchronize()
+    assert (host64(Y) == 7.0).all()
