@@ -134,6 +134,20 @@ __device__ __forceinline__ void mfmas(f32x16_t (*acc)[TN], const bf16x8_t* fa, c
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
 }
 
+// Scheduling of one sub-step: the TM+TN fragment reads of the next sub-step
+// are placed one after each MFMA of this sub-step, so their LDS latency is
+// covered by the matrix pipeline instead of being waited out.
+template <int TM, int TN>
+__device__ __forceinline__ void interleave_reads() {
+    static_assert(TM * TN >= TM + TN, "more reads than MFMAs");
+#pragma unroll
+    for (int x = 0; x < TM + TN; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - (TM + TN), 0);
+}
+
 // Matrices handed to this kernel hold fewer than 2^31 elements, so per-lane
 // load offsets fit in 32 bits (the launcher checks).
 template <int BM, int BN, int WM, int WN, int BK, int STAGES, bool OUT_F32>
@@ -218,6 +232,7 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
                     read_frags<T>(smem, fa1, fb1, st, s + 1, a_off, b_off, lh, sw);
                     mfmas<T::TM, T::TN>(acc, fa0, fb0);
                 }
+                interleave_reads<T::TM, T::TN>();
             }
             // the last sub-step's fragments sit in buffer (NSUB-1)&1 (NSUB is even);
             // once they have landed this wave is done reading stage st
