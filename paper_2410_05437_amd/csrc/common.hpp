@@ -52,6 +52,15 @@ __device__ __forceinline__ u32x4_t load_chunk_masked(const uint16_t* row, int k,
     return v;
 }
 
+// Branch-free variant for loops that keep many loads in flight: the chunk at
+// element k of a row padded to a multiple of 8 elements, keeping `valid`
+// elements (valid >= 8: all, valid <= 0: none; the address is then clamped
+// to the row start so that the load stays inside the row).
+__device__ __forceinline__ u32x4_t load_chunk_clamped(const uint16_t* row, int k, int valid) {
+    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(row + (valid > 0 ? k : 0));
+    return mask_chunk(v, valid);
+}
+
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) {
     return __builtin_bit_cast(bf16x8_t, v);
 }

@@ -9,9 +9,11 @@
 
 #include <cstdarg>
 #include <cstdio>
+#include <atomic>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
+#include <random>
 #include <string>
 
 #include "kernels.hpp"
@@ -125,7 +127,7 @@ Plan plan_tiled(int R, int Cc, int D) {
 // ESPACE_SPLITK=<n> force the tiled configuration, ESPACE_KERNEL=1 selects
 // the register-staged kernel, ESPACE_VARIANT=<n> a kernel variant (read once
 // per process).
-struct Override { int tile = -1; int splits = 0; int kernel = 2; int variant = 1; };
+struct Override { int tile = -1; int splits = 0; int kernel = 2; int variant = 1; int skinny = -1; };
 
 const Override& tile_override() {
     static const Override o = [] {
@@ -141,6 +143,10 @@ const Override& tile_override() {
         if (const char* s = std::getenv("ESPACE_SPLITK")) r.splits = std::atoi(s);
         if (const char* s = std::getenv("ESPACE_KERNEL")) r.kernel = std::atoi(s);
         if (const char* s = std::getenv("ESPACE_VARIANT")) r.variant = std::atoi(s);
+        if (const char* s = std::getenv("ESPACE_SKINNY")) {
+            const int v = std::atoi(s);
+            if (v >= espace::SKINNY_RG1_W4 && v <= espace::SKINNY_RG2_W8_U8) r.skinny = v;
+        }
         return r;
     }();
     return o;
@@ -148,7 +154,16 @@ const Override& tile_override() {
 
 Plan plan_tn(int64_t R, int64_t Cc, int64_t D, espace_dtype dt) {
     if (dt == ESPACE_F32) return Plan{};
-    if (R <= 32) return plan_skinny((int)R, (int)Cc, (int)D);
+    if (R <= 32) {
+        Plan p = plan_skinny((int)R, (int)Cc, (int)D);
+        const Override& o = tile_override();
+        if (o.skinny >= 0) p.tile = o.skinny;
+        if (o.splits > 0) {
+            p.splits = o.splits < ceil_div(D, 32) ? o.splits : (int)ceil_div(D, 32);
+            p.partial_bytes = p.splits > 1 ? (size_t)p.splits * R * espace::splitk_ld(Cc) * sizeof(float) : 0;
+        }
+        return p;
+    }
     Plan p = plan_tiled((int)R, (int)Cc, (int)D);
     const Override& o = tile_override();
     if (o.tile >= 0 || o.splits > 0) {
@@ -161,6 +176,48 @@ Plan plan_tn(int64_t R, int64_t Cc, int64_t D, espace_dtype dt) {
 }
 
 int64_t z_ld(int64_t L, espace_dtype dt) { return round_up(L, dt == ESPACE_BF16 ? 64 : 32); }
+
+// One-launch decode path (bf16, N <= 32).  It is selected per call with
+// ESPACE_DECODE=fused; by default the two-launch path runs, which is faster
+// on this device today (the fused path spends its time on cross-workgroup
+// hand-offs; see decode_fused.hip).
+bool use_fused_decode(int64_t N, int64_t L, espace_dtype dt) {
+    const char* s = std::getenv("ESPACE_DECODE");
+    const bool enabled = s && !std::strcmp(s, "fused");
+    return enabled && dt == ESPACE_BF16 && N >= 1 && N <= 32 && espace::decode_fused_supported((int)N, (int)L);
+}
+
+int64_t part_ld(int64_t L) { return round_up(L, 4); }
+
+struct FusedPlan { int S1 = 1, steps1 = 0, P1 = 0, P2 = 0; };
+
+FusedPlan fused_plan(int64_t N, int64_t K, int64_t L, int64_t M) {
+    FusedPlan p;
+    espace::decode_fused_plan((int)N, (int)K, (int)L, (int)M, kNumCUs, &p.S1, &p.steps1, &p.P1, &p.P2);
+    return p;
+}
+
+size_t fused_partial_bytes(int64_t N, int64_t K, int64_t L, int64_t M, espace_dtype dt) {
+    if (!use_fused_decode(N, L, dt)) return 0;
+    const FusedPlan p = fused_plan(N, K, L, M);
+    return p.S1 > 1 ? (size_t)p.S1 * N * part_ld(L) * sizeof(float) : 0;
+}
+
+// The counter block of the one-launch path sits at the end of the workspace.
+size_t fused_sync_bytes(int64_t N, int64_t L, espace_dtype dt) {
+    return use_fused_decode(N, L, dt) ? espace::decode_fused_sync_bytes((int)L) : 0;
+}
+
+// Per-call tags of the counter block: a counter started from a random 64-bit
+// value, so that leftover workspace contents match a tag with negligible
+// probability.
+unsigned long long next_epoch() {
+    static std::atomic<unsigned long long> next{[] {
+        std::random_device rd;
+        return ((unsigned long long)rd() << 32) ^ (unsigned long long)rd();
+    }()};
+    return next.fetch_add(1, std::memory_order_relaxed);
+}
 
 size_t z_bytes(int64_t N, int64_t L, espace_dtype dt) {
     return align_ws((size_t)N * z_ld(L, dt) * elem_size(dt));
@@ -176,7 +233,10 @@ size_t ws_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int64_t N, espace
             if (!N || !M) return 0;
             size_t a = plan_tn(N, L, K, dt).partial_bytes;
             size_t b = plan_tn(N, M, L, dt).partial_bytes;
-            return z_bytes(N, L, dt) + align_ws(a > b ? a : b);
+            const size_t c = fused_partial_bytes(N, K, L, M, dt);
+            size_t m = a > b ? a : b;
+            m = m > c ? m : c;
+            return z_bytes(N, L, dt) + align_ws(m) + fused_sync_bytes(N, L, dt);
         }
     }
     return SIZE_MAX;
@@ -416,6 +476,22 @@ espace_status espace_projected_linear(const void* X, int64_t ldx, const void* Pt
     const int64_t ldz = z_ld(L, dt);
     void* Z = workspace;
     void* partial = (char*)workspace + z_bytes(N, L, dt);
+    if (use_fused_decode(N, L, dt)) {
+        const FusedPlan p = fused_plan(N, K, L, M);
+        espace::DecodeArgs a;
+        a.X = (const uint16_t*)X; a.ldx = ldx;
+        a.Pt = (const uint16_t*)Pt; a.ldp = ldp;
+        a.Wf = (const uint16_t*)Wf; a.ldwf = ldwf;
+        a.Y = (uint16_t*)Y; a.ldy = ldy;
+        a.Z = (uint16_t*)Z; a.ldz = ldz;
+        a.part = (float*)partial; a.ldpart = part_ld(L);
+        a.sync = (unsigned long long*)((char*)workspace + need - fused_sync_bytes(N, L, dt));
+        a.epoch = next_epoch();
+        a.N = (int)N; a.K = (int)K; a.L = (int)L; a.M = (int)M;
+        a.S1 = p.S1; a.steps1 = p.steps1; a.P1 = p.P1; a.P2 = p.P2;
+        if (espace::launch_decode_fused(a, stream) == hipSuccess) return ok();
+        (void)hipGetLastError();   // not launched: take the two-launch path
+    }
     ESPACE_TRY(run_tn(X, ldx, Pt, ldp, Z, ldz, N, L, K, dt, partial, stream));
     ESPACE_TRY(run_tn(Z, ldz, Wf, ldwf, Y, ldy, N, M, L, dt, partial, stream));
     return ok();

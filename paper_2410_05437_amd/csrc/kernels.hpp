@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 namespace espace {
@@ -17,6 +18,10 @@ enum TileKind {
     SKINNY_RG2_W4 = 11,
     SKINNY_RG1_W8 = 12,
     SKINNY_RG2_W8 = 13,
+    SKINNY_RG1_W4_U8 = 14,   // as above with 8 steps of loads in flight per wave
+    SKINNY_RG2_W4_U8 = 15,
+    SKINNY_RG1_W8_U8 = 16,
+    SKINNY_RG2_W8_U8 = 17,
 };
 
 // One "TN" product C[r][c] = sum_k A[r][k] * B[c][k]  (bf16 in, fp32 accumulate).
@@ -47,6 +52,26 @@ hipError_t launch_skinny_tn_bf16(const GemmArgs& g, hipStream_t stream);
 hipError_t launch_splitk_reduce(const float* P, int S, int64_t split_stride, int64_t ldp,
                                 void* C, int64_t ldc, int R, int Cc, int out_bf16,
                                 hipStream_t stream);
+// One-launch projected linear layer for N <= 32 tokens (bf16).
+struct DecodeArgs {
+    const uint16_t* X;  int64_t ldx;    // [N][K]
+    const uint16_t* Pt; int64_t ldp;    // [L][K]
+    const uint16_t* Wf; int64_t ldwf;   // [M][L]
+    uint16_t* Y;        int64_t ldy;    // [N][M]
+    uint16_t* Z;        int64_t ldz;    // workspace [N][ldz], ldz >= round_up(L, 16)
+    float* part;        int64_t ldpart; // workspace [S1][N][ldpart] (S1 > 1), ldpart = round_up(L, 4)
+    unsigned long long* sync;           // workspace: counter block (decode_fused_sync_bytes)
+    unsigned long long epoch;           // per-call tag of the counter block
+    int N, K, L, M;
+    int S1, steps1;                     // depth splits of the projection
+    int P1, P2;                         // projection units, phase-2 workgroups
+};
+
+bool decode_fused_supported(int N, int L);
+size_t decode_fused_sync_bytes(int L);
+void decode_fused_plan(int N, int K, int L, int M, int cus, int* S1, int* steps1, int* P1, int* P2);
+hipError_t launch_decode_fused(const DecodeArgs& a, hipStream_t stream);
+
 hipError_t launch_gemm_tn_f32(const float* A, int64_t lda, const float* B, int64_t ldb,
                               float* C, int64_t ldc, int R, int Cc, int D, hipStream_t stream);
 

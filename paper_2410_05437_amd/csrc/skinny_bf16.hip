@@ -6,7 +6,8 @@
 // exactly once; the few-row operand A (the tokens) is small and stays in L2.
 // A workgroup owns 16*RG consecutive rows of B and one range of the reduced
 // dimension; its WAVES waves take interleaved 32-element steps of that range,
-// so at any moment the workgroup reads WAVES*64 contiguous bytes of each row.
+// so at any moment the workgroup reads WAVES*64 contiguous bytes of each row,
+// and each wave keeps UNROLL steps of loads in flight.
 // The arithmetic is done by v_mfma_f32_16x16x32_bf16 with the B rows as the
 // 16-row operand and up to 16 tokens as the 16-column operand, which keeps
 // the ALU cost negligible next to the memory stream.  Per-wave partial sums
@@ -21,9 +22,8 @@ namespace espace {
 namespace {
 
 constexpr int STEP = 32;   // reduced elements per MFMA
-constexpr int UNROLL = 4;  // steps whose loads are issued together
 
-template <int RG, int TG, int WAVES>
+template <int RG, int TG, int WAVES, int UNROLL>
 __global__ __launch_bounds__(WAVES * 64)
 void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
                            const uint16_t* __restrict__ B, int64_t ldb,
@@ -39,6 +39,8 @@ void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
     const int s_begin = blockIdx.y * steps_per_split;
     int s_end = s_begin + steps_per_split;
     s_end = s_end < nsteps ? s_end : nsteps;
+    // steps whose 32 elements all lie below D
+    const int s_fast_end = s_end < D / STEP ? s_end : D / STEP;
 
     const int lr = lane & 15;          // B row / token inside a 16-wide group
     const int lk = (lane >> 4) * 8;    // element offset of this lane's chunk
@@ -50,13 +52,14 @@ void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
         j = j < Cc ? j : Cc - 1;
         brow[g] = B + (int64_t)j * ldb;
     }
+    // token rows beyond R read row 0 and are zeroed with a mask
     const uint16_t* arow[TG];
-    bool avalid[TG];
+    uint32_t amask[TG];
 #pragma unroll
     for (int t = 0; t < TG; ++t) {
         const int n = t * 16 + lr;
-        avalid[t] = n < R;
-        arow[t] = A + (int64_t)(avalid[t] ? n : 0) * lda;
+        amask[t] = n < R ? 0xffffffffu : 0u;
+        arow[t] = A + (int64_t)(n < R ? n : 0) * lda;
     }
 
     f32x4_t acc[RG][TG];
@@ -65,27 +68,54 @@ void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
 #pragma unroll
         for (int t = 0; t < TG; ++t) acc[g][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    const bool full_depth = (D % STEP) == 0;
-    for (int s0 = s_begin + wave; s0 < s_end; s0 += WAVES * UNROLL) {
+    // Main loop: UNROLL whole steps per wave, every load unconditional, so
+    // that all of them are in flight together.
+    int s0 = s_begin + wave;
+    for (; s0 + (UNROLL - 1) * WAVES < s_fast_end; s0 += WAVES * UNROLL) {
         u32x4_t vb[UNROLL][RG];
         u32x4_t va[UNROLL][TG];
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
+            const int k = (s0 + u * WAVES) * STEP + lk;
+#pragma unroll
+            for (int g = 0; g < RG; ++g) vb[u][g] = *reinterpret_cast<const u32x4_t*>(brow[g] + k);
+#pragma unroll
+            for (int t = 0; t < TG; ++t) va[u][t] = *reinterpret_cast<const u32x4_t*>(arow[t] + k) & amask[t];
+        }
+        __builtin_amdgcn_sched_barrier(0);   // all loads issue before the first MFMA
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u)
+#pragma unroll
+            for (int g = 0; g < RG; ++g)
+#pragma unroll
+                for (int t = 0; t < TG; ++t)
+                    acc[g][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        as_bf16x8(vb[u][g]), as_bf16x8(va[u][t]), acc[g][t], 0, 0, 0);
+    }
+    // Tail (at most one pass): steps past the range or the depth load from a
+    // clamped address and are masked, without branches.
+    for (; s0 < s_end; s0 += WAVES * UNROLL) {
+        u32x4_t vb[UNROLL][RG];
+        u32x4_t va[UNROLL][TG];
+        int valid[UNROLL];
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
             const int s = s0 + u * WAVES;
             const int k = s * STEP + lk;
-            const bool live = s < s_end;
-            const bool full = live && (full_depth || (s + 1) * STEP <= D);
+            valid[u] = s < s_end ? D - k : 0;
+            const int kk = valid[u] > 0 ? k : 0;
 #pragma unroll
-            for (int g = 0; g < RG; ++g) {
-                vb[u][g] = full ? *reinterpret_cast<const u32x4_t*>(brow[g] + k)
-                                : (live ? load_chunk_masked(brow[g], k, D) : u32x4_t{0u, 0u, 0u, 0u});
-            }
+            for (int g = 0; g < RG; ++g) vb[u][g] = *reinterpret_cast<const u32x4_t*>(brow[g] + kk);
 #pragma unroll
-            for (int t = 0; t < TG; ++t) {
-                va[u][t] = (full && avalid[t]) ? *reinterpret_cast<const u32x4_t*>(arow[t] + k)
-                         : ((live && avalid[t]) ? load_chunk_masked(arow[t], k, D)
-                                                : u32x4_t{0u, 0u, 0u, 0u});
-            }
+            for (int t = 0; t < TG; ++t) va[u][t] = *reinterpret_cast<const u32x4_t*>(arow[t] + kk);
+        }
+        __builtin_amdgcn_sched_barrier(0);   // masks are applied once the loads are in flight
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+#pragma unroll
+            for (int g = 0; g < RG; ++g) vb[u][g] = mask_chunk(vb[u][g], valid[u]);
+#pragma unroll
+            for (int t = 0; t < TG; ++t) va[u][t] = mask_chunk(va[u][t], valid[u]) & amask[t];
         }
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u)
@@ -144,7 +174,7 @@ void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
     }
 }
 
-template <int RG, int TG, int WAVES>
+template <int RG, int TG, int WAVES, int UNROLL>
 hipError_t launch_skinny_cfg(const GemmArgs& g, hipStream_t stream) {
     const int nsteps = (g.D + STEP - 1) / STEP;
     const int S = g.splits;
@@ -152,14 +182,14 @@ hipError_t launch_skinny_cfg(const GemmArgs& g, hipStream_t stream) {
     dim3 grid((g.Cc + 16 * RG - 1) / (16 * RG), S);
     dim3 block(WAVES * 64);
     if (S == 1) {
-        hipLaunchKernelGGL((skinny_tn_bf16_kernel<RG, TG, WAVES>), grid, block, 0, stream,
+        hipLaunchKernelGGL((skinny_tn_bf16_kernel<RG, TG, WAVES, UNROLL>), grid, block, 0, stream,
                            g.A, g.lda, g.B, g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, sps, g.c_f32,
                            (int64_t)0);
         return hipGetLastError();
     }
     const int64_t ldp = splitk_ld(g.Cc);
     const int64_t split_stride = (int64_t)g.R * ldp;
-    hipLaunchKernelGGL((skinny_tn_bf16_kernel<RG, TG, WAVES>), grid, block, 0, stream,
+    hipLaunchKernelGGL((skinny_tn_bf16_kernel<RG, TG, WAVES, UNROLL>), grid, block, 0, stream,
                        g.A, g.lda, g.B, g.ldb, (void*)g.partial, ldp, g.R, g.Cc, g.D, sps, 1,
                        split_stride);
     hipError_t e = hipGetLastError();
@@ -168,10 +198,10 @@ hipError_t launch_skinny_cfg(const GemmArgs& g, hipStream_t stream) {
                                 g.c_f32 ? 0 : 1, stream);
 }
 
-template <int RG, int WAVES>
+template <int RG, int WAVES, int UNROLL>
 hipError_t launch_skinny_tg(const GemmArgs& g, hipStream_t stream) {
-    if (g.R <= 16) return launch_skinny_cfg<RG, 1, WAVES>(g, stream);
-    return launch_skinny_cfg<RG, 2, WAVES>(g, stream);
+    if (g.R <= 16) return launch_skinny_cfg<RG, 1, WAVES, UNROLL>(g, stream);
+    return launch_skinny_cfg<RG, 2, WAVES, UNROLL>(g, stream);
 }
 
 }  // namespace
@@ -179,10 +209,14 @@ hipError_t launch_skinny_tg(const GemmArgs& g, hipStream_t stream) {
 hipError_t launch_skinny_tn_bf16(const GemmArgs& g, hipStream_t stream) {
     if (g.R > 32) return hipErrorInvalidValue;
     switch (g.tile) {
-        case SKINNY_RG1_W4: return launch_skinny_tg<1, 4>(g, stream);
-        case SKINNY_RG2_W4: return launch_skinny_tg<2, 4>(g, stream);
-        case SKINNY_RG1_W8: return launch_skinny_tg<1, 8>(g, stream);
-        case SKINNY_RG2_W8: return launch_skinny_tg<2, 8>(g, stream);
+        case SKINNY_RG1_W4: return launch_skinny_tg<1, 4, 4>(g, stream);
+        case SKINNY_RG2_W4: return launch_skinny_tg<2, 4, 4>(g, stream);
+        case SKINNY_RG1_W8: return launch_skinny_tg<1, 8, 4>(g, stream);
+        case SKINNY_RG2_W8: return launch_skinny_tg<2, 8, 4>(g, stream);
+        case SKINNY_RG1_W4_U8: return launch_skinny_tg<1, 4, 8>(g, stream);
+        case SKINNY_RG2_W4_U8: return launch_skinny_tg<2, 4, 8>(g, stream);
+        case SKINNY_RG1_W8_U8: return launch_skinny_tg<1, 8, 8>(g, stream);
+        case SKINNY_RG2_W8_U8: return launch_skinny_tg<2, 8, 8>(g, stream);
         default: return hipErrorInvalidValue;
     }
 }

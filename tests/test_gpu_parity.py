@@ -225,3 +225,56 @@ def test_invalid_arguments_write_nothing(E):
     assert ei.value.status == 3
     torch.cuda.synchronize()
     assert (host64(Y) == 7.0).all()
+
+
+DECODE_SHAPES = [s for s in SHAPES if s[3] <= 32] + [(4096, 3000, 1536, 16), (11008, 700, 1536, 3)]
+
+
+@pytest.mark.parametrize("shape", DECODE_SHAPES, ids=lambda s: "K%d_M%d_L%d_N%d" % s)
+def test_one_launch_decode_path(E, shape, monkeypatch):
+    """The one-launch decode path (selected with ESPACE_DECODE=fused) against
+    the oracle, over ragged shapes, one and two token groups and depth splits."""
+    dev = need_gpu()
+    monkeypatch.setenv("ESPACE_DECODE", "fused")
+    K, M, L, N = shape
+    inp = _inputs(K, M, L, N, "bf16", seed=30)
+    X, Pt, W = _dev_inputs(inp, dev)
+    Wf = E.espace_fold_weights(W, Pt)
+    Y = E.espace_projected_linear(X, Pt, Wf, out_mat(N, M, "bf16", dev))
+    torch.cuda.synchronize()
+    Y64 = oracle.projected_linear_from_weights(inp.X, inp.Pt, inp.W)
+    assert oracle.rel_fro(host64(Y), Y64) <= TOL["bf16"]
+
+
+def test_decode_workspace_contents_do_not_matter(E, monkeypatch):
+    """The one-launch decode path keeps its counters in the workspace, which
+    need no initialisation: leftover bytes (zeros, all ones, random, another
+    shape's counter state) give the same, bitwise identical output."""
+    dev = need_gpu()
+    monkeypatch.setenv("ESPACE_DECODE", "fused")
+    shapes = [(1003, 1500, 200, 16), (768, 1000, 96, 17), (1024, 2000, 256, 1), (4096, 3000, 1536, 8)]
+    cases = []
+    for i, (K, M, L, N) in enumerate(shapes):
+        inp = _inputs(K, M, L, N, "bf16", seed=20 + i)
+        X, Pt, W = _dev_inputs(inp, dev)
+        Wf = E.espace_fold_weights(W, Pt)
+        ref = E.espace_projected_linear(X, Pt, Wf).clone()
+        torch.cuda.synchronize()
+        Y64 = oracle.projected_linear_from_weights(inp.X, inp.Pt, inp.W)
+        assert oracle.rel_fro(host64(ref), Y64) <= TOL["bf16"]
+        cases.append((X, Pt, Wf, ref))
+    need = max(E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, Wf.shape[0], X.shape[1], Pt.shape[0],
+                                        X.shape[0], torch.bfloat16) for X, Pt, Wf, _ in cases)
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    gen = torch.Generator(device="cpu").manual_seed(5)
+    fills = ["zeros", "ones", "random", "keep", "keep"]
+    for fill in fills:
+        for X, Pt, Wf, ref in cases + cases[::-1]:
+            if fill == "zeros":
+                ws.zero_()
+            elif fill == "ones":
+                ws.fill_(255)
+            elif fill == "random":
+                ws.copy_(torch.randint(0, 256, (need,), dtype=torch.uint8, generator=gen))
+            Y = E.espace_projected_linear(X, Pt, Wf, workspace=ws)
+            assert torch.equal(Y, ref), fill
