@@ -94,6 +94,7 @@ Plan plan_tiled(int R, int Cc, int D) {
         {espace::TILE_256x128, 256, 128, 1, 0.85},
         {espace::TILE_128x256, 128, 256, 1, 0.85},
         {espace::TILE_128x128, 128, 128, 2, 0.70},
+        {espace::TILE_128x192, 128, 192, 1, 0.70},
     };
     const int ktiles = ceil_div(D, 64);
     Plan best;
@@ -139,6 +140,7 @@ const Override& tile_override() {
             else if (!std::strcmp(t, "128x128")) r.tile = espace::TILE_128x128;
             else if (!std::strcmp(t, "256x256w8")) r.tile = espace::TILE_256x256_W8;
             else if (!std::strcmp(t, "256x256w8t")) r.tile = espace::TILE_256x256_W8T;
+            else if (!std::strcmp(t, "128x192")) r.tile = espace::TILE_128x192;
         }
         if (const char* s = std::getenv("ESPACE_SPLITK")) r.splits = std::atoi(s);
         if (const char* s = std::getenv("ESPACE_KERNEL")) r.kernel = std::atoi(s);

@@ -299,12 +299,16 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
         uint16_t* C = reinterpret_cast<uint16_t*>(Cout);
         constexpr int CPRO = T::WTN / 8;           // 16-byte chunks per wave-tile row
         constexpr int RPI = 64 / CPRO;             // rows per instruction
+        constexpr int ITERS = (T::WTM + RPI - 1) / RPI;
+        // lanes past RPI*CPRO idle when CPRO does not divide 64 (96-wide tiles)
+        const bool lane_used = lane < RPI * CPRO;
 #pragma unroll 4
-        for (int it = 0; it < T::WTM / RPI; ++it) {
+        for (int it = 0; it < ITERS; ++it) {
             const int rl = it * RPI + lane / CPRO;
             const int cl = (lane % CPRO) * 8;
             const int r = row0 + wrow0 + rl;
             const int c = col0 + wcol0 + cl;
+            if (!lane_used || rl >= T::WTM) continue;
             const u32x4_t v = *reinterpret_cast<const u32x4_t*>(ep + rl * T::EPI_LD + cl * 2);
             if (r < R) {
                 uint16_t* p = C + (int64_t)r * ldc + c;
@@ -374,6 +378,9 @@ hipError_t launch_gemm_tn_bf16_v2(const GemmArgs& g, hipStream_t stream) {
         case TILE_128x128:
             return deep ? launch_v2<128, 128, 2, 2, 32, 4>(g, stream)
                         : launch_v2<128, 128, 2, 2, 64, 2>(g, stream);
+        case TILE_128x192:
+            return deep ? launch_v2<128, 192, 2, 2, 32, 4>(g, stream)
+                        : launch_v2<128, 192, 2, 2, 64, 2>(g, stream);
         default: return hipErrorInvalidValue;
     }
 }

@@ -9,6 +9,7 @@ from .bf16 import bf16_bits_from_f64, f64_from_bf16_bits  # noqa: F401
 from .configs import CONFIGS, Workload, workloads, workload  # noqa: F401
 from .generate import (  # noqa: F401
     haar_orthogonal,
+    index_pattern,
     spectrum,
     gaussian_tokens,
     structured_tokens,

@@ -278,3 +278,29 @@ def test_decode_workspace_contents_do_not_matter(E, monkeypatch):
                 ws.copy_(torch.randint(0, 256, (need,), dtype=torch.uint8, generator=gen))
             Y = E.espace_projected_linear(X, Pt, Wf, workspace=ws)
             assert torch.equal(Y, ref), fill
+
+
+def test_matrices_past_2g_elements(E):
+    """A weight of 524296 x 4096 bf16 (more than 2^31 elements, 4 GiB) takes the
+    kernel with 64-bit row offsets; sampled outputs, including the last rows,
+    against the oracle."""
+    dev = need_gpu()
+    M, K, N = (1 << 19) + 8, 4096, 48
+    assert M * K >= 1 << 31
+    W = torch.empty((M, K), dtype=torch.bfloat16, device=dev)
+    kk = torch.arange(K, device=dev, dtype=torch.int32)[None, :]
+    for r0 in range(0, M, 1 << 16):
+        r1 = min(M, r0 + (1 << 16))
+        mm = torch.arange(r0, r1, device=dev, dtype=torch.int32)[:, None]
+        W[r0:r1] = synth.index_pattern(mm, kk).to(torch.float32).to(torch.bfloat16)
+    inp = _inputs(K, 64, 32, N, "bf16", seed=40)
+    X = dev_mat(inp.X_s, "bf16", dev)
+    Y = E.espace_dense_linear(X, W)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(3)
+    cols = np.unique(np.concatenate([rng.choice(M, 200, replace=False), np.arange(M - 40, M)]))
+    W_sel = synth.index_pattern(cols[:, None].astype(np.int64), np.arange(K)[None, :])
+    ref = oracle.dense(inp.X, W_sel)
+    got = host64(Y[:, torch.as_tensor(cols, device=dev)])
+    assert oracle.rel_fro(got, ref) <= TOL["bf16"]
+    del W
