@@ -30,6 +30,16 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 ROTATE_BYTES = 600 << 20    # > 2x the 256 MB last-level cache
+COPY_PROBE_BYTES = 1 << 30  # calibration copy for the traffic counters
+TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                            "expand_gemm_llama2_7b_qkv_traffic.md")
+
+# Table 1 of the paper (NVIDIA A100, BF16, batch 1, sequence 4096, native
+# PyTorch GEMMs): Llama2-7B at 50% compression, whole-model totals.
+PAPER_TABLE1 = {"hardware": "NVIDIA A100, BF16, native PyTorch (Table 1, App. B.4)",
+                "model": "Llama2-7B, sequence 4096, 50% compression",
+                "gemm_latency_reduction": 0.46, "ttft_reduction": 0.28,
+                "headline": "35-45% GEMM latency, up to ~40% TTFT reduction"}
 
 
 def parse():
@@ -40,6 +50,9 @@ def parse():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--kernel-probe", action="store_true",
+                    help="run only a 1 GiB elementwise copy and `steps` launches of the "
+                         "expand GEMM (for hardware-counter runs), then exit")
     return ap.parse_args()
 
 
@@ -85,6 +98,51 @@ def time_each(fn, n_args, steps, stream):
         b.record(stream)
     torch.cuda.synchronize()
     return float(np.mean([a.elapsed_time(b) for a, b in evs]))
+
+
+def copy_probe(dev):
+    """One elementwise copy of COPY_PROBE_BYTES (read that many bytes, write
+    that many): the reference the traffic counters are scaled by."""
+    import torch
+    n = COPY_PROBE_BYTES // 2
+    src = torch.ones(n, dtype=torch.bfloat16, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def traffic_sources():
+    """Sources whose change invalidates the stored traffic counters of the
+    expand GEMM (the kernel, its helpers and the tile planner)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("paper_2410_05437_amd/csrc/gemm_bf16_v2.hip", "paper_2410_05437_amd/csrc/common.hpp",
+              "paper_2410_05437_amd/csrc/kernels.hpp", "paper_2410_05437_amd/csrc/espace_api.hip"):
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def stored_traffic():
+    """HBM bytes per launch of the expand GEMM from the committed counter
+    summary, or None when it is missing or the kernel changed since."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None, "no counter summary"
+    vals = {}
+    for line in text.splitlines():
+        if ":" in line and line.strip().startswith("- "):
+            k, v = line.strip()[2:].split(":", 1)
+            vals[k.strip()] = v.strip().strip("`")
+    if vals.get("source_sha256") != traffic_sources():
+        return None, "kernel changed since the counters were taken"
+    try:
+        return int(float(vals["hbm_bytes_per_launch"])), vals.get("ratio_to_algorithmic")
+    except (KeyError, ValueError):
+        return None, "summary unreadable"
 
 
 def cpu_baseline(inp, seconds):
@@ -157,6 +215,16 @@ def main():
     def step(i):
         E.espace_projected_linear(Xr[i], Pr[i], Wfr[i], Y, ws)
 
+    if args.kernel_probe:
+        copy_probe(dev)
+        E.espace_project(Pts, Xs, Z, wsz)
+        for i in range(args.steps):
+            E.espace_expand(Z, Wfr[i % R], Y, wse)
+        torch.cuda.synchronize()
+        print(json.dumps({"kernel_probe": "expand", "launches": args.steps, "R": N, "Cc": M, "D": L,
+                          "copy_probe_bytes": COPY_PROBE_BYTES}), flush=True)
+        return
+
     # the timed region: exactly `steps` calls, synchronised on both sides
     for i in range(args.warmup):
         step(i % R)
@@ -173,9 +241,10 @@ def main():
     flops = acc.projected_flops(K, M, L, N)
     tflops = flops / (ms * 1e-3) / 1e12
 
-    # the two kernels of the path, each bracketed by events on the launch stream
-    ms_proj = time_each(lambda i: E.espace_project(Pr[i], Xr[i], Z, wsz), R, args.steps, stream)
-    ms_exp = time_each(lambda i: E.espace_expand(Z, Wfr[i], Y, wse), R, args.steps, stream)
+    # the two kernels of the path, each as `steps` back-to-back launches between
+    # two events on the launch stream (average launch duration)
+    ms_proj = time_calls(lambda i: E.espace_project(Pr[i], Xr[i], Z, wsz), R, args.steps, 2, stream)
+    ms_exp = time_calls(lambda i: E.espace_expand(Z, Wfr[i], Y, wse), R, args.steps, 2, stream)
     kern = {
         "project": {"ms": ms_proj, "flops": acc.gemm_flops(N, L, K)},
         "expand": {"ms": ms_exp, "flops": acc.gemm_flops(N, M, L)},
@@ -214,7 +283,12 @@ def main():
         "expand_us": round(ms_exp * 1e3, 2),
         "compression": round(acc.compression(K, M, L), 4),
         "rotating_copies": R,
+        "gemm_time_reduction_vs_dense": round(1.0 - ms / ms_dense, 4),
+        "paper_table1": PAPER_TABLE1,
     }
+    traffic, traffic_note = stored_traffic()
+    detail["expand_algorithmic_bytes"] = acc.gemm_bytes(N, M, L)
+    detail["traffic_note"] = traffic_note
 
     if not args.no_decode:
         detail["decode"] = decode_lines(E, acc, synth, dev, stream, args)
@@ -241,7 +315,7 @@ def main():
         "roofline": {"bound": "mfma", "kernel": dom,
                      "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": traffic if dom == "expand" else None},
         "cpu_baseline": cpu,
         "detail": detail,
     }
