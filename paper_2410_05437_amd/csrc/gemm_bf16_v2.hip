@@ -9,8 +9,11 @@
 // v_mfma_f32_32x32x16_bf16 blocks held in accumulation registers.
 //
 // Data movement:
-//  * global -> LDS with global_load_lds_dwordx4: each wave instruction moves
-//    64 x 16 B into 1 KB of contiguous LDS (1024/(2*BK) tile rows).  The
+//  * global -> LDS with buffer_load_dwordx4 ... lds: each wave instruction
+//    moves 64 x 16 B into 1 KB of contiguous LDS (1024/(2*BK) tile rows).
+//    The buffer form (not global_load_lds) matters: it is counted by vmcnt
+//    only, so the compiler keeps precise lgkmcnt waits for the fragment reads
+//    of the same step instead of lgkmcnt(0).  The
 //    swizzle is applied on the global side: the lane that writes chunk slot p
 //    of row r fetches logical chunk p ^ swz(r), so chunk c of row r lives at
 //    slot c ^ swz(r).  swz(r) spreads the 16 rows read by 16 consecutive lanes
@@ -82,16 +85,26 @@ __device__ __forceinline__ void wait_steps(int n) {
 // Issue the loads of depth step kt into LDS stage st.
 template <class T, int BM>
 __device__ __forceinline__ void issue(unsigned char* smem, const uint16_t* __restrict__ A,
-                                      const uint16_t* __restrict__ B, const int* off, int wave,
+                                      const uint16_t* __restrict__ B, unsigned a_bytes,
+                                      unsigned b_bytes, const int* off, int wave,
                                       int lane, int kt, int st, int D) {
     const int k0 = kt * (T::ROWB / 2);
     unsigned char* sbase = smem + st * T::STAGE;
     if (k0 + T::ROWB / 2 <= D) {
+        // buffer loads into LDS: counted by vmcnt only, so the LDS fragment
+        // reads of the same step keep precise lgkmcnt waits (descriptors over
+        // the rows of A and B; fewer than 2^31 elements, so the byte counts
+        // fit the 32-bit record count)
 #pragma unroll
         for (int j = 0; j < T::LPW; ++j) {
             const int q = wave + j * T::NW;
-            const uint16_t* base = (q * T::RPL < BM) ? A : B;
-            __builtin_amdgcn_global_load_lds(base + off[j] + k0, sbase + q * 1024, 16, 0, 0);
+            const bool isA = q * T::RPL < BM;
+            const unsigned voff = (unsigned)(off[j] + k0) * 2u;
+            const auto rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(isA ? A : B), (short)0,
+                                                                (int)(isA ? a_bytes : b_bytes), 0x00020000);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc,
+                                                     (__attribute__((address_space(3))) void*)(sbase + q * 1024),
+                                                     16, (int)voff, 0, 0, 0);
         }
     } else {
         // depth tail: through registers, zeroing elements at or beyond D
@@ -193,6 +206,9 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
         off[j] = gr * (int)(isA ? lda : ldb) + lc * 8;
     }
 
+    const unsigned ra = (unsigned)((uint64_t)R * lda * 2u);    // bytes of A's rows
+    const unsigned rb = (unsigned)((uint64_t)Cc * ldb * 2u);   // bytes of B's rows
+
     const int lr = lane & 31;
     const int lh = lane >> 5;
     const int sw = swz<T>(lr);                    // rows of a fragment are lr mod 32
@@ -214,7 +230,7 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
         // prologue: steps kt0 .. kt0+STAGES-1 fill the stages
 #pragma unroll
         for (int p = 0; p < STAGES; ++p)
-            if (kt0 + p < kt_end) issue<T, BM>(smem, A, B, off, wave, lane, kt0 + p, p, D);
+            if (kt0 + p < kt_end) issue<T, BM>(smem, A, B, ra, rb, off, wave, lane, kt0 + p, p, D);
         {
             const int newer = (kt_end - kt0 - 1) < (STAGES - 1) ? (kt_end - kt0 - 1) : (STAGES - 1);
             wait_steps<T>(newer);
@@ -244,7 +260,7 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
                 __builtin_amdgcn_s_barrier();
                 // stage st held step kt; it now receives step kt+STAGES
                 if (kt + STAGES < kt_end)
-                    issue<T, BM>(smem, A, B, off, wave, lane, kt + STAGES, st, D);
+                    issue<T, BM>(smem, A, B, ra, rb, off, wave, lane, kt + STAGES, st, D);
                 st = (st + 1 == STAGES) ? 0 : st + 1;
                 read_frags<T>(smem, fa0, fb0, st, 0, a_off, b_off, lh, sw);
             }
