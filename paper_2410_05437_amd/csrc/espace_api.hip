@@ -62,22 +62,26 @@ struct Plan {
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 Plan plan_skinny(int R, int Cc, int D) {
+    // Measured on the decode layers (N <= 32): a launch costs a few µs
+    // whatever its size, so the depth is split only when the tokens make
+    // each workgroup's loads heavy; 8 waves with 6 loads in flight fit
+    // 48-step depths exactly; 32-row groups halve the token re-reads from L2
+    // when there are 9 or more tokens.
     Plan p;
     p.kind = KIND_SKINNY;
-    const int nb2 = ceil_div(Cc, 32);
     const int nb1 = ceil_div(Cc, 16);
     const int steps = ceil_div(D, 32);
     const int target = 2 * kNumCUs;
-    if (nb2 >= target) {
-        p.tile = espace::SKINNY_RG2_W4;
-    } else if (nb1 >= target) {
-        p.tile = espace::SKINNY_RG1_W4;
+    if (nb1 >= target) {
+        if (R > 8) p.tile = espace::SKINNY_RG2_W4;
+        else p.tile = (steps <= 48) ? espace::SKINNY_RG1_W8_U6 : espace::SKINNY_RG1_W8_U8;
     } else {
-        p.tile = espace::SKINNY_RG1_W8;
-        int s = ceil_div(target, nb1);
-        int smax = steps / 32;              // keep >= 4 steps per wave per split
-        if (smax < 1) smax = 1;
-        p.splits = s < smax ? s : smax;
+        p.tile = espace::SKINNY_RG1_W8_U8;
+        int s = R > 8 ? 2 : 1;
+        const int by_depth = ceil_div(steps, 128);   // at most 128 KB of each 16 rows per workgroup
+        if (by_depth > s) s = by_depth;
+        if (s > 1 && steps / s < 32) s = steps / 32 > 1 ? steps / 32 : 1;   // >= 4 steps per wave
+        p.splits = s;
     }
     if (p.splits > 1) p.partial_bytes = (size_t)p.splits * R * espace::splitk_ld(Cc) * sizeof(float);
     return p;
@@ -147,7 +151,7 @@ const Override& tile_override() {
         if (const char* s = std::getenv("ESPACE_VARIANT")) r.variant = std::atoi(s);
         if (const char* s = std::getenv("ESPACE_SKINNY")) {
             const int v = std::atoi(s);
-            if (v >= espace::SKINNY_RG1_W4 && v <= espace::SKINNY_RG2_W8_U8) r.skinny = v;
+            if (v >= espace::SKINNY_RG1_W4 && v <= espace::SKINNY_RG1_W16_U4) r.skinny = v;
         }
         return r;
     }();

@@ -23,6 +23,10 @@ enum TileKind {
     SKINNY_RG2_W4_U8 = 15,
     SKINNY_RG1_W8_U8 = 16,
     SKINNY_RG2_W8_U8 = 17,
+    SKINNY_RG1_W8_U6 = 18,   // 6 steps in flight (48-step depths split evenly over 8 waves)
+    SKINNY_RG2_W4_U6 = 19,
+    SKINNY_RG1_W16_U8 = 20,  // 16 waves: one workgroup keeps 128 steps in flight
+    SKINNY_RG1_W16_U4 = 21,
 };
 
 // One "TN" product C[r][c] = sum_k A[r][k] * B[c][k]  (bf16 in, fp32 accumulate).

@@ -217,6 +217,10 @@ hipError_t launch_skinny_tn_bf16(const GemmArgs& g, hipStream_t stream) {
         case SKINNY_RG2_W4_U8: return launch_skinny_tg<2, 4, 8>(g, stream);
         case SKINNY_RG1_W8_U8: return launch_skinny_tg<1, 8, 8>(g, stream);
         case SKINNY_RG2_W8_U8: return launch_skinny_tg<2, 8, 8>(g, stream);
+        case SKINNY_RG1_W8_U6: return launch_skinny_tg<1, 8, 6>(g, stream);
+        case SKINNY_RG2_W4_U6: return launch_skinny_tg<2, 4, 6>(g, stream);
+        case SKINNY_RG1_W16_U8: return launch_skinny_tg<1, 16, 8>(g, stream);
+        case SKINNY_RG1_W16_U4: return launch_skinny_tg<1, 16, 4>(g, stream);
         default: return hipErrorInvalidValue;
     }
 }
