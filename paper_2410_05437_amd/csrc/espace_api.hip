@@ -56,7 +56,8 @@ struct Plan {
     int kind = KIND_F32;
     int tile = 0;
     int splits = 1;
-    size_t partial_bytes = 0;   // fp32 partial sums for splits > 1
+    int pair = 0;               // splits == 2 combined inside the GEMM kernel
+    size_t partial_bytes = 0;   // fp32 partial sums for splits > 1 (and pair state words)
 };
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
@@ -89,50 +90,91 @@ Plan plan_skinny(int R, int Cc, int D) {
 
 struct TileShape { int tile, bm, bn, per_cu; double eff; };
 
+// Per-call tags of the state words in workspaces (decode counters, pair
+// states): a counter started from a random 64-bit value, so that leftover
+// workspace contents match a tag with negligible probability.
+unsigned long long next_epoch() {
+    static std::atomic<unsigned long long> next{[] {
+        std::random_device rd;
+        return ((unsigned long long)rd() << 32) ^ (unsigned long long)rd();
+    }()};
+    return next.fetch_add(1, std::memory_order_relaxed);
+}
+
+// Workspace of a tiled plan: pair state words after the pair tiles, or the
+// split-K partial sums.
+void set_partial_bytes(Plan& p, int64_t R, int64_t Cc) {
+    p.partial_bytes = 0;
+    if (p.pair) {
+        int bm = 0, bn = 0;
+        espace::tile_dims(p.tile, &bm, &bn);
+        const size_t tiles = (size_t)ceil_div(R, bm) * ceil_div(Cc, bn);
+        p.partial_bytes = tiles * bm * bn * sizeof(float) + tiles * 8;
+    } else if (p.splits > 1) {
+        p.partial_bytes = (size_t)p.splits * R * espace::splitk_ld(Cc) * sizeof(float);
+    }
+}
+
 Plan plan_tiled(int R, int Cc, int D) {
     // Estimated time of each tile shape (and depth split) from the number of
     // rounds of workgroups the chip needs, the per-tile work and a relative
-    // efficiency of the tile shape; the cheapest wins.
+    // efficiency of the tile shape; the cheapest wins.  Two depth halves can
+    // also be combined inside the kernel ("pair"), which costs one fp32 tile
+    // written and read per output tile instead of a reduction pass.
     static const TileShape shapes[] = {
         {espace::TILE_256x256_W8T, 256, 256, 1, 1.00},
+        {espace::TILE_256x192_W8, 256, 192, 1, 0.97},
         {espace::TILE_256x128, 256, 128, 1, 0.85},
         {espace::TILE_128x256, 128, 256, 1, 0.85},
         {espace::TILE_128x128, 128, 128, 2, 0.70},
         {espace::TILE_128x192, 128, 192, 1, 0.70},
     };
     const int ktiles = ceil_div(D, 64);
+    const double byte_cost = 315.0 / (2.0 * 64 * kNumCUs);   // bytes priced against the MFMA rate
     Plan best;
     best.kind = KIND_TILED;
     double best_cost = 1e300;
     for (const TileShape& s : shapes) {
         const int64_t tiles = (int64_t)ceil_div(R, s.bm) * ceil_div(Cc, s.bn);
+        const int64_t slots = (int64_t)kNumCUs * s.per_cu;
         for (int splits = 1; splits <= 4; ++splits) {
             if (splits > 1 && ktiles / splits < 8) break;
-            const int64_t blocks = tiles * splits;
-            const int64_t slots = (int64_t)kNumCUs * s.per_cu;
-            const int64_t rounds = (blocks + slots - 1) / slots;
-            // a round runs per_cu blocks on every CU
-            const double per_round = (double)s.bm * s.bn * ceil_div(ktiles, splits) * s.per_cu;
-            double cost = rounds * per_round / s.eff;
-            // partial sums: written and read back once each (fp32), priced
-            // against the MFMA rate as bytes per flop of the machine balance
-            if (splits > 1) cost += 2.0 * splits * (double)R * Cc * 4.0 * 315.0 / (2.0 * 64 * kNumCUs);
-            if (cost < best_cost) {
-                best_cost = cost;
-                best.tile = s.tile;
-                best.splits = splits;
+            for (int pair = 0; pair <= (splits == 2 ? 1 : 0); ++pair) {
+                const int64_t blocks = tiles * splits;
+                const int64_t rounds = (blocks + slots - 1) / slots;
+                // a round runs per_cu blocks on every CU
+                const double per_round = (double)s.bm * s.bn * ceil_div(ktiles, splits) * s.per_cu;
+                double cost = rounds * per_round / s.eff;
+                // the pair hand-off prices at 1.6x its bytes (measured: the
+                // second half waits for the first's stores)
+                if (pair) cost += 3.2 * tiles * s.bm * s.bn * 4.0 * byte_cost;
+                else if (splits > 1) cost += 2.0 * splits * (double)R * Cc * 4.0 * byte_cost;
+                if (cost < best_cost) {
+                    best_cost = cost;
+                    best.tile = s.tile;
+                    best.splits = splits;
+                    best.pair = pair;
+                }
             }
         }
     }
-    if (best.splits > 1) best.partial_bytes = (size_t)best.splits * R * espace::splitk_ld(Cc) * sizeof(float);
+    set_partial_bytes(best, R, Cc);
     return best;
 }
 
-// Tuning override: ESPACE_TILE=256x256|256x128|128x256|128x128 and
-// ESPACE_SPLITK=<n> force the tiled configuration, ESPACE_KERNEL=1 selects
-// the register-staged kernel, ESPACE_VARIANT=<n> a kernel variant (read once
-// per process).
-struct Override { int tile = -1; int splits = 0; int kernel = 2; int variant = 1; int skinny = -1; };
+// Tuning overrides, read once per process: ESPACE_TILE=<shape name> and
+// ESPACE_SPLITK=<n> force the tiled configuration, ESPACE_PAIR=0|1 turns the
+// in-kernel combine of two depth halves off or on, ESPACE_TUNE_SHAPE=R,Cc,D
+// restricts those three to products of that shape; ESPACE_KERNEL=1|3 selects
+// the register-staged or the ping-pong kernel, ESPACE_VARIANT=<n> a kernel
+// variant, ESPACE_SKINNY=<kind> the small-N kernel.
+struct Override {
+    int tile = -1, splits = 0, kernel = 2, variant = 1, skinny = -1, pair = -1;
+    long long shape[3] = {-1, -1, -1};
+    bool applies(int64_t R, int64_t Cc, int64_t D) const {
+        return shape[0] < 0 || (shape[0] == R && shape[1] == Cc && shape[2] == D);
+    }
+};
 
 const Override& tile_override() {
     static const Override o = [] {
@@ -145,8 +187,13 @@ const Override& tile_override() {
             else if (!std::strcmp(t, "256x256w8")) r.tile = espace::TILE_256x256_W8;
             else if (!std::strcmp(t, "256x256w8t")) r.tile = espace::TILE_256x256_W8T;
             else if (!std::strcmp(t, "128x192")) r.tile = espace::TILE_128x192;
+            else if (!std::strcmp(t, "256x192w8")) r.tile = espace::TILE_256x192_W8;
         }
         if (const char* s = std::getenv("ESPACE_SPLITK")) r.splits = std::atoi(s);
+        if (const char* s = std::getenv("ESPACE_PAIR")) r.pair = std::atoi(s) ? 1 : 0;
+        if (const char* s = std::getenv("ESPACE_TUNE_SHAPE"))
+            if (std::sscanf(s, "%lld,%lld,%lld", &r.shape[0], &r.shape[1], &r.shape[2]) != 3)
+                r.shape[0] = -1;
         if (const char* s = std::getenv("ESPACE_KERNEL")) r.kernel = std::atoi(s);
         if (const char* s = std::getenv("ESPACE_VARIANT")) r.variant = std::atoi(s);
         if (const char* s = std::getenv("ESPACE_SKINNY")) {
@@ -172,12 +219,31 @@ Plan plan_tn(int64_t R, int64_t Cc, int64_t D, espace_dtype dt) {
     }
     Plan p = plan_tiled((int)R, (int)Cc, (int)D);
     const Override& o = tile_override();
-    if (o.tile >= 0 || o.splits > 0) {
+    if ((o.tile >= 0 || o.splits > 0 || o.pair >= 0) && o.applies(R, Cc, D)) {
         if (o.tile >= 0) p.tile = o.tile;
-        if (o.splits > 0) p.splits = o.splits;
+        if (o.splits > 0) {
+            p.splits = o.splits;
+            p.pair = 0;
+        }
         if (p.splits > ceil_div(D, 64)) p.splits = ceil_div(D, 64);
-        p.partial_bytes = p.splits > 1 ? (size_t)p.splits * R * espace::splitk_ld(Cc) * sizeof(float) : 0;
+        if (o.pair >= 0) p.pair = (o.pair == 1 && p.splits == 2) ? 1 : 0;
+        if (p.splits != 2) p.pair = 0;
+        set_partial_bytes(p, R, Cc);
     }
+    return p;
+}
+
+// ESPACE_PLAN_LOG=1 prints each product's plan to stderr (read once per process).
+Plan plan_tn_logged(int64_t R, int64_t Cc, int64_t D, espace_dtype dt) {
+    static const bool log = [] {
+        const char* s = std::getenv("ESPACE_PLAN_LOG");
+        return s && std::atoi(s) != 0;
+    }();
+    const Plan p = plan_tn(R, Cc, D, dt);
+    if (log)
+        std::fprintf(stderr, "espace plan R=%lld Cc=%lld D=%lld: kind=%d tile=%d splits=%d pair=%d partial=%zu\n",
+                     (long long)R, (long long)Cc, (long long)D, (int)p.kind, p.tile, p.splits, p.pair,
+                     p.partial_bytes);
     return p;
 }
 
@@ -214,16 +280,6 @@ size_t fused_sync_bytes(int64_t N, int64_t L, espace_dtype dt) {
     return use_fused_decode(N, L, dt) ? espace::decode_fused_sync_bytes((int)L) : 0;
 }
 
-// Per-call tags of the counter block: a counter started from a random 64-bit
-// value, so that leftover workspace contents match a tag with negligible
-// probability.
-unsigned long long next_epoch() {
-    static std::atomic<unsigned long long> next{[] {
-        std::random_device rd;
-        return ((unsigned long long)rd() << 32) ^ (unsigned long long)rd();
-    }()};
-    return next.fetch_add(1, std::memory_order_relaxed);
-}
 
 size_t z_bytes(int64_t N, int64_t L, espace_dtype dt) {
     return align_ws((size_t)N * z_ld(L, dt) * elem_size(dt));
@@ -340,7 +396,7 @@ espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, voi
         e = espace::launch_gemm_tn_f32((const float*)A, lda, (const float*)B, ldb, (float*)C, ldc,
                                        (int)R, (int)Cc, (int)D, stream);
     } else {
-        const Plan p = plan_tn(R, Cc, D, dt);
+        const Plan p = plan_tn_logged(R, Cc, D, dt);
         GemmArgs g;
         g.A = (const uint16_t*)A;
         g.lda = lda;
@@ -356,6 +412,8 @@ espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, voi
         g.splits = p.splits;
         g.partial = (float*)partial;
         g.variant = tile_override().variant;
+        g.pair = p.pair;
+        if (p.pair) g.epoch = next_epoch();
         e = p.kind == KIND_SKINNY ? espace::launch_skinny_tn_bf16(g, stream)
                                   : (tile_override().kernel == 1 ? espace::launch_gemm_tn_bf16(g, stream)
                                      : tile_override().kernel == 3 ? espace::launch_gemm_tn_bf16_pp(g, stream)

@@ -266,7 +266,12 @@ hipError_t launch_splitk_reduce(const float* P, int S, int64_t split_stride, int
 
 // The planner's tile is a hint here: shapes this kernel does not have map to
 // the nearest one it has (the grid follows the shape actually launched).
-hipError_t launch_gemm_tn_bf16(const GemmArgs& g, hipStream_t stream) {
+hipError_t launch_gemm_tn_bf16(const GemmArgs& g0, hipStream_t stream) {
+    GemmArgs g = g0;
+    if (g.pair) {            // no in-kernel pair combine here: one depth range
+        g.splits = 1;
+        g.pair = 0;
+    }
     switch (g.tile) {
         case TILE_256x256:
         case TILE_256x256_W8:
@@ -274,6 +279,7 @@ hipError_t launch_gemm_tn_bf16(const GemmArgs& g, hipStream_t stream) {
         case TILE_256x128: return launch_cfg<256, 128, 2, 2>(g, stream);
         case TILE_128x256:
         case TILE_128x192: return launch_cfg<128, 256, 2, 2>(g, stream);
+        case TILE_256x192_W8: return launch_cfg<256, 256, 2, 4>(g, stream);
         case TILE_128x128: return launch_cfg<128, 128, 2, 2>(g, stream);
         default: return hipErrorInvalidValue;
     }

@@ -319,7 +319,12 @@ hipError_t launch_pp(const GemmArgs& g, hipStream_t stream) {
 
 }  // namespace
 
-hipError_t launch_gemm_tn_bf16_pp(const GemmArgs& g, hipStream_t stream) {
+hipError_t launch_gemm_tn_bf16_pp(const GemmArgs& g0, hipStream_t stream) {
+    GemmArgs g = g0;
+    if (g.pair) {            // no in-kernel pair combine here: one depth range
+        g.splits = 1;
+        g.pair = 0;
+    }
     const int64_t lim = (int64_t)1 << 31;
     if ((int64_t)g.R * g.lda >= lim || (int64_t)g.Cc * g.ldb >= lim || g.c_f32)
         return launch_gemm_tn_bf16(g, stream);

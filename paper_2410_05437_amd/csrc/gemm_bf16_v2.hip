@@ -161,15 +161,103 @@ __device__ __forceinline__ void interleave_reads() {
     __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - (TM + TN), 0);
 }
 
+enum { MODE_BF16 = 0, MODE_F32 = 1, MODE_PAIR = 2 };
+
+// Two depth halves of one output tile, combined without a second kernel and
+// without waiting for a workgroup that may not have started: the half whose
+// workgroup arrives first (one compare-and-swap on the tile's state word)
+// writes its fp32 sums to the workspace and marks them ready; the second
+// adds them to its own and writes the bf16 tile.  fp32 addition of two terms
+// is commutative, so the result is the same whichever half comes first.
+// The state word is (48-bit call tag << 16 | state), state 1 = first
+// arrived, 2 = its sums are ready, 3 = consumed; any other content (another
+// call, uninitialised memory, the previous replay of a captured launch) makes
+// the next arrival the first.  Sums move through agent-scope (L2-coherent)
+// 64-bit atomic stores and loads; the waits are bounded.
+// Returns true on the workgroup that writes the output.
+template <class T>
+__device__ bool pair_combine(f32x16_t (&acc)[T::TM][T::TN], unsigned long long* state, float* part,
+                             unsigned long long epoch, int* role, int wave, int lane) {
+    const unsigned long long tag = (epoch & 0xFFFFFFFFFFFFull) << 16;
+    if (threadIdx.x == 0) {
+        unsigned long long old = __hip_atomic_load(state, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        int second = 0;
+        for (int it = 0; it < (1 << 20); ++it) {
+            const unsigned long long st = old & 0xFFFFull;
+            if ((old & ~0xFFFFull) == tag && (st == 1 || st == 2)) {
+                second = 1;
+                break;
+            }
+            if (__hip_atomic_compare_exchange_strong(state, &old, tag | 1ull, __ATOMIC_RELAXED,
+                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+                break;
+        }
+        *role = second;
+    }
+    __syncthreads();
+    const bool second = *role != 0;
+    // this wave's region: [wave][i][j][q][lane] of f32x4
+    unsigned long long* base =
+        reinterpret_cast<unsigned long long*>(part) + (size_t)wave * T::TM * T::TN * 4 * 64 * 2;
+    if (!second) {
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+            for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    unsigned long long* p = base + (((i * T::TN + j) * 4 + q) * 64 + lane) * 2;
+                    const unsigned long long lo =
+                        (unsigned long long)__float_as_uint(acc[i][j][4 * q]) |
+                        ((unsigned long long)__float_as_uint(acc[i][j][4 * q + 1]) << 32);
+                    const unsigned long long hi =
+                        (unsigned long long)__float_as_uint(acc[i][j][4 * q + 2]) |
+                        ((unsigned long long)__float_as_uint(acc[i][j][4 * q + 3]) << 32);
+                    __hip_atomic_store(p, lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(p + 1, hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+        __builtin_amdgcn_s_waitcnt(0);           // this wave's stores are complete
+        __syncthreads();
+        if (threadIdx.x == 0) __hip_atomic_store(state, tag | 2ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return false;
+    }
+    if (threadIdx.x == 0) {
+        for (int it = 0; it < (1 << 24); ++it) {
+            if (__hip_atomic_load(state, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (tag | 2ull)) break;
+            __builtin_amdgcn_s_sleep(2);
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const unsigned long long* p = base + (((i * T::TN + j) * 4 + q) * 64 + lane) * 2;
+                const unsigned long long lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                const unsigned long long hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                acc[i][j][4 * q] += __uint_as_float((unsigned)lo);
+                acc[i][j][4 * q + 1] += __uint_as_float((unsigned)(lo >> 32));
+                acc[i][j][4 * q + 2] += __uint_as_float((unsigned)hi);
+                acc[i][j][4 * q + 3] += __uint_as_float((unsigned)(hi >> 32));
+            }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) __hip_atomic_store(state, tag | 3ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return true;
+}
+
 // Matrices handed to this kernel hold fewer than 2^31 elements, so per-lane
 // load offsets fit in 32 bits (the launcher checks).
-template <int BM, int BN, int WM, int WN, int BK, int STAGES, bool OUT_F32>
+template <int BM, int BN, int WM, int WN, int BK, int STAGES, int MODE>
 __global__ __launch_bounds__(WM * WN * 64, 1)
 void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
                             const uint16_t* __restrict__ B, int64_t ldb,
                             void* __restrict__ Cout, int64_t ldc,
                             int R, int Cc, int D, int tiles_c, int ktiles_per_split,
-                            int64_t split_stride, int map) {
+                            int64_t split_stride, int map, unsigned long long* tile_state,
+                            float* pair_part, unsigned long long epoch) {
     using T = Cfg<BM, BN, WM, WN, BK, STAGES>;
     __shared__ __attribute__((aligned(1024))) unsigned char smem[T::SMEM];
 
@@ -269,10 +357,17 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
     }
     __syncthreads();
 
+    if constexpr (MODE == MODE_PAIR) {
+        const int tile = tile_r * tiles_c + tile_c;
+        if (!pair_combine<T>(acc, tile_state + tile, pair_part + (size_t)tile * (BM * BN), epoch,
+                             reinterpret_cast<int*>(smem), wave, lane))
+            return;
+    }
+
     // ---- epilogue ----------------------------------------------------------------
     // lane holds, for MFMA block (i, j) and group q = v/4, the output row
     // wrow0 + 32i + lr and the 4 columns wcol0 + 32j + 8q + 4lh + {0..3}
-    if constexpr (OUT_F32) {
+    if constexpr (MODE == MODE_F32) {
         float* C = reinterpret_cast<float*>(Cout) + blockIdx.y * split_stride;
 #pragma unroll
         for (int i = 0; i < T::TM; ++i) {
@@ -350,16 +445,27 @@ hipError_t launch_v2(const GemmArgs& g, hipStream_t stream) {
     dim3 grid(tiles_r * tiles_c, S);
     dim3 block(WM * WN * 64);
     if (S == 1) {
-        hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, false>), grid, block,
+        hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_BF16>), grid, block,
                            0, stream, g.A, g.lda, g.B, g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c,
-                           ktps, (int64_t)0, g.variant >> 2);
+                           ktps, (int64_t)0, g.variant >> 2, nullptr, nullptr, 0ull);
+        return hipGetLastError();
+    }
+    if (S == 2 && g.pair) {
+        // two depth halves per tile combined in the kernel; partial: tiles x BM x BN fp32,
+        // then one state word per tile
+        const int ntiles = tiles_r * tiles_c;
+        unsigned long long* state =
+            reinterpret_cast<unsigned long long*>(g.partial + (size_t)ntiles * BM * BN);
+        hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_PAIR>), grid, block,
+                           0, stream, g.A, g.lda, g.B, g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c,
+                           ktps, (int64_t)0, g.variant >> 2, state, g.partial, g.epoch);
         return hipGetLastError();
     }
     const int64_t ldp = splitk_ld(g.Cc);
     const int64_t split_stride = (int64_t)g.R * ldp;
-    hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, true>), grid, block, 0,
+    hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_F32>), grid, block, 0,
                        stream, g.A, g.lda, g.B, g.ldb, (void*)g.partial, ldp, g.R, g.Cc, g.D,
-                       tiles_c, ktps, split_stride, g.variant >> 2);
+                       tiles_c, ktps, split_stride, g.variant >> 2, nullptr, nullptr, 0ull);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_splitk_reduce(g.partial, S, split_stride, ldp, g.C, g.ldc, g.R, g.Cc,
@@ -368,12 +474,23 @@ hipError_t launch_v2(const GemmArgs& g, hipStream_t stream) {
 
 }  // namespace
 
+void tile_dims(int tile, int* bm, int* bn) {
+    switch (tile) {
+        case TILE_256x128: *bm = 256; *bn = 128; return;
+        case TILE_128x256: *bm = 128; *bn = 256; return;
+        case TILE_128x128: *bm = 128; *bn = 128; return;
+        case TILE_128x192: *bm = 128; *bn = 192; return;
+        case TILE_256x192_W8: *bm = 256; *bn = 192; return;
+        default: *bm = 256; *bn = 256; return;
+    }
+}
+
 // variant bit 0 clear: depth step 32 with 4 LDS stages; set: depth step 64
 // with 2.  Bits 2-3: tile order (tile_coords).
 hipError_t launch_gemm_tn_bf16_v2(const GemmArgs& g, hipStream_t stream) {
     const int64_t lim = (int64_t)1 << 31;
     if ((int64_t)g.R * g.lda >= lim || (int64_t)g.Cc * g.ldb >= lim || g.c_f32)
-        return launch_gemm_tn_bf16(g, stream);
+        return launch_gemm_tn_bf16(g, stream);   // runs a pair plan as one depth range
     const bool deep = (g.variant & 1) == 0;
     switch (g.tile) {
         case TILE_256x256:
@@ -397,6 +514,8 @@ hipError_t launch_gemm_tn_bf16_v2(const GemmArgs& g, hipStream_t stream) {
         case TILE_128x192:
             return deep ? launch_v2<128, 192, 2, 2, 32, 4>(g, stream)
                         : launch_v2<128, 192, 2, 2, 64, 2>(g, stream);
+        case TILE_256x192_W8:   // depth step 64 only (448 rows of 32 deep do not split over 8 waves)
+            return launch_v2<256, 192, 4, 2, 64, 2>(g, stream);
         default: return hipErrorInvalidValue;
     }
 }

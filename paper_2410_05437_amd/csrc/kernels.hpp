@@ -15,6 +15,7 @@ enum TileKind {
     TILE_256x256_W8 = 4,     // 8 waves as 2 x 4 (128 x 64 each)
     TILE_256x256_W8T = 5,    // 8 waves as 4 x 2 (64 x 128 each)
     TILE_128x192 = 6,        // 4 waves as 2 x 2 (64 x 96 each)
+    TILE_256x192_W8 = 7,     // 8 waves as 4 x 2 (64 x 96 each)
     SKINNY_RG1_W4 = 10,
     SKINNY_RG2_W4 = 11,
     SKINNY_RG1_W8 = 12,
@@ -43,9 +44,15 @@ struct GemmArgs {
     int c_f32;          // 1: write fp32 output
     int tile;           // TileKind
     int splits;         // depth ranges; > 1 needs `partial`
-    float* partial;     // splits * R * splitk_ld(Cc) fp32 (workspace)
+    float* partial;     // splits * R * splitk_ld(Cc) fp32 (workspace); with `pair`:
+                        // tiles * tile area fp32, then one 8-byte state word per tile
     int variant = 0;    // kernel variant (tuning)
+    int pair = 0;       // splits == 2 combined inside the kernel (no reduce pass)
+    unsigned long long epoch = 0;   // per-call tag of the pair state words
 };
+
+// Tile size of a TileKind in the pair-combine kernel (rows, columns).
+void tile_dims(int tile, int* bm, int* bn);
 
 // leading dimension of split-K partial sums
 inline int64_t splitk_ld(int Cc) { return (Cc + 7) / 8 * 8; }

@@ -127,7 +127,10 @@ def _haar_torch(Gn, dev):
         if int(info) != 0:
             ok = False
             break
-        Q = torch.linalg.solve_triangular(R, Q, upper=True, left=False)
+        # Q·R⁻¹ one block of rows at a time: rows are independent, and the
+        # BLAS triangular solve's workspace grows with the right-hand side
+        Q = torch.cat([torch.linalg.solve_triangular(R, Q[r:r + 1024], upper=True, left=False)
+                       for r in range(0, Q.shape[0], 1024)])
     if ok:
         I = torch.eye(64, Q.shape[0], dtype=Q.dtype, device=dev)
         ok = float((Q[:, :64].T @ Q - I).abs().max()) < 1e-12
