@@ -169,7 +169,7 @@ Plan plan_tiled(int R, int Cc, int D) {
 // the register-staged or the ping-pong kernel, ESPACE_VARIANT=<n> a kernel
 // variant, ESPACE_SKINNY=<kind> the small-N kernel.
 struct Override {
-    int tile = -1, splits = 0, kernel = 2, variant = 1, skinny = -1, pair = -1;
+    int tile = -1, splits = 0, kernel = 2, variant = 3, skinny = -1, pair = -1;
     long long shape[3] = {-1, -1, -1};
     bool applies(int64_t R, int64_t Cc, int64_t D) const {
         return shape[0] < 0 || (shape[0] == R && shape[1] == Cc && shape[2] == D);

@@ -36,18 +36,21 @@ namespace espace {
 
 namespace {
 
-template <int BM, int BN, int WM, int WN, int BK, int STAGES>
+// MI: MFMA block edge, 32 (v_mfma_f32_32x32x16_bf16) or 16 (v_mfma_f32_16x16x32_bf16)
+template <int BM, int BN, int WM, int WN, int BK, int STAGES, int MI = 32>
 struct Cfg {
     static constexpr int NW = WM * WN;
     static constexpr int WTM = BM / WM;
     static constexpr int WTN = BN / WN;
-    static constexpr int TM = WTM / 32;
-    static constexpr int TN = WTN / 32;
+    static constexpr int TM = WTM / MI;
+    static constexpr int TN = WTN / MI;
+    static constexpr int KSUB = 512 / MI;                 // depth of one MFMA
+    static constexpr int ACC = MI * MI / 64;              // accumulators per lane and block
     static constexpr int ROWB = BK * 2;                   // bytes per LDS tile row
     static constexpr int CPR = BK / 8;                    // 16-byte chunks per row
     static constexpr int RPL = 1024 / ROWB;               // rows per 1 KB wave-load
     static constexpr int SWZ_SH = ROWB == 128 ? 1 : 2;    // rows sharing a 256-B bank line
-    static constexpr int NSUB = BK / 16;                  // MFMA sub-steps per step
+    static constexpr int NSUB = BK / KSUB;                // MFMA sub-steps per step
     static constexpr int STAGE = (BM + BN) * ROWB;        // bytes per LDS stage
     static constexpr int NLOAD = (BM + BN) / RPL;         // wave-loads per stage
     static constexpr int LPW = NLOAD / NW;                // wave-loads per wave per stage
@@ -55,10 +58,14 @@ struct Cfg {
     static constexpr int EPI = NW * WTM * EPI_LD;
     static constexpr int SMEM = (STAGES * STAGE > EPI) ? STAGES * STAGE : EPI;
     static_assert(NLOAD % NW == 0, "loads per wave");
-    static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
+    static_assert(WTM % 32 == 0 && WTN % 32 == 0 && (MI == 32 || MI == 16), "wave tile");
+    static_assert(NSUB % 2 == 0, "sub-steps alternate two fragment buffers");
     static_assert(BK == 32 || BK == 64, "depth step");
     static_assert(LPW * (STAGES - 1) < 64, "vmcnt range");
 };
+
+template <int MI> struct AccOf { typedef f32x16_t type; };
+template <> struct AccOf<16> { typedef f32x4_t type; };
 
 template <class T>
 __device__ __forceinline__ int swz(int r) { return (r >> T::SWZ_SH) & (T::CPR - 1); }
@@ -122,29 +129,36 @@ __device__ __forceinline__ void issue(unsigned char* smem, const uint16_t* __res
     }
 }
 
-// Read the fragments of 16-deep sub-step s of stage st.
+// Read the fragments of sub-step s (KSUB deep) of stage st: lane l holds
+// row l % MI of each block and the 8 depth elements of chunk
+// (KSUB/8)*s + l/MI.
 template <class T>
 __device__ __forceinline__ void read_frags(const unsigned char* smem, bf16x8_t* fa, bf16x8_t* fb,
                                            int st, int s, int a_off, int b_off, int lh, int sw) {
     const unsigned char* sbase = smem + st * T::STAGE;
-    const int pc = ((2 * s + lh) ^ sw) * 16;
+    const int pc = (((T::KSUB / 8) * s + lh) ^ sw) * 16;
+    constexpr int MI = T::WTM / T::TM;
 #pragma unroll
     for (int i = 0; i < T::TM; ++i)
-        fa[i] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(sbase + a_off + i * 32 * T::ROWB + pc));
+        fa[i] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(sbase + a_off + i * MI * T::ROWB + pc));
 #pragma unroll
     for (int j = 0; j < T::TN; ++j)
-        fb[j] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(sbase + b_off + j * 32 * T::ROWB + pc));
+        fb[j] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(sbase + b_off + j * MI * T::ROWB + pc));
 }
 
 // The MFMA is issued with the B rows as its first operand: the result of
 // block (i, j) holds output rows in lanes and output columns in registers.
-template <int TM, int TN>
-__device__ __forceinline__ void mfmas(f32x16_t (*acc)[TN], const bf16x8_t* fa, const bf16x8_t* fb) {
+template <int TM, int TN, class Acc>
+__device__ __forceinline__ void mfmas(Acc (*acc)[TN], const bf16x8_t* fa, const bf16x8_t* fb) {
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < TN; ++j) {
+            if constexpr (sizeof(Acc) == 64)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+            else
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+        }
 }
 
 // Scheduling of one sub-step: the TM+TN fragment reads of the next sub-step
@@ -175,8 +189,8 @@ enum { MODE_BF16 = 0, MODE_F32 = 1, MODE_PAIR = 2 };
 // the next arrival the first.  Sums move through agent-scope (L2-coherent)
 // 64-bit atomic stores and loads; the waits are bounded.
 // Returns true on the workgroup that writes the output.
-template <class T>
-__device__ bool pair_combine(f32x16_t (&acc)[T::TM][T::TN], unsigned long long* state, float* part,
+template <class T, class Acc>
+__device__ bool pair_combine(Acc (&acc)[T::TM][T::TN], unsigned long long* state, float* part,
                              unsigned long long epoch, int* role, int wave, int lane) {
     const unsigned long long tag = (epoch & 0xFFFFFFFFFFFFull) << 16;
     if (threadIdx.x == 0) {
@@ -198,15 +212,15 @@ __device__ bool pair_combine(f32x16_t (&acc)[T::TM][T::TN], unsigned long long* 
     const bool second = *role != 0;
     // this wave's region: [wave][i][j][q][lane] of f32x4
     unsigned long long* base =
-        reinterpret_cast<unsigned long long*>(part) + (size_t)wave * T::TM * T::TN * 4 * 64 * 2;
+        reinterpret_cast<unsigned long long*>(part) + (size_t)wave * T::TM * T::TN * T::ACC * 64 / 2;
     if (!second) {
 #pragma unroll
         for (int i = 0; i < T::TM; ++i)
 #pragma unroll
             for (int j = 0; j < T::TN; ++j)
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    unsigned long long* p = base + (((i * T::TN + j) * 4 + q) * 64 + lane) * 2;
+                for (int q = 0; q < T::ACC / 4; ++q) {
+                    unsigned long long* p = base + (((i * T::TN + j) * (T::ACC / 4) + q) * 64 + lane) * 2;
                     const unsigned long long lo =
                         (unsigned long long)__float_as_uint(acc[i][j][4 * q]) |
                         ((unsigned long long)__float_as_uint(acc[i][j][4 * q + 1]) << 32);
@@ -233,8 +247,8 @@ __device__ bool pair_combine(f32x16_t (&acc)[T::TM][T::TN], unsigned long long* 
 #pragma unroll
         for (int j = 0; j < T::TN; ++j)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const unsigned long long* p = base + (((i * T::TN + j) * 4 + q) * 64 + lane) * 2;
+            for (int q = 0; q < T::ACC / 4; ++q) {
+                const unsigned long long* p = base + (((i * T::TN + j) * (T::ACC / 4) + q) * 64 + lane) * 2;
                 const unsigned long long lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 const unsigned long long hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 acc[i][j][4 * q] += __uint_as_float((unsigned)lo);
@@ -250,7 +264,7 @@ __device__ bool pair_combine(f32x16_t (&acc)[T::TM][T::TN], unsigned long long* 
 
 // Matrices handed to this kernel hold fewer than 2^31 elements, so per-lane
 // load offsets fit in 32 bits (the launcher checks).
-template <int BM, int BN, int WM, int WN, int BK, int STAGES, int MODE>
+template <int BM, int BN, int WM, int WN, int BK, int STAGES, int MODE, int MI>
 __global__ __launch_bounds__(WM * WN * 64, 1)
 void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
                             const uint16_t* __restrict__ B, int64_t ldb,
@@ -258,7 +272,8 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
                             int R, int Cc, int D, int tiles_c, int ktiles_per_split,
                             int64_t split_stride, int map, unsigned long long* tile_state,
                             float* pair_part, unsigned long long epoch) {
-    using T = Cfg<BM, BN, WM, WN, BK, STAGES>;
+    using T = Cfg<BM, BN, WM, WN, BK, STAGES, MI>;
+    using Acc = typename AccOf<MI>::type;
     __shared__ __attribute__((aligned(1024))) unsigned char smem[T::SMEM];
 
     // XCD-contiguous tile order, then groups of 4 tile-rows walked by column
@@ -297,19 +312,19 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
     const unsigned ra = (unsigned)((uint64_t)R * lda * 2u);    // bytes of A's rows
     const unsigned rb = (unsigned)((uint64_t)Cc * ldb * 2u);   // bytes of B's rows
 
-    const int lr = lane & 31;
-    const int lh = lane >> 5;
-    const int sw = swz<T>(lr);                    // rows of a fragment are lr mod 32
+    const int lr = lane % MI;                     // fragment row
+    const int lh = lane / MI;                     // depth chunk within a sub-step
+    const int sw = swz<T>(lr);                    // the swizzle depends on the row mod 16
     const int a_off = (wrow0 + lr) * T::ROWB;
     const int b_off = (BM + wcol0 + lr) * T::ROWB;
 
-    f32x16_t acc[T::TM][T::TN];
+    Acc acc[T::TM][T::TN];
 #pragma unroll
     for (int i = 0; i < T::TM; ++i)
 #pragma unroll
         for (int j = 0; j < T::TN; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+            for (int v = 0; v < T::ACC; ++v) acc[i][j][v] = 0.f;
 
     bf16x8_t fa0[T::TM], fa1[T::TM];
     bf16x8_t fb0[T::TN], fb1[T::TN];
@@ -359,25 +374,25 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
 
     if constexpr (MODE == MODE_PAIR) {
         const int tile = tile_r * tiles_c + tile_c;
-        if (!pair_combine<T>(acc, tile_state + tile, pair_part + (size_t)tile * (BM * BN), epoch,
+        if (!pair_combine<T, Acc>(acc, tile_state + tile, pair_part + (size_t)tile * (BM * BN), epoch,
                              reinterpret_cast<int*>(smem), wave, lane))
             return;
     }
 
     // ---- epilogue ----------------------------------------------------------------
     // lane holds, for MFMA block (i, j) and group q = v/4, the output row
-    // wrow0 + 32i + lr and the 4 columns wcol0 + 32j + 8q + 4lh + {0..3}
+    // wrow0 + MI*i + lr and the 4 columns wcol0 + MI*j + 8q + 4lh + {0..3}
     if constexpr (MODE == MODE_F32) {
         float* C = reinterpret_cast<float*>(Cout) + blockIdx.y * split_stride;
 #pragma unroll
         for (int i = 0; i < T::TM; ++i) {
-            const int r = row0 + wrow0 + 32 * i + lr;
+            const int r = row0 + wrow0 + MI * i + lr;
             if (r >= R) continue;
 #pragma unroll
             for (int j = 0; j < T::TN; ++j) {
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int c = col0 + wcol0 + 32 * j + 8 * q + 4 * lh;
+                for (int q = 0; q < T::ACC / 4; ++q) {
+                    const int c = col0 + wcol0 + MI * j + 8 * q + 4 * lh;
                     f32x4_t v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
                                  acc[i][j][4 * q + 3]};
                     float* p = C + (int64_t)r * ldc + c;
@@ -398,12 +413,12 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
 #pragma unroll
             for (int j = 0; j < T::TN; ++j)
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
+                for (int q = 0; q < T::ACC / 4; ++q) {
                     u32x2_t v;
                     v[0] = pack_bf16x2(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
                     v[1] = pack_bf16x2(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-                    const int rl = 32 * i + lr;
-                    const int cl = 32 * j + 8 * q + 4 * lh;
+                    const int rl = MI * i + lr;
+                    const int cl = MI * j + 8 * q + 4 * lh;
                     *reinterpret_cast<u32x2_t*>(ep + rl * T::EPI_LD + cl * 2) = v;
                 }
         __syncthreads();
@@ -435,7 +450,7 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
     }
 }
 
-template <int BM, int BN, int WM, int WN, int BK, int STAGES>
+template <int BM, int BN, int WM, int WN, int BK, int STAGES, int MI = 32>
 hipError_t launch_v2(const GemmArgs& g, hipStream_t stream) {
     const int tiles_r = (g.R + BM - 1) / BM;
     const int tiles_c = (g.Cc + BN - 1) / BN;
@@ -445,7 +460,7 @@ hipError_t launch_v2(const GemmArgs& g, hipStream_t stream) {
     dim3 grid(tiles_r * tiles_c, S);
     dim3 block(WM * WN * 64);
     if (S == 1) {
-        hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_BF16>), grid, block,
+        hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_BF16, MI>), grid, block,
                            0, stream, g.A, g.lda, g.B, g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c,
                            ktps, (int64_t)0, g.variant >> 2, nullptr, nullptr, 0ull);
         return hipGetLastError();
@@ -456,14 +471,14 @@ hipError_t launch_v2(const GemmArgs& g, hipStream_t stream) {
         const int ntiles = tiles_r * tiles_c;
         unsigned long long* state =
             reinterpret_cast<unsigned long long*>(g.partial + (size_t)ntiles * BM * BN);
-        hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_PAIR>), grid, block,
+        hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_PAIR, MI>), grid, block,
                            0, stream, g.A, g.lda, g.B, g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c,
                            ktps, (int64_t)0, g.variant >> 2, state, g.partial, g.epoch);
         return hipGetLastError();
     }
     const int64_t ldp = splitk_ld(g.Cc);
     const int64_t split_stride = (int64_t)g.R * ldp;
-    hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_F32>), grid, block, 0,
+    hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_F32, MI>), grid, block, 0,
                        stream, g.A, g.lda, g.B, g.ldb, (void*)g.partial, ldp, g.R, g.Cc, g.D,
                        tiles_c, ktps, split_stride, g.variant >> 2, nullptr, nullptr, 0ull);
     hipError_t e = hipGetLastError();
@@ -486,12 +501,22 @@ void tile_dims(int tile, int* bm, int* bn) {
 }
 
 // variant bit 0 clear: depth step 32 with 4 LDS stages; set: depth step 64
-// with 2.  Bits 2-3: tile order (tile_coords).
+// with 2.  Bit 1 (with bit 0): 16x16x32 MFMA blocks for the eight-wave
+// tiles.  Bits 2-3: tile order (tile_coords).
 hipError_t launch_gemm_tn_bf16_v2(const GemmArgs& g, hipStream_t stream) {
     const int64_t lim = (int64_t)1 << 31;
     if ((int64_t)g.R * g.lda >= lim || (int64_t)g.Cc * g.ldb >= lim || g.c_f32)
         return launch_gemm_tn_bf16(g, stream);   // runs a pair plan as one depth range
     const bool deep = (g.variant & 1) == 0;
+    if (!deep && (g.variant & 2)) {
+        // 16x16x32 blocks: measured faster for the eight-wave tiles (5-6% on
+        // 4096 x 12288 x 1536), slower for the four-wave ones
+        switch (g.tile) {
+            case TILE_256x256_W8T: return launch_v2<256, 256, 4, 2, 64, 2, 16>(g, stream);
+            case TILE_256x192_W8: return launch_v2<256, 192, 4, 2, 64, 2, 16>(g, stream);
+            default: break;
+        }
+    }
     switch (g.tile) {
         case TILE_256x256:
             return deep ? launch_v2<256, 256, 2, 2, 32, 4>(g, stream)
