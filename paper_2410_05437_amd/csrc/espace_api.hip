@@ -414,10 +414,17 @@ espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, voi
         g.variant = tile_override().variant;
         g.pair = p.pair;
         if (p.pair) g.epoch = next_epoch();
-        e = p.kind == KIND_SKINNY ? espace::launch_skinny_tn_bf16(g, stream)
-                                  : (tile_override().kernel == 1 ? espace::launch_gemm_tn_bf16(g, stream)
-                                     : tile_override().kernel == 3 ? espace::launch_gemm_tn_bf16_pp(g, stream)
-                                                                   : espace::launch_gemm_tn_bf16_v2(g, stream));
+        const int kern = tile_override().kernel;
+        if (p.kind == KIND_SKINNY) {
+            e = espace::launch_skinny_tn_bf16(g, stream);
+        } else if (kern == 4 && (p.tile == espace::TILE_256x256_W8T || p.tile == espace::TILE_256x256)) {
+            e = espace::launch_gemm_tn_bf16_v3(g, stream);
+            if (e == hipErrorInvalidValue) e = espace::launch_gemm_tn_bf16_v2(g, stream);
+        } else {
+            e = kern == 1 ? espace::launch_gemm_tn_bf16(g, stream)
+                : kern == 3 ? espace::launch_gemm_tn_bf16_pp(g, stream)
+                            : espace::launch_gemm_tn_bf16_v2(g, stream);
+        }
     }
     if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
     return ESPACE_OK;
