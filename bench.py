@@ -118,8 +118,9 @@ def traffic_sources():
     expand GEMM (the kernel, its helpers and the tile planner)."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("paper_2410_05437_amd/csrc/gemm_bf16_v2.hip", "paper_2410_05437_amd/csrc/common.hpp",
-              "paper_2410_05437_amd/csrc/kernels.hpp", "paper_2410_05437_amd/csrc/espace_api.hip"):
+    for f in ("paper_2410_05437_amd/csrc/gemm_bf16_v3.hip", "paper_2410_05437_amd/csrc/gemm_bf16_v2.hip",
+              "paper_2410_05437_amd/csrc/common.hpp", "paper_2410_05437_amd/csrc/kernels.hpp",
+              "paper_2410_05437_amd/csrc/espace_api.hip"):
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()

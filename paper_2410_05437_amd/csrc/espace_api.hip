@@ -165,11 +165,13 @@ Plan plan_tiled(int R, int Cc, int D) {
 // Tuning overrides, read once per process: ESPACE_TILE=<shape name> and
 // ESPACE_SPLITK=<n> force the tiled configuration, ESPACE_PAIR=0|1 turns the
 // in-kernel combine of two depth halves off or on, ESPACE_TUNE_SHAPE=R,Cc,D
-// restricts those three to products of that shape; ESPACE_KERNEL=1|3 selects
-// the register-staged or the ping-pong kernel, ESPACE_VARIANT=<n> a kernel
-// variant, ESPACE_SKINNY=<kind> the small-N kernel.
+// restricts those three to products of that shape; ESPACE_KERNEL=1|2|3
+// selects the register-staged, the eight-wave direct-to-LDS or the ping-pong
+// kernel for every tiled product (default 4: the hand-ordered four-wave
+// kernel for 256 x 256 tiles, the direct-to-LDS kernel for the others),
+// ESPACE_VARIANT=<n> a kernel variant, ESPACE_SKINNY=<kind> the small-N kernel.
 struct Override {
-    int tile = -1, splits = 0, kernel = 2, variant = 3, skinny = -1, pair = -1;
+    int tile = -1, splits = 0, kernel = 4, variant = 3, skinny = -1, pair = -1;
     long long shape[3] = {-1, -1, -1};
     bool applies(int64_t R, int64_t Cc, int64_t D) const {
         return shape[0] < 0 || (shape[0] == R && shape[1] == Cc && shape[2] == D);

@@ -17,8 +17,8 @@ import os
 import sys
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-EXPAND_KERNEL = "gemm_tn_bf16_v2_kernel<256, 256, 4, 2"   # the 8-wave 256x256 tile
-EXPAND_GRID = 768 * 512                                    # workgroups x threads
+EXPAND_KERNEL = "gemm_tn_bf16_v3_kernel<0>"   # the four-wave 256x256 kernel, bf16 output
+EXPAND_GRID = 256 * 256                        # one workgroup of 256 threads per CU
 COPY_KERNELS = ("AUnaryFunctor<c10::BFloat16", "MulFunctor")   # torch.mul(bf16, 1.0)
 COPY_BYTES = 1 << 30
 
@@ -57,8 +57,8 @@ def stats(args):
     seg = [("expand, inside the timed projected-linear steps", big[:W + S]),
            ("expand, back-to-back loop (the roofline kernel; 2 warm-up launches)", big[W + S + 2:W + 2 * S + 2]),
            ("dense baseline", big[W + 2 * S + 2:2 * W + 3 * S + 2])]
-    lines += ["", "The 256x256 kernel at 768 workgroups serves both the expand GEMM (depth "
-              "L=1536) and the dense baseline (depth K=4096); split by position in bench.py's "
+    lines += ["", "The 256x256 kernel (one workgroup per CU, 768 tiles) serves both the expand GEMM "
+              "(depth L=1536) and the dense baseline (depth K=4096); split by position in bench.py's "
               "launch order:", "", "| launches | count | average (us) | median (us) |",
               "|---|---|---|---|"]
     for name, rs in seg:
