@@ -165,7 +165,8 @@ Plan plan_tiled(int R, int Cc, int D) {
 // Tuning overrides, read once per process: ESPACE_TILE=<shape name> and
 // ESPACE_SPLITK=<n> force the tiled configuration, ESPACE_PAIR=0|1 turns the
 // in-kernel combine of two depth halves off or on, ESPACE_TUNE_SHAPE=R,Cc,D
-// restricts those three to products of that shape; ESPACE_KERNEL=1|2|3
+// restricts those three (and ESPACE_SKINNY) to products of that shape;
+// ESPACE_KERNEL=1|2|3
 // selects the register-staged, the eight-wave direct-to-LDS or the ping-pong
 // kernel for every tiled product (default 4: the hand-ordered four-wave
 // kernel for 256 x 256 tiles, the direct-to-LDS kernel for the others),
@@ -212,6 +213,7 @@ Plan plan_tn(int64_t R, int64_t Cc, int64_t D, espace_dtype dt) {
     if (R <= 32) {
         Plan p = plan_skinny((int)R, (int)Cc, (int)D);
         const Override& o = tile_override();
+        if (!o.applies(R, Cc, D)) return p;
         if (o.skinny >= 0) p.tile = o.skinny;
         if (o.splits > 0) {
             p.splits = o.splits < ceil_div(D, 32) ? o.splits : (int)ceil_div(D, 32);
