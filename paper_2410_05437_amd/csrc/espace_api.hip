@@ -421,7 +421,8 @@ espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, voi
         const int kern = tile_override().kernel;
         if (p.kind == KIND_SKINNY) {
             e = espace::launch_skinny_tn_bf16(g, stream);
-        } else if (kern == 4 && (p.tile == espace::TILE_256x256_W8T || p.tile == espace::TILE_256x256)) {
+        } else if (kern == 4 && (p.tile == espace::TILE_256x256_W8T || p.tile == espace::TILE_256x256 ||
+                                 p.tile == espace::TILE_256x192_W8)) {
             e = espace::launch_gemm_tn_bf16_v3(g, stream);
             if (e == hipErrorInvalidValue) e = espace::launch_gemm_tn_bf16_v2(g, stream);
         } else {

@@ -60,8 +60,9 @@ inline int64_t splitk_ld(int Cc) { return (Cc + 7) / 8 * 8; }
 hipError_t launch_gemm_tn_bf16(const GemmArgs& g, hipStream_t stream);
 hipError_t launch_gemm_tn_bf16_v2(const GemmArgs& g, hipStream_t stream);
 hipError_t launch_gemm_tn_bf16_pp(const GemmArgs& g, hipStream_t stream);
-// Four-wave 256 x 256 kernel with a hand-ordered main loop; hipErrorInvalidValue
-// for products it does not take (pair combine, fp32 output, >= 2^31 elements).
+// Four-wave 256 x 256 and 256 x 192 kernel with a hand-ordered main loop;
+// hipErrorInvalidValue for products it does not take (other tiles, fp32
+// output, >= 2^31 elements).
 hipError_t launch_gemm_tn_bf16_v3(const GemmArgs& g, hipStream_t stream);
 hipError_t launch_skinny_tn_bf16(const GemmArgs& g, hipStream_t stream);
 hipError_t launch_splitk_reduce(const float* P, int S, int64_t split_stride, int64_t ldp,

@@ -307,9 +307,12 @@ def test_matrices_past_2g_elements(E):
 
 
 # (K, M, L, N) whose projection (N x L, depth K) the tile planner runs as two
-# depth halves combined inside the GEMM kernel, on the 128x192 and 256x128
-# tiles (the 256x192 tile takes this path in the Llama2-7B FFN-down workload)
-PAIR_SHAPES = [(1100, 600, 700, 1000), (4100, 500, 1100, 2500), (3003, 520, 1300, 2500)]
+# depth halves combined inside the GEMM kernel: on the 128x192 and 256x128
+# tiles, and on the four-wave 256x192 tile (also the Llama2-7B FFN-down
+# workload's plan), there with ragged rows, a column count that is not a
+# multiple of 8 and a depth tail
+PAIR_SHAPES = [(1100, 600, 700, 1000), (4100, 500, 1100, 2500), (3003, 520, 1300, 2500),
+               (4100, 300, 1536, 3000), (4100, 300, 1100, 4096)]
 
 
 @pytest.mark.parametrize("shape", PAIR_SHAPES, ids=lambda s: "K%d_M%d_L%d_N%d" % s)
@@ -338,12 +341,13 @@ def test_pair_combined_depth_halves(E, shape):
         assert torch.equal(E.espace_project(Pt, X, workspace=ws), Z), fill
 
 
-def test_pair_combine_under_graph_replay(E):
+@pytest.mark.parametrize("shape", [PAIR_SHAPES[0], PAIR_SHAPES[4]], ids=lambda s: "K%d_M%d_L%d_N%d" % s)
+def test_pair_combine_under_graph_replay(E, shape):
     """A captured projection that uses the pair combine replays correctly: each
     replay, with new inputs copied in between and eager work in between,
     matches the eager call bitwise."""
     dev = need_gpu()
-    K, M, L, N = PAIR_SHAPES[0]
+    K, M, L, N = shape
     inps = [_inputs(K, M, L, N, "bf16", seed=60 + i) for i in range(3)]
     X, Pt, _ = _dev_inputs(inps[0], dev)
     Z = out_mat(N, L, "bf16", dev)
