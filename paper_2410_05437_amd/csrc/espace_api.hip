@@ -169,7 +169,8 @@ Plan plan_tiled(int R, int Cc, int D) {
 // ESPACE_KERNEL=1|2|3
 // selects the register-staged, the eight-wave direct-to-LDS or the ping-pong
 // kernel for every tiled product (default 4: the hand-ordered four-wave
-// kernel for 256 x 256 tiles, the direct-to-LDS kernel for the others),
+// kernel for 256 x 256 and 256 x 192 tiles, the direct-to-LDS kernel for the
+// others),
 // ESPACE_VARIANT=<n> a kernel variant, ESPACE_SKINNY=<kind> the small-N kernel.
 struct Override {
     int tile = -1, splits = 0, kernel = 4, variant = 3, skinny = -1, pair = -1;

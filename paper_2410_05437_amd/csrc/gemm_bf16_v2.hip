@@ -187,7 +187,10 @@ enum { MODE_BF16 = 0, MODE_F32 = 1, MODE_PAIR = 2 };
 // arrived, 2 = its sums are ready, 3 = consumed; any other content (another
 // call, uninitialised memory, the previous replay of a captured launch) makes
 // the next arrival the first.  Sums move through agent-scope (L2-coherent)
-// 64-bit atomic stores and loads; the waits are bounded.
+// 64-bit atomic stores and loads; the waits are bounded.  Each 64-lane store
+// or load covers 512 contiguous bytes (values 4q, 4q+1 of every lane, then
+// 4q+2, 4q+3): these writes go through to memory, where partial cache lines
+// cost a read-modify-write.
 // Returns true on the workgroup that writes the output.
 template <class T, class Acc>
 __device__ bool pair_combine(Acc (&acc)[T::TM][T::TN], unsigned long long* state, float* part,
@@ -210,7 +213,7 @@ __device__ bool pair_combine(Acc (&acc)[T::TM][T::TN], unsigned long long* state
     }
     __syncthreads();
     const bool second = *role != 0;
-    // this wave's region: [wave][i][j][q][lane] of f32x4
+    // this wave's region: [wave][i][j][q][half][lane] of 8 bytes
     unsigned long long* base =
         reinterpret_cast<unsigned long long*>(part) + (size_t)wave * T::TM * T::TN * T::ACC * 64 / 2;
     if (!second) {
@@ -220,7 +223,7 @@ __device__ bool pair_combine(Acc (&acc)[T::TM][T::TN], unsigned long long* state
             for (int j = 0; j < T::TN; ++j)
 #pragma unroll
                 for (int q = 0; q < T::ACC / 4; ++q) {
-                    unsigned long long* p = base + (((i * T::TN + j) * (T::ACC / 4) + q) * 64 + lane) * 2;
+                    unsigned long long* p = base + ((i * T::TN + j) * (T::ACC / 4) + q) * 128 + lane;
                     const unsigned long long lo =
                         (unsigned long long)__float_as_uint(acc[i][j][4 * q]) |
                         ((unsigned long long)__float_as_uint(acc[i][j][4 * q + 1]) << 32);
@@ -228,7 +231,7 @@ __device__ bool pair_combine(Acc (&acc)[T::TM][T::TN], unsigned long long* state
                         (unsigned long long)__float_as_uint(acc[i][j][4 * q + 2]) |
                         ((unsigned long long)__float_as_uint(acc[i][j][4 * q + 3]) << 32);
                     __hip_atomic_store(p, lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    __hip_atomic_store(p + 1, hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(p + 64, hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
         __builtin_amdgcn_s_waitcnt(0);           // this wave's stores are complete
         __syncthreads();
@@ -248,9 +251,9 @@ __device__ bool pair_combine(Acc (&acc)[T::TM][T::TN], unsigned long long* state
         for (int j = 0; j < T::TN; ++j)
 #pragma unroll
             for (int q = 0; q < T::ACC / 4; ++q) {
-                const unsigned long long* p = base + (((i * T::TN + j) * (T::ACC / 4) + q) * 64 + lane) * 2;
+                const unsigned long long* p = base + ((i * T::TN + j) * (T::ACC / 4) + q) * 128 + lane;
                 const unsigned long long lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                const unsigned long long hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                const unsigned long long hi = __hip_atomic_load(p + 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 acc[i][j][4 * q] += __uint_as_float((unsigned)lo);
                 acc[i][j][4 * q + 1] += __uint_as_float((unsigned)(lo >> 32));
                 acc[i][j][4 * q + 2] += __uint_as_float((unsigned)hi);

@@ -52,6 +52,9 @@ struct V3Cfg {
     static constexpr int NMF = V3_NB * NBJ;               // MFMAs per sub-step
     static constexpr int NST = V3_NB * NBJ / 2;           // epilogue stores per wave
     static constexpr int SMEM = 4 * HS;
+    // row blocks of the partner's sums in flight in the pair epilogue: all
+    // of them where the registers allow (256 x 192), else one ahead
+    static constexpr int PD = BN == 192 ? V3_NB - 1 : 1;
     static_assert(ROWS % (16 * V3_NW) == 0 && 2 * NRD <= NMF && NBJ % 2 == 0, "tile");
     // MFMA after which wave-load y of a sub-step is issued
     static constexpr int load_slot(int y) { return y * NMF / LPH + NMF / (2 * LPH); }
@@ -225,11 +228,14 @@ __device__ __forceinline__ void v3_offsets(int* voff, int row0, int col0, int R,
 // uninitialised memory, the previous replay of a captured launch) makes the
 // next arrival the first.  Sums move through agent-scope (L2-coherent)
 // 64-bit atomic stores and loads; the waits are bounded.  The sums of a
-// wave sit at [wave][row block][column block][lane] (f32x4 each) of the
-// tile's area `part`.
+// wave sit at [wave][row block][column block][pair e][lane] of the tile's
+// area `part`, 8 bytes (values 2e and 2e + 1 of the lane's four) each, so
+// that every 64-lane store or load covers 512 contiguous bytes (whole cache
+// lines: these writes go through to memory, where partial lines cost a
+// read-modify-write).  Returns the lane's pair-0 word; pair 1 is 64 words on.
 __device__ inline unsigned long long* v3_part_at(float* part, int wave, int nbj, int i, int j, int lane) {
     return reinterpret_cast<unsigned long long*>(part) +
-           ((((size_t)wave * V3_NB + i) * nbj + j) * 64 + lane) * 2;
+           (((size_t)wave * V3_NB + i) * nbj + j) * 128 + lane;
 }
 
 // true on the workgroup that writes the output (the second to arrive),
@@ -265,7 +271,7 @@ __device__ bool v3_pair(const f32x4_t (&acc)[V3_NB][C::NBJ], unsigned long long*
                 __hip_atomic_store(p, (unsigned long long)__float_as_uint(v[0]) |
                                           ((unsigned long long)__float_as_uint(v[1]) << 32),
                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(p + 1, (unsigned long long)__float_as_uint(v[2]) |
+                __hip_atomic_store(p + 64, (unsigned long long)__float_as_uint(v[2]) |
                                               ((unsigned long long)__float_as_uint(v[3]) << 32),
                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
@@ -288,7 +294,7 @@ __device__ bool v3_pair(const f32x4_t (&acc)[V3_NB][C::NBJ], unsigned long long*
 __device__ inline f32x4_t v3_part_load(float* part, int wave, int nbj, int i, int j, int lane) {
     const unsigned long long* p = v3_part_at(part, wave, nbj, i, j, lane);
     const unsigned long long lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const unsigned long long hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned long long hi = __hip_atomic_load(p + 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return f32x4_t{__uint_as_float((unsigned)lo), __uint_as_float((unsigned)(lo >> 32)),
                    __uint_as_float((unsigned)hi), __uint_as_float((unsigned)(hi >> 32))};
 }
@@ -497,21 +503,23 @@ void gemm_tn_bf16_v3_kernel(const uint16_t* __restrict__ A, int64_t lda,
             tstate = tile_state + tile;
             if (!v3_pair<C>(acc, tstate, tpart, epoch, &pair_role, wave, lane)) return;
         }
-        // the first half's sums of row blocks i and i + 1 (pbuf[i & 1]): the
-        // loads of the next row block are issued before the current one is
-        // written, so their round trips overlap
-        f32x4_t pbuf[2][NBJ];
+        // the first half's sums of row blocks i .. i + C::PD - 1 are in
+        // flight while row block i is written (pbuf[i % (C::PD + 1)]), so
+        // that many device-scope round trips overlap
+        f32x4_t pbuf[C::PD + 1][NBJ];
         auto part_row = [&](int i) {
             if constexpr (MODE == V3_PAIR) {
 #pragma unroll
-                for (int j = 0; j < NBJ; ++j) pbuf[i & 1][j] = v3_part_load(tpart, wave, NBJ, i, j, lane);
+                for (int j = 0; j < NBJ; ++j)
+                    pbuf[i % (C::PD + 1)][j] = v3_part_load(tpart, wave, NBJ, i, j, lane);
             }
         };
-        part_row(0);
+#pragma unroll
+        for (int i = 0; i < C::PD; ++i) part_row(i);
         // the value of block (i, j) to write
         auto value = [&](int i, int j) -> f32x4_t {
             const f32x4_t a = v3_acc_read(acc[i][j]);
-            if constexpr (MODE == V3_PAIR) return a + pbuf[i & 1][j];
+            if constexpr (MODE == V3_PAIR) return a + pbuf[i % (C::PD + 1)][j];
             return a;
         };
         if constexpr (MODE == V3_F32) {
@@ -560,7 +568,7 @@ void gemm_tn_bf16_v3_kernel(const uint16_t* __restrict__ A, int64_t lda,
                 const auto crsrc = __builtin_amdgcn_make_buffer_rsrc((void*)Cb, (short)0, (int)cbytes, 0x00020000);
 #pragma unroll
                 for (int i = 0; i < V3_NB; ++i) {
-                    if (i + 1 < V3_NB) part_row(i + 1);
+                    if (i + C::PD < V3_NB) part_row(i + C::PD);
                     const int r = row0 + wrow0 + 16 * i + lr;
                     const unsigned rowoff = (unsigned)r * (unsigned)ldc;
 #pragma unroll
@@ -574,7 +582,7 @@ void gemm_tn_bf16_v3_kernel(const uint16_t* __restrict__ A, int64_t lda,
             } else {
 #pragma unroll
                 for (int i = 0; i < V3_NB; ++i) {
-                    if (i + 1 < V3_NB) part_row(i + 1);
+                    if (i + C::PD < V3_NB) part_row(i + C::PD);
                     const int r = row0 + wrow0 + 16 * i + lr;
 #pragma unroll
                     for (int m = 0; m < NBJ / 2; ++m) {

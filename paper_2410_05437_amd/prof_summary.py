@@ -17,7 +17,7 @@ import os
 import sys
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-EXPAND_KERNEL = "gemm_tn_bf16_v3_kernel<0>"   # the four-wave 256x256 kernel, bf16 output
+EXPAND_KERNEL = "gemm_tn_bf16_v3_kernel<0, 256>"   # the four-wave 256x256 kernel, bf16 output
 EXPAND_GRID = 256 * 256                        # one workgroup of 256 threads per CU
 COPY_KERNELS = ("AUnaryFunctor<c10::BFloat16", "MulFunctor")   # torch.mul(bf16, 1.0)
 COPY_BYTES = 1 << 30
