@@ -48,6 +48,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-calibration", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--kernel-probe", action="store_true",
@@ -293,6 +294,8 @@ def main():
 
     if not args.no_decode:
         detail["decode"] = decode_lines(E, acc, synth, dev, stream, args)
+    if not args.no_calibration:
+        detail["calibration"] = calibration_lines(E, Xs, dev, stream, args)
 
     cpu = None
     if not args.no_cpu:
@@ -321,6 +324,53 @@ def main():
         "detail": detail,
     }
     print(json.dumps(out), flush=True)
+
+
+def calibration_lines(E, Xs, dev, stream, args):
+    """Calibration of P for the Llama2-7B QKV layer (Section 3.1, Eq. 5;
+    Theorem 1): one autocorrelation update over a batch of 16384 tokens
+    (K=4096; the benchmark's 4096 synthetic tokens repeated four times), plain
+    and input-normalised, then the L=1536 principal components of C.  The
+    update computes the full K×K product: 2·K²·N flops."""
+    import torch
+    K = Xs.shape[1]
+    L = 1536
+    Xc = E.padded_empty(4 * Xs.shape[0], K, torch.bfloat16, dev)
+    for i in range(4):
+        Xc[i * Xs.shape[0]:(i + 1) * Xs.shape[0]].copy_(Xs)
+    Nc = Xc.shape[0]
+    C = torch.zeros(K, K, dtype=torch.float32, device=dev)
+    wsa = torch.empty(E.espace_workspace_bytes(E.OP_AUTOCORR, 0, K, 0, Nc, torch.bfloat16),
+                      dtype=torch.uint8, device=dev)
+    n = max(5, args.steps // 5)
+    ms = time_calls(lambda i: E.espace_autocorrelation_update(Xc, C, 1.0 / Nc, workspace=wsa), 1, n, 2, stream)
+    ms_n = time_calls(lambda i: E.espace_autocorrelation_update(Xc, C, 1.0 / Nc, normalize=True, workspace=wsa),
+                      1, n, 2, stream)
+    C.zero_()
+    E.espace_autocorrelation_update(Xc, C, 1.0 / Nc, workspace=wsa)
+    del wsa, Xc
+    wsp = torch.empty(E.espace_workspace_bytes(E.OP_PCA, 0, K, L, 0, torch.bfloat16), dtype=torch.uint8,
+                      device=dev)
+    pca = []
+    for _ in range(2):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        Pt, ev, info = E.espace_principal_components(C, L, workspace=wsp)
+        torch.cuda.synchronize()
+        pca.append(time.perf_counter() - t0)
+    flops = 2.0 * K * K * Nc
+    tf = flops / (ms * 1e-3) / 1e12
+    return {
+        "tokens": Nc, "K": K, "L": L,
+        "autocorr_us": round(ms * 1e3, 1),
+        "autocorr_tflops": round(tf, 1),
+        "autocorr_mfma_frac": round(tf / PEAK_BF16_TFLOPS, 4),
+        "autocorr_normalized_us": round(ms_n * 1e3, 1),
+        "pca_ms": round(pca[1] * 1e3, 1),
+        "pca_first_call_ms": round(pca[0] * 1e3, 1),
+        "pca_info": int(info.item()),
+        "eigenvalue_range": [float(ev[0]), float(ev[-1])],
+    }
 
 
 def decode_lines(E, acc, synth, dev, stream, args):

@@ -61,7 +61,7 @@
 extern "C" {
 #endif
 
-#define ESPACE_ABI_VERSION 1
+#define ESPACE_ABI_VERSION 2
 
 typedef enum {
     ESPACE_F32 = 0,
@@ -85,7 +85,9 @@ typedef enum {
     ESPACE_OP_PROJECT = 1,
     ESPACE_OP_EXPAND = 2,
     ESPACE_OP_PROJECTED_LINEAR = 3,
-    ESPACE_OP_DENSE = 4
+    ESPACE_OP_DENSE = 4,
+    ESPACE_OP_AUTOCORR = 5,    /* espace_autocorrelation_update: uses K, N */
+    ESPACE_OP_PCA = 6          /* espace_principal_components: uses K, L */
 } espace_op;
 
 /* Folded weight Wf = W·P (Section 2.2: the paper's PᵀW, "pre-computed before
@@ -145,6 +147,53 @@ espace_status espace_dense_linear(const void* X, int64_t ldx,
                                   espace_dtype dt,
                                   void* workspace, size_t workspace_bytes,
                                   hipStream_t stream);
+
+/* ---- Calibration of P (before deployment) --------------------------------
+ *
+ * Activation autocorrelation update (Section 3.1, Eq. 5; Corollary 1):
+ *
+ *        C += alpha · Σ_n x̂_n x̂_nᵀ      over the N tokens x_n (rows) of X,
+ *
+ * with x̂_n = x_n, or x̂_n = x_n / ||x_n||₂ when normalize != 0 (a zero token
+ * then contributes nothing).  With alpha = 1/(N_i·B) for each of B batches
+ * the calls accumulate Eq. 5's batch-averaged estimate C_X; with normalize,
+ * Corollary 1's input-normalised Ĉ_X.  C[r][c] += alpha·Σ_n x̂_n[r]·x̂_n[c].
+ * In: X [N][K] (ldx, dt).  In/out: C [K][K] (ldc, always float32; initialise
+ * it, e.g. to zero, before the first batch).  bf16: products of bfloat16
+ * values are exact in fp32 and summed in fp32; with normalize the scaled
+ * tokens are rounded to bfloat16 first (1/||x_n|| from an fp64 sum of
+ * squares).  f32: float32 throughout.  Limits: K·round_up(N, 8) and
+ * K·round_up(K, 8) below 2^31 (split larger batches into several calls).
+ * Needs espace_workspace_bytes(ESPACE_OP_AUTOCORR, 0, K, 0, N, dt). */
+espace_status espace_autocorrelation_update(const void* X, int64_t ldx,
+                                            float* C, int64_t ldc,
+                                            int64_t K, int64_t N,
+                                            int normalize, float alpha,
+                                            espace_dtype dt,
+                                            void* workspace, size_t workspace_bytes,
+                                            hipStream_t stream);
+
+/* Principal activation components (Theorem 1; Corollary 1 with Ĉ_X): row l
+ * of Pt is the eigenvector of the l-th largest eigenvalue of the symmetric
+ * C, for l < L, signed so that its entry of largest magnitude (the first
+ * such on ties) is positive.  Only the upper triangle of C (c >= r) is read.
+ * The decomposition runs in float64 (rocSOLVER's divide-and-conquer dsyevd,
+ * loaded at the first call; ESPACE_ERR_HIP if it cannot be loaded).
+ * In: C [K][K] (ldc, float32).  Out: Pt [L][K] (ldp, dt); eigenvalues: all K
+ * in decreasing order (float32, device, may be NULL); info: one device int
+ * (may be NULL), 0 on success, > 0 when the solver did not converge.
+ * Exception to the conventions above: the first call on a device creates a
+ * rocBLAS handle, and the solver may allocate device scratch of its own
+ * (kept by that handle), so the call is not for graph capture.
+ * Limits: K <= 32768.  Needs espace_workspace_bytes(ESPACE_OP_PCA, 0, K, L,
+ * 0, dt). */
+espace_status espace_principal_components(const float* C, int64_t ldc,
+                                          void* Pt, int64_t ldp,
+                                          float* eigenvalues, int* info,
+                                          int64_t K, int64_t L,
+                                          espace_dtype dt,
+                                          void* workspace, size_t workspace_bytes,
+                                          hipStream_t stream);
 
 /* Workspace bytes needed by `op` for these sizes (0 when none is needed).
  * Arguments an op does not use are ignored (e.g. L for ESPACE_OP_DENSE).

@@ -9,15 +9,19 @@ from ._lib import (  # noqa: F401
     ABI_VERSION,
     BF16,
     F32,
+    OP_AUTOCORR,
     OP_DENSE,
     OP_EXPAND,
     OP_FOLD,
     OP_PROJECT,
+    OP_PCA,
     OP_PROJECTED_LINEAR,
     EspaceError,
+    espace_autocorrelation_update,
     espace_dense_linear,
     espace_expand,
     espace_fold_weights,
+    espace_principal_components,
     espace_project,
     espace_projected_linear,
     espace_workspace_bytes,

@@ -18,7 +18,7 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "espace.h")
 
 F32 = 0
 BF16 = 1
-OP_FOLD, OP_PROJECT, OP_EXPAND, OP_PROJECTED_LINEAR, OP_DENSE = range(5)
+OP_FOLD, OP_PROJECT, OP_EXPAND, OP_PROJECTED_LINEAR, OP_DENSE, OP_AUTOCORR, OP_PCA = range(7)
 
 _c_i64 = ctypes.c_int64
 _c_p = ctypes.c_void_p
@@ -37,6 +37,10 @@ _SIGS = {
                                  _c_i64, _c_i64, _c_i64, _c_i64, _c_int, _c_p, _c_sz, _c_p], _c_int),
     "espace_dense_linear": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_i64, _c_i64,
                              _c_int, _c_p, _c_sz, _c_p], _c_int),
+    "espace_autocorrelation_update": ([_c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_i64, _c_int, ctypes.c_float,
+                                       _c_int, _c_p, _c_sz, _c_p], _c_int),
+    "espace_principal_components": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_p, _c_i64, _c_i64, _c_int, _c_p,
+                                     _c_sz, _c_p], _c_int),
     "espace_workspace_bytes": ([_c_int, _c_i64, _c_i64, _c_i64, _c_i64, _c_int], _c_sz),
     "espace_status_string": ([_c_int], ctypes.c_char_p),
     "espace_last_error": ([], ctypes.c_char_p),
@@ -216,3 +220,48 @@ def espace_dense_linear(X, W, Y=None, workspace=None):
                                        ctypes.c_void_p(ws.data_ptr() if ws is not None else 0),
                                        wsb, _stream(X.device)))
     return Y
+
+
+def espace_autocorrelation_update(X, C, alpha, normalize=False, workspace=None):
+    """C += alpha · Σ_n x̂_n x̂_nᵀ over the tokens (rows) of X [N][K]; x̂_n = x_n,
+    or x_n/||x_n|| with `normalize` (Section 3.1, Eq. 5; Corollary 1).  C is a
+    float32 [K][K] tensor updated in place."""
+    N, K = X.shape
+    if C.dtype != torch.float32 or tuple(C.shape) != (K, K):
+        raise ValueError(f"C must be a float32 {K}x{K} tensor")
+    ws, wsb = _ws(workspace, espace_workspace_bytes(OP_AUTOCORR, 0, K, 0, N, X.dtype), X.device)
+    px, ldx = _mat(X, "X")
+    pc, ldc = _mat(C, "C")
+    with torch.cuda.device(X.device):
+        _check(lib.espace_autocorrelation_update(px, ldx, pc, ldc, K, N, 1 if normalize else 0, float(alpha),
+                                                 _dt(X), ctypes.c_void_p(ws.data_ptr() if ws is not None else 0),
+                                                 wsb, _stream(X.device)))
+    return C
+
+
+def espace_principal_components(C, L, dtype=torch.bfloat16, Pt=None, eigenvalues=None, info=None,
+                                workspace=None):
+    """Pt [L][K]: the eigenvectors of the L largest eigenvalues of the
+    symmetric float32 C [K][K] (Theorem 1), each signed so that its entry of
+    largest magnitude is positive.  Returns (Pt, eigenvalues [K] decreasing,
+    info: a one-element int32 tensor, 0 on success)."""
+    K = C.shape[0]
+    if C.dtype != torch.float32 or tuple(C.shape) != (K, K):
+        raise ValueError("C must be a square float32 tensor")
+    if Pt is None:
+        Pt = padded_empty(L, K, dtype, C.device, 8 if dtype == torch.bfloat16 else 4)
+    if tuple(Pt.shape) != (L, K):
+        raise ValueError(f"Pt must be {L}x{K}")
+    if eigenvalues is None:
+        eigenvalues = torch.empty(K, dtype=torch.float32, device=C.device)
+    if info is None:
+        info = torch.zeros(1, dtype=torch.int32, device=C.device)
+    ws, wsb = _ws(workspace, espace_workspace_bytes(OP_PCA, 0, K, L, 0, Pt.dtype), C.device)
+    pc, ldc = _mat(C, "C")
+    pp, ldp = _mat(Pt, "Pt")
+    with torch.cuda.device(C.device):
+        _check(lib.espace_principal_components(pc, ldc, pp, ldp, ctypes.c_void_p(eigenvalues.data_ptr()),
+                                               ctypes.c_void_p(info.data_ptr()), K, L, _dt(Pt),
+                                               ctypes.c_void_p(ws.data_ptr() if ws is not None else 0), wsb,
+                                               _stream(C.device)))
+    return Pt, eigenvalues, info

@@ -1,0 +1,320 @@
+// Calibration of the projection (paper Section 3.1-3.2): the activation
+// autocorrelation C_X = E[x xᵀ] estimated from calibration batches (Eq. 5),
+// its input-normalised variant Ĉ_X (Corollary 1), and the projection made of
+// its L principal eigenvectors (Theorem 1).
+//
+//  * Autocorrelation update C += alpha · Σ_n x̂_n x̂_nᵀ over the M tokens of a
+//    batch X[M][K] (x̂_n = x_n, or x_n / ||x_n|| when normalising): the tokens
+//    are transposed (and scaled) into Xt[K][M] so that the sum over tokens is
+//    the contiguous dimension of a "TN" product Xt·Xtᵀ, which runs on the
+//    MFMA GEMM kernels with fp32 results per depth range; a last pass adds
+//    alpha times their sum to C in fixed order.
+//  * Principal components: C (fp32, upper triangle read) is widened to fp64
+//    and handed to rocSOLVER's symmetric divide-and-conquer eigensolver
+//    (dsyevd, loaded at the first call: the library is large and only
+//    calibration needs it); the eigenvectors of the L largest eigenvalues
+//    become the rows of Pt, each with the sign that makes its entry of largest
+//    magnitude positive.
+#include <dlfcn.h>
+#include <math.h>
+#include <mutex>
+
+#include <rocblas/rocblas.h>
+#include <rocsolver/rocsolver-extra-types.h>
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace espace {
+
+namespace {
+
+__device__ __forceinline__ float load_f(const uint16_t* p) { return bf16_to_f32(*p); }
+__device__ __forceinline__ float load_f(const float* p) { return *p; }
+__device__ __forceinline__ void store_f(uint16_t* p, float v) { *p = (uint16_t)bf16_rne(v); }
+__device__ __forceinline__ void store_f(float* p, float v) { *p = v; }
+
+// 1 / ||x_n|| for each token (0 for a zero token), the sum of squares in fp64.
+// One wave per token.
+template <typename T>
+__global__ __launch_bounds__(256) void token_inv_norm_kernel(const T* __restrict__ X, int64_t ldx, int M,
+                                                             int K, float* __restrict__ inv) {
+    const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (n >= M) return;
+    const T* row = X + (int64_t)n * ldx;
+    double s = 0.0;
+    for (int k = lane; k < K; k += 64) {
+        const double v = (double)load_f(row + k);
+        s += v * v;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+    if (lane == 0) inv[n] = s > 0.0 ? (float)(1.0 / sqrt(s)) : 0.f;
+}
+
+// Xt[k][n] = X[n][k] (times inv[n] when inv is given), rounded to T.  64 x 64
+// tiles through LDS so that both the reads and the writes are row-contiguous.
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_scale_kernel(const T* __restrict__ X, int64_t ldx,
+                                                              const float* __restrict__ inv,
+                                                              T* __restrict__ Xt, int64_t ldt, int M, int K) {
+    __shared__ float tile[64][65];
+    const int n0 = blockIdx.x * 64, k0 = blockIdx.y * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+#pragma unroll 4
+    for (int i = 0; i < 16; ++i) {
+        const int n = n0 + ty * 16 + i, k = k0 + tx;
+        float v = 0.f;
+        if (n < M && k < K) {
+            v = load_f(X + (int64_t)n * ldx + k);
+            if (inv) v *= inv[n];
+        }
+        tile[ty * 16 + i][tx] = v;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int i = 0; i < 16; ++i) {
+        const int k = k0 + ty * 16 + i, n = n0 + tx;
+        if (k < K && n < M) store_f(Xt + (int64_t)k * ldt + n, tile[tx][ty * 16 + i]);
+    }
+}
+
+// C[r][c] += alpha · Σ_s P_s[r][c], the depth ranges added in order.
+__global__ __launch_bounds__(256) void accumulate_kernel(const float* __restrict__ P, int S, int64_t stride,
+                                                         int64_t ldp, float* __restrict__ C, int64_t ldc,
+                                                         int R, int Cc, float alpha) {
+    const int64_t total = (int64_t)R * Cc;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int r = (int)(i / Cc), c = (int)(i % Cc);
+        float s = 0.f;
+        for (int q = 0; q < S; ++q) s += P[q * stride + (int64_t)r * ldp + c];
+        float* o = C + (int64_t)r * ldc + c;
+        *o = fmaf(alpha, s, *o);
+    }
+}
+
+// A[r][c] = C[r][c] in fp64 (K x K, leading dimension K).
+__global__ __launch_bounds__(256) void widen_kernel(const float* __restrict__ C, int64_t ldc,
+                                                    double* __restrict__ A, int K) {
+    const int64_t total = (int64_t)K * K;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int r = (int)(i / K), c = (int)(i % K);
+        A[i] = (double)C[(int64_t)r * ldc + c];
+    }
+}
+
+// Row l of Pt: the eigenvector of the l-th largest eigenvalue (column K-1-l
+// of the solver's column-major V, contiguous), signed so that its entry of
+// largest magnitude (the first such) is positive.  One workgroup per row;
+// workgroup 0 also writes the eigenvalues in decreasing order.
+template <typename T>
+__global__ __launch_bounds__(256) void select_kernel(const double* __restrict__ V, const double* __restrict__ D,
+                                                     int K, int L, T* __restrict__ Pt, int64_t ldp,
+                                                     float* __restrict__ evals) {
+    __shared__ double best_v[256];
+    __shared__ int best_i[256];
+    const int l = blockIdx.x;
+    const double* v = V + (int64_t)(K - 1 - l) * K;
+    double bv = -1.0;
+    int bi = K;
+    for (int k = threadIdx.x; k < K; k += 256) {
+        const double a = fabs(v[k]);
+        if (a > bv) { bv = a; bi = k; }       // first index of the largest within the thread
+    }
+    best_v[threadIdx.x] = bv;
+    best_i[threadIdx.x] = bi;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+        if (threadIdx.x < off) {
+            const double ov = best_v[threadIdx.x + off];
+            const int oi = best_i[threadIdx.x + off];
+            if (ov > best_v[threadIdx.x] || (ov == best_v[threadIdx.x] && oi < best_i[threadIdx.x])) {
+                best_v[threadIdx.x] = ov;
+                best_i[threadIdx.x] = oi;
+            }
+        }
+        __syncthreads();
+    }
+    const double sign = v[best_i[0]] < 0.0 ? -1.0 : 1.0;
+    for (int k = threadIdx.x; k < K; k += 256) store_f(Pt + (int64_t)l * ldp + k, (float)(sign * v[k]));
+    if (l == 0 && evals)
+        for (int i = threadIdx.x; i < K; i += 256) evals[i] = (float)D[K - 1 - i];
+}
+
+inline int ceil_div_i(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+// ---- rocSOLVER, loaded on first use ----------------------------------------
+
+typedef rocblas_status (*create_handle_fn)(rocblas_handle*);
+typedef rocblas_status (*set_stream_fn)(rocblas_handle, hipStream_t);
+typedef rocblas_status (*dsyevd_fn)(rocblas_handle, const rocblas_evect, const rocblas_fill, const rocblas_int,
+                                    double*, const rocblas_int, double*, double*, rocblas_int*);
+
+struct Solver {
+    bool ok = false;
+    create_handle_fn create = nullptr;
+    set_stream_fn set_stream = nullptr;
+    dsyevd_fn dsyevd = nullptr;
+    rocblas_handle handles[64] = {};   // one per device, created on first use
+    std::mutex mu;
+};
+
+Solver& solver() {
+    static Solver s;
+    static std::once_flag once;
+    std::call_once(once, [] {
+        void* blas = dlopen("librocblas.so.5", RTLD_NOW | RTLD_GLOBAL);
+        void* sol = dlopen("librocsolver.so.0", RTLD_NOW | RTLD_GLOBAL);
+        if (!blas || !sol) return;
+        s.create = (create_handle_fn)dlsym(blas, "rocblas_create_handle");
+        s.set_stream = (set_stream_fn)dlsym(blas, "rocblas_set_stream");
+        s.dsyevd = (dsyevd_fn)dlsym(sol, "rocsolver_dsyevd");
+        s.ok = s.create && s.set_stream && s.dsyevd;
+    });
+    return s;
+}
+
+}  // namespace
+
+size_t autocorr_workspace_bytes(int64_t M, int64_t K, bool f32) {
+    const int64_t ldt = (M + 7) / 8 * 8;
+    size_t b = (size_t)K * ldt * (f32 ? 4 : 2);               // Xt
+    b = (b + 255) / 256 * 256;
+    b += (size_t)((M + 63) / 64 * 64) * 4;                    // inverse norms
+    b = (b + 255) / 256 * 256;
+    b += (size_t)autocorr_ranges(M, K, f32) * K * splitk_ld((int)K) * 4;   // fp32 sums per depth range
+    return b;
+}
+
+int autocorr_ranges(int64_t M, int64_t K, bool f32) {
+    if (f32) return 1;
+    // enough depth ranges to give the chip ~256 workgroups, each range at
+    // least 16 steps of 64 tokens deep
+    const int64_t tiles = ((K + 255) / 256) * ((K + 255) / 256);
+    const int64_t steps = (M + 63) / 64;
+    int64_t S = 256 / tiles;
+    if (S > steps / 16) S = steps / 16;
+    if (S < 1) S = 1;
+    // the GEMM uses ceil(steps / ceil(steps / S)) non-empty ranges
+    const int64_t per = (steps + S - 1) / S;
+    return (int)((steps + per - 1) / per);
+}
+
+hipError_t launch_autocorr_update(const void* X, int64_t ldx, int M, int K, bool f32, bool normalize,
+                                  float alpha, float* C, int64_t ldc, void* workspace, hipStream_t stream) {
+    const int64_t ldt = (M + 7) / 8 * 8;
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    size_t off = (size_t)K * ldt * (f32 ? 4 : 2);
+    off = (off + 255) / 256 * 256;
+    float* inv = reinterpret_cast<float*>(ws + off);
+    off += (size_t)((M + 63) / 64 * 64) * 4;
+    off = (off + 255) / 256 * 256;
+    float* part = reinterpret_cast<float*>(ws + off);
+    const int S = autocorr_ranges(M, K, f32);
+    const int64_t ldp = splitk_ld(K);
+
+    if (normalize) {
+        if (f32)
+            hipLaunchKernelGGL(token_inv_norm_kernel<float>, dim3(ceil_div_i(M, 4)), dim3(256), 0, stream,
+                               static_cast<const float*>(X), ldx, M, K, inv);
+        else
+            hipLaunchKernelGGL(token_inv_norm_kernel<uint16_t>, dim3(ceil_div_i(M, 4)), dim3(256), 0, stream,
+                               static_cast<const uint16_t*>(X), ldx, M, K, inv);
+    }
+    const dim3 tgrid(ceil_div_i(M, 64), ceil_div_i(K, 64));
+    if (f32)
+        hipLaunchKernelGGL(transpose_scale_kernel<float>, tgrid, dim3(256), 0, stream, static_cast<const float*>(X),
+                           ldx, normalize ? inv : nullptr, reinterpret_cast<float*>(ws), ldt, M, K);
+    else
+        hipLaunchKernelGGL(transpose_scale_kernel<uint16_t>, tgrid, dim3(256), 0, stream,
+                           static_cast<const uint16_t*>(X), ldx, normalize ? inv : nullptr,
+                           reinterpret_cast<uint16_t*>(ws), ldt, M, K);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+
+    if (f32) {
+        const float* Xt = reinterpret_cast<const float*>(ws);
+        e = launch_gemm_tn_f32(Xt, ldt, Xt, ldt, part, ldp, K, K, M, stream);
+    } else {
+        GemmArgs g{};
+        g.A = reinterpret_cast<const uint16_t*>(ws);
+        g.lda = ldt;
+        g.B = g.A;
+        g.ldb = ldt;
+        g.R = K;
+        g.Cc = K;
+        g.D = M;
+        g.tile = TILE_256x256;
+        g.splits = S;
+        g.partial = part;
+        int used = 0;
+        e = launch_gemm_tn_bf16_v3_ranges(g, &used, stream);
+        if (e == hipSuccess && used != S) return hipErrorInvalidValue;
+    }
+    if (e != hipSuccess) return e;
+    const int64_t total = (int64_t)K * K;
+    const int blocks = (int)(total / 256 < 4096 ? (total + 255) / 256 : 4096);
+    hipLaunchKernelGGL(accumulate_kernel, dim3(blocks), dim3(256), 0, stream, part, S, (int64_t)K * ldp, ldp, C,
+                       ldc, K, K, alpha);
+    return hipGetLastError();
+}
+
+size_t pca_workspace_bytes(int64_t K) {
+    size_t b = (size_t)K * K * 8;          // the matrix, then its eigenvectors
+    b += (size_t)K * 8 * 2;                // eigenvalues, off-diagonal scratch
+    b += 256;                              // solver status
+    return (b + 255) / 256 * 256;
+}
+
+bool pca_available() { return solver().ok; }
+
+hipError_t launch_principal_components(const float* C, int64_t ldc, int K, int L, void* Pt, int64_t ldp,
+                                       bool f32, float* evals, int* info, void* workspace,
+                                       hipStream_t stream) {
+    Solver& s = solver();
+    if (!s.ok) return hipErrorSharedObjectInitFailed;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    double* A = reinterpret_cast<double*>(ws);
+    double* D = A + (int64_t)K * K;
+    double* E = D + K;
+    rocblas_int* st = reinterpret_cast<rocblas_int*>(E + K);
+    const int64_t total = (int64_t)K * K;
+    const int blocks = (int)(total / 256 < 4096 ? (total + 255) / 256 : 4096);
+    hipLaunchKernelGGL(widen_kernel, dim3(blocks), dim3(256), 0, stream, C, ldc, A, K);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    {
+        // one handle per device, shared by the calls on it: the stream is set
+        // and the solver enqueued under the lock
+        std::lock_guard<std::mutex> lk(s.mu);
+        if (!s.handles[dev] && s.create(&s.handles[dev]) != rocblas_status_success) {
+            s.handles[dev] = nullptr;
+            return hipErrorSharedObjectInitFailed;
+        }
+        rocblas_handle h = s.handles[dev];
+        if (s.set_stream(h, stream) != rocblas_status_success) return hipErrorInvalidHandle;
+        // A row-major is Aᵀ column-major; the lower triangle of that is the
+        // upper triangle (c >= r) of C
+        const rocblas_status rs = s.dsyevd(h, rocblas_evect_original, rocblas_fill_lower, K, A, K, D, E, st);
+        if (rs != rocblas_status_success) return hipErrorLaunchFailure;
+    }
+    if (f32)
+        hipLaunchKernelGGL(select_kernel<float>, dim3(L), dim3(256), 0, stream, A, D, K, L,
+                           static_cast<float*>(Pt), ldp, evals);
+    else
+        hipLaunchKernelGGL(select_kernel<uint16_t>, dim3(L), dim3(256), 0, stream, A, D, K, L,
+                           static_cast<uint16_t*>(Pt), ldp, evals);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (info) e = hipMemcpyAsync(info, st, sizeof(int), hipMemcpyDeviceToDevice, stream);
+    return e;
+}
+
+}  // namespace espace

@@ -296,6 +296,8 @@ size_t ws_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int64_t N, espace
         case ESPACE_OP_PROJECT: return N ? align_ws(plan_tn(N, L, K, dt).partial_bytes) : 0;
         case ESPACE_OP_EXPAND: return (N && M) ? align_ws(plan_tn(N, M, L, dt).partial_bytes) : 0;
         case ESPACE_OP_DENSE: return (N && M) ? align_ws(plan_tn(N, M, K, dt).partial_bytes) : 0;
+        case ESPACE_OP_AUTOCORR: return N ? align_ws(espace::autocorr_workspace_bytes(N, K, dt == ESPACE_F32)) : 0;
+        case ESPACE_OP_PCA: return align_ws(espace::pca_workspace_bytes(K));
         case ESPACE_OP_PROJECTED_LINEAR: {
             if (!N || !M) return 0;
             size_t a = plan_tn(N, L, K, dt).partial_bytes;
@@ -385,6 +387,15 @@ espace_status check_device() {
     return ESPACE_OK;
 }
 
+// the calibration GEMM indexes Xt [K][round_up(N, 8)] and the fp32 sums
+// [K][round_up(K, 8)] with 32-bit offsets
+bool autocorr_fits(int64_t K, int64_t N) {
+    const int64_t lim = (int64_t)1 << 31;
+    return K * ((N + 7) / 8 * 8) < lim && K * ((K + 7) / 8 * 8) < lim;
+}
+
+constexpr int64_t kMaxPcaDim = 32768;
+
 #define ESPACE_TRY(x)                       \
     do {                                    \
         espace_status _s = (x);             \
@@ -462,6 +473,14 @@ const char* espace_status_string(espace_status s) {
 size_t espace_workspace_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int64_t N,
                               espace_dtype dt) {
     if (dt != ESPACE_F32 && dt != ESPACE_BF16) return SIZE_MAX;
+    if (op == ESPACE_OP_AUTOCORR) {
+        if (K < 1 || N < 0 || K > kMaxDim || N > kMaxDim || !autocorr_fits(K, N)) return SIZE_MAX;
+        return ws_bytes(op, 0, K, 0, N, dt);
+    }
+    if (op == ESPACE_OP_PCA) {
+        if (K < 1 || K > kMaxPcaDim || L < 1 || L > K) return SIZE_MAX;
+        return ws_bytes(op, 0, K, L, 0, dt);
+    }
     const bool has_L = op != ESPACE_OP_DENSE;
     int64_t Kc = K;
     if (op == ESPACE_OP_EXPAND) Kc = L;       // expand has no K; L bounds itself
@@ -590,6 +609,64 @@ espace_status espace_dense_linear(const void* X, int64_t ldx, const void* W, int
     ESPACE_TRY(check_alias(mat_range("Y", Y, N, ldy, dt), ins, 3));
     ESPACE_TRY(check_device());
     ESPACE_TRY(run_tn(X, ldx, W, ldw, Y, ldy, N, M, K, dt, workspace, stream));
+    return ok();
+}
+
+espace_status espace_autocorrelation_update(const void* X, int64_t ldx, float* C, int64_t ldc, int64_t K,
+                                            int64_t N, int normalize, float alpha, espace_dtype dt,
+                                            void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    ESPACE_TRY(check_dtype(dt));
+    ESPACE_TRY(check_dims(0, K, 1, N, false));
+    if (N == 0) return ok();
+    if (!autocorr_fits(K, N))
+        return fail(ESPACE_ERR_SHAPE, "K=%lld, N=%lld too large for one update (split the batch)", (long long)K,
+                    (long long)N);
+    ESPACE_TRY(check_mat("X", X, N, K, ldx, dt));
+    ESPACE_TRY(check_mat("C", C, K, K, ldc, ESPACE_F32));
+    const size_t need = ws_bytes(ESPACE_OP_AUTOCORR, 0, K, 0, N, dt);
+    ESPACE_TRY(check_workspace(workspace, workspace_bytes, need));
+    const Range ins[] = {mat_range("X", X, N, ldx, dt),
+                         Range{"workspace", (uintptr_t)workspace, (uintptr_t)workspace + workspace_bytes}};
+    ESPACE_TRY(check_alias(mat_range("C", C, K, ldc, ESPACE_F32), ins, 2));
+    ESPACE_TRY(check_device());
+    const hipError_t e = espace::launch_autocorr_update(X, ldx, (int)N, (int)K, dt == ESPACE_F32, normalize != 0,
+                                                        alpha, C, ldc, workspace, stream);
+    if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "autocorrelation update: %s", hipGetErrorString(e));
+    return ok();
+}
+
+espace_status espace_principal_components(const float* C, int64_t ldc, void* Pt, int64_t ldp, float* eigenvalues,
+                                          int* info, int64_t K, int64_t L, espace_dtype dt, void* workspace,
+                                          size_t workspace_bytes, hipStream_t stream) {
+    ESPACE_TRY(check_dtype(dt));
+    ESPACE_TRY(check_dims(0, K, L, 0, true));
+    if (K > kMaxPcaDim) return fail(ESPACE_ERR_SHAPE, "K=%lld above %lld", (long long)K, (long long)kMaxPcaDim);
+    ESPACE_TRY(check_mat("C", C, K, K, ldc, ESPACE_F32));
+    ESPACE_TRY(check_mat("Pt", Pt, L, K, ldp, dt));
+    if ((uintptr_t)eigenvalues % 4) return fail(ESPACE_ERR_ALIGN, "eigenvalues: pointer not 4-byte aligned");
+    if ((uintptr_t)info % 4) return fail(ESPACE_ERR_ALIGN, "info: pointer not 4-byte aligned");
+    const size_t need = ws_bytes(ESPACE_OP_PCA, 0, K, L, 0, dt);
+    ESPACE_TRY(check_workspace(workspace, workspace_bytes, need));
+    const Range ws{"workspace", (uintptr_t)workspace, (uintptr_t)workspace + workspace_bytes};
+    const Range cr = mat_range("C", C, K, ldc, ESPACE_F32);
+    const Range pr = mat_range("Pt", Pt, L, ldp, dt);
+    const Range er{"eigenvalues", (uintptr_t)eigenvalues, (uintptr_t)eigenvalues + (eigenvalues ? K * 4 : 0)};
+    const Range ir{"info", (uintptr_t)info, (uintptr_t)info + (info ? 4 : 0)};
+    const Range for_pt[] = {cr, ws, er, ir};
+    ESPACE_TRY(check_alias(pr, for_pt, 4));
+    if (eigenvalues) {
+        const Range for_ev[] = {cr, ws, ir};
+        ESPACE_TRY(check_alias(er, for_ev, 3));
+    }
+    if (info) {
+        const Range for_info[] = {cr, ws};
+        ESPACE_TRY(check_alias(ir, for_info, 2));
+    }
+    ESPACE_TRY(check_device());
+    if (!espace::pca_available()) return fail(ESPACE_ERR_HIP, "rocSOLVER (librocsolver.so.0) could not be loaded");
+    const hipError_t e = espace::launch_principal_components(C, ldc, (int)K, (int)L, Pt, ldp, dt == ESPACE_F32,
+                                                             eigenvalues, info, workspace, stream);
+    if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "principal components: %s", hipGetErrorString(e));
     return ok();
 }
 

@@ -91,4 +91,20 @@ hipError_t launch_decode_fused(const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_gemm_tn_f32(const float* A, int64_t lda, const float* B, int64_t ldb,
                               float* C, int64_t ldc, int R, int Cc, int D, hipStream_t stream);
 
+// fp32 sums of the depth ranges of a 256 x 256 or 256 x 192 tiled product
+// (g.splits ranges requested; *ranges receives the number of non-empty ones),
+// range s at g.partial + s * R * splitk_ld(Cc); not combined.
+hipError_t launch_gemm_tn_bf16_v3_ranges(const GemmArgs& g, int* ranges, hipStream_t stream);
+
+// Calibration (autocorrelation of calibration tokens, principal components).
+int autocorr_ranges(int64_t M, int64_t K, bool f32);
+size_t autocorr_workspace_bytes(int64_t M, int64_t K, bool f32);
+hipError_t launch_autocorr_update(const void* X, int64_t ldx, int M, int K, bool f32, bool normalize,
+                                  float alpha, float* C, int64_t ldc, void* workspace, hipStream_t stream);
+size_t pca_workspace_bytes(int64_t K);
+bool pca_available();
+hipError_t launch_principal_components(const float* C, int64_t ldc, int K, int L, void* Pt, int64_t ldp,
+                                       bool f32, float* evals, int* info, void* workspace,
+                                       hipStream_t stream);
+
 }  // namespace espace

@@ -11,6 +11,7 @@ from .generate import (  # noqa: F401
     haar_orthogonal,
     index_pattern,
     spectrum,
+    symmetric_with_spectrum,
     gaussian_tokens,
     structured_tokens,
     silu_gated_tokens,

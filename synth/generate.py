@@ -15,7 +15,8 @@ Random streams: stream s of key k fills a row-major array in blocks of 2^20
 elements, block b drawn by a numpy Generator seeded with
 SeedSequence([241005437, k, s, b]) (blocks are independent, so large arrays
 are drawn by several threads); s = 0 (Q), 1 (evaluation tokens), 2 (W), 4/5
-(a/b evaluation), 6/7 (a/b calibration).  Tokens are drawn token by token, so
+(a/b evaluation), 6/7 (a/b calibration), 8 (rotation of a symmetric test
+matrix with a given spectrum).  Tokens are drawn token by token, so
 the first n tokens of a larger draw equal a draw of n tokens.
 
 For K >= 4096 on a machine with a GPU, the dense float64 linear algebra of the
@@ -156,6 +157,14 @@ def index_pattern(m, k):
     matrix of any size can be built on the device in pieces and any row of it
     recomputed on the host."""
     return ((m * 73 + k * 151) % 255 - 127) / 512.0
+
+
+def symmetric_with_spectrum(K, lam, key):
+    """K×K symmetric matrix Q·diag(lam)·Qᵀ, Q Haar-random from stream 8 of
+    `key` (float64, exactly symmetric): an input with known eigenvalues."""
+    Q = haar_orthogonal(K, rng_for(key, 8))
+    C = (Q * np.asarray(lam, dtype=np.float64)[None, :]) @ Q.T
+    return (C + C.T) / 2
 
 
 def spectrum(K, floor=0.0):

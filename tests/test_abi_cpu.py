@@ -19,10 +19,11 @@ def test_exports_every_declared_function():
     assert set(names) == {
         "espace_fold_weights", "espace_project", "espace_expand", "espace_projected_linear",
         "espace_dense_linear", "espace_workspace_bytes", "espace_status_string",
-        "espace_last_error", "espace_abi_version"}
+        "espace_last_error", "espace_abi_version", "espace_autocorrelation_update",
+        "espace_principal_components"}
     for n in names:
         assert hasattr(L, n)
-    assert E.ABI_VERSION == 1
+    assert E.ABI_VERSION == 2
 
 
 def _fold(W=P16, ldw=64, Pt=P16b, ldp=64, Wf=P16c, ldwf=16, M=32, K=64, Lc=16, dt=1,
@@ -88,3 +89,58 @@ def test_status_strings():
     for s in range(9):
         assert L.espace_status_string(s)
     assert isinstance(_lib.header_functions(), list)
+
+
+def _ac(X=P16, ldx=64, C=P16b, ldc=64, K=64, N=100, norm=0, alpha=1.0, dt=1,
+        ws=ctypes.c_void_p(0x70000000), wsb=1 << 24):
+    return L.espace_autocorrelation_update(X, ldx, C, ldc, K, N, norm, alpha, dt, ws, wsb, NULL)
+
+
+def _pca(C=P16, ldc=64, Pt=P16b, ldp=64, ev=P16c, info=ctypes.c_void_p(0x50000000), K=64, Lc=16, dt=1,
+         ws=ctypes.c_void_p(0x70000000), wsb=1 << 24):
+    return L.espace_principal_components(C, ldc, Pt, ldp, ev, info, K, Lc, dt, ws, wsb, NULL)
+
+
+def test_calibration_validation():
+    assert _ac(X=NULL) == 1
+    assert _ac(C=NULL) == 1
+    assert _ac(K=0) == 2
+    assert _ac(N=-1) == 2
+    assert _ac(ldc=60) == 2                                             # C ld < K
+    assert _ac(ldc=66) == 3                                             # C is float32: ld % 4
+    assert _ac(ldx=68) == 3                                             # bf16 X: ld % 8
+    assert _ac(dt=3) == 4
+    assert _ac(C=ctypes.c_void_p(0x10000 + 128)) == 5                   # C inside X
+    assert _ac(C=ctypes.c_void_p(0x70000000 + 256)) == 5                # C inside the workspace
+    assert _ac(ws=NULL, wsb=0) == 6
+    assert _ac(wsb=1024) == 6
+    assert _ac(K=1 << 16, ldx=1 << 16, ldc=1 << 16, N=10) == 2          # K·K above 2^31
+    assert _ac(N=0, X=NULL, ws=NULL, wsb=0) == 0                        # empty batch: nothing to do
+    assert _pca(C=NULL) == 1
+    assert _pca(Pt=NULL) == 1
+    assert _pca(Lc=0) == 2
+    assert _pca(Lc=65) == 2                                             # L > K
+    assert _pca(K=40000, ldc=40000, ldp=40000, Lc=10) == 2              # above the solver limit
+    assert _pca(ev=ctypes.c_void_p(0x30000002)) == 3
+    assert _pca(Pt=ctypes.c_void_p(0x10000 + 64)) == 5                  # Pt inside C
+    assert _pca(ev=ctypes.c_void_p(0x70000000)) == 5                    # eigenvalues in the workspace
+    assert _pca(ws=NULL, wsb=0) == 6
+    # every argument valid: the library asks the runtime for the device
+    assert _ac() in (7, 8)
+    assert _pca() in (7, 8)
+    assert _pca(ev=NULL, info=NULL) in (7, 8)
+
+
+def test_calibration_workspace_sizes():
+    bf16, f32 = 1, 0
+    ws = L.espace_workspace_bytes
+    K, N = 4096, 16384
+    # transposed tokens K x N (bf16), the inverse norms, fp32 sums of one depth range
+    assert ws(5, 0, K, 0, N, bf16) >= K * N * 2 + N * 4 + K * K * 4
+    assert ws(5, 0, K, 0, N, f32) >= K * N * 4 + K * K * 4
+    assert ws(5, 0, K, 0, 0, bf16) == 0
+    assert ws(5, 0, 0, 0, N, bf16) == ctypes.c_size_t(-1).value
+    # the eigensolver works on a float64 copy of C
+    assert ws(6, 0, K, 1536, 0, bf16) >= K * K * 8 + 2 * K * 8
+    assert ws(6, 0, K, K + 1, 0, bf16) == ctypes.c_size_t(-1).value
+    assert ws(6, 0, K, 0, 0, bf16) == ctypes.c_size_t(-1).value
