@@ -331,7 +331,8 @@ def calibration_lines(E, Xs, dev, stream, args):
     Theorem 1): one autocorrelation update over a batch of 16384 tokens
     (K=4096; the benchmark's 4096 synthetic tokens repeated four times), plain
     and input-normalised, then the L=1536 principal components of C.  The
-    update computes the full K×K product: 2·K²·N flops."""
+    product is symmetric: its algorithmic work is each distinct entry once,
+    K·(K+1)·N flops."""
     import torch
     K = Xs.shape[1]
     L = 1536
@@ -358,7 +359,7 @@ def calibration_lines(E, Xs, dev, stream, args):
         Pt, ev, info = E.espace_principal_components(C, L, workspace=wsp)
         torch.cuda.synchronize()
         pca.append(time.perf_counter() - t0)
-    flops = 2.0 * K * K * Nc
+    flops = float(K) * (K + 1) * Nc
     tf = flops / (ms * 1e-3) / 1e12
     return {
         "tokens": Nc, "K": K, "L": L,

@@ -7,8 +7,10 @@
 //    batch X[M][K] (x̂_n = x_n, or x_n / ||x_n|| when normalising): the tokens
 //    are transposed (and scaled) into Xt[K][M] so that the sum over tokens is
 //    the contiguous dimension of a "TN" product Xt·Xtᵀ, which runs on the
-//    MFMA GEMM kernels with fp32 results per depth range; a last pass adds
-//    alpha times their sum to C in fixed order.
+//    MFMA GEMM kernels with fp32 results per depth range; the product is
+//    symmetric, so (bf16) only the 256 x 256 tiles on and above the diagonal
+//    are computed, and a last pass adds alpha times the sum of the ranges to
+//    C in fixed order, reading the mirrored entry below the diagonal tiles.
 //  * Principal components: C (fp32, upper triangle read) is widened to fp64
 //    and handed to rocSOLVER's symmetric divide-and-conquer eigensolver
 //    (dsyevd, loaded at the first call: the library is large and only
@@ -80,16 +82,20 @@ __global__ __launch_bounds__(256) void transpose_scale_kernel(const T* __restric
     }
 }
 
-// C[r][c] += alpha · Σ_s P_s[r][c], the depth ranges added in order.
+// C[r][c] += alpha · Σ_s P_s[r][c], the depth ranges added in order.  With
+// tile > 0 only the tiles on and above the diagonal of P (tile x tile) hold
+// sums: an entry below them is read from its mirror P[c][r].
 __global__ __launch_bounds__(256) void accumulate_kernel(const float* __restrict__ P, int S, int64_t stride,
                                                          int64_t ldp, float* __restrict__ C, int64_t ldc,
-                                                         int R, int Cc, float alpha) {
+                                                         int R, int Cc, float alpha, int tile) {
     const int64_t total = (int64_t)R * Cc;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += (int64_t)gridDim.x * blockDim.x) {
         const int r = (int)(i / Cc), c = (int)(i % Cc);
+        const bool mirror = tile > 0 && r / tile > c / tile;
+        const int64_t at = mirror ? (int64_t)c * ldp + r : (int64_t)r * ldp + c;
         float s = 0.f;
-        for (int q = 0; q < S; ++q) s += P[q * stride + (int64_t)r * ldp + c];
+        for (int q = 0; q < S; ++q) s += P[q * stride + at];
         float* o = C + (int64_t)r * ldc + c;
         *o = fmaf(alpha, s, *o);
     }
@@ -191,9 +197,10 @@ size_t autocorr_workspace_bytes(int64_t M, int64_t K, bool f32) {
 
 int autocorr_ranges(int64_t M, int64_t K, bool f32) {
     if (f32) return 1;
-    // enough depth ranges to give the chip ~256 workgroups, each range at
-    // least 16 steps of 64 tokens deep
-    const int64_t tiles = ((K + 255) / 256) * ((K + 255) / 256);
+    // enough depth ranges to give the chip up to 256 workgroups in one
+    // round, each range at least 16 steps of 64 tokens deep
+    const int64_t n = (K + 255) / 256;
+    const int64_t tiles = n * (n + 1) / 2;
     const int64_t steps = (M + 63) / 64;
     int64_t S = 256 / tiles;
     if (S > steps / 16) S = steps / 16;
@@ -251,14 +258,14 @@ hipError_t launch_autocorr_update(const void* X, int64_t ldx, int M, int K, bool
         g.splits = S;
         g.partial = part;
         int used = 0;
-        e = launch_gemm_tn_bf16_v3_ranges(g, &used, stream);
+        e = launch_gemm_tn_bf16_v3_ranges(g, true, &used, stream);
         if (e == hipSuccess && used != S) return hipErrorInvalidValue;
     }
     if (e != hipSuccess) return e;
     const int64_t total = (int64_t)K * K;
     const int blocks = (int)(total / 256 < 4096 ? (total + 255) / 256 : 4096);
     hipLaunchKernelGGL(accumulate_kernel, dim3(blocks), dim3(256), 0, stream, part, S, (int64_t)K * ldp, ldp, C,
-                       ldc, K, K, alpha);
+                       ldc, K, K, alpha, f32 ? 0 : 256);
     return hipGetLastError();
 }
 

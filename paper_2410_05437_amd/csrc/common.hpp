@@ -79,11 +79,23 @@ __device__ __forceinline__ int xcd_contiguous(int bid, int nblocks) {
 
 // Output-tile coordinates of workgroup bid among tiles_r x tiles_c tiles.
 // map bit 0: skip the XCD remapping; bit 1: plain row-major order instead of
-// groups of GROUP tile-rows walked column by column.
+// groups of GROUP tile-rows walked column by column; bit 3: only the tiles on
+// and above the diagonal of a square tiling (nblocks = n(n+1)/2 for
+// tiles_c = n), row by row.
 template <int GROUP>
 __device__ __forceinline__ void tile_coords(int bid, int nblocks, int tiles_c, int map,
                                             int& tile_r, int& tile_c) {
     const int t = (map & 1) ? bid : xcd_contiguous(bid, nblocks);
+    if (map & 8) {
+        int r = 0, off = 0;
+        while (r < tiles_c - 1 && off + (tiles_c - r) <= t) {
+            off += tiles_c - r;
+            ++r;
+        }
+        tile_r = r;
+        tile_c = r + (t - off);
+        return;
+    }
     if (map & 2) {
         tile_r = t / tiles_c;
         tile_c = t - tile_r * tiles_c;

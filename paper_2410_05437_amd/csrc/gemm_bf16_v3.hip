@@ -664,10 +664,10 @@ hipError_t launch_v3(const GemmArgs& g, hipStream_t stream) {
 }
 
 template <int BN>
-hipError_t launch_v3_ranges(const GemmArgs& g, int* ranges, hipStream_t stream) {
+hipError_t launch_v3_ranges(const GemmArgs& g, bool upper, int* ranges, hipStream_t stream) {
     const int tiles_r = (g.R + V3_BM - 1) / V3_BM;
     const int tiles_c = (g.Cc + BN - 1) / BN;
-    const int ntiles = tiles_r * tiles_c;
+    const int ntiles = upper ? tiles_c * (tiles_c + 1) / 2 : tiles_r * tiles_c;
     const int ktiles = (g.D + V3_BK - 1) / V3_BK;
     const int S0 = g.splits < 1 ? 1 : g.splits;
     const int ktps = (ktiles + S0 - 1) / S0;
@@ -676,21 +676,24 @@ hipError_t launch_v3_ranges(const GemmArgs& g, int* ranges, hipStream_t stream) 
     const int64_t ldp = splitk_ld(g.Cc);
     hipLaunchKernelGGL((gemm_tn_bf16_v3_kernel<V3_F32, BN>), dim3(ntiles, S), dim3(V3_NW * 64), 0, stream, g.A,
                        g.lda, g.B, g.ldb, (void*)g.partial, ldp, g.R, g.Cc, g.D, tiles_c, ntiles, ktps,
-                       (int64_t)g.R * ldp, g.variant >> 2, nullptr, nullptr, 0ull);
+                       (int64_t)g.R * ldp, (g.variant >> 2) | (upper ? 8 : 0), nullptr, nullptr, 0ull);
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_gemm_tn_bf16_v3_ranges(const GemmArgs& g, int* ranges, hipStream_t stream) {
+hipError_t launch_gemm_tn_bf16_v3_ranges(const GemmArgs& g, bool upper, int* ranges, hipStream_t stream) {
     const int64_t lim = (int64_t)1 << 31;
     if ((int64_t)g.R * g.lda >= lim || (int64_t)g.Cc * g.ldb >= lim || g.D < 1 || !g.partial)
+        return hipErrorInvalidValue;
+    if (upper && (g.R != g.Cc || (g.tile != TILE_256x256 && g.tile != TILE_256x256_W8 &&
+                                  g.tile != TILE_256x256_W8T)))
         return hipErrorInvalidValue;
     switch (g.tile) {
         case TILE_256x256:
         case TILE_256x256_W8:
-        case TILE_256x256_W8T: return launch_v3_ranges<256>(g, ranges, stream);
-        case TILE_256x192_W8: return launch_v3_ranges<192>(g, ranges, stream);
+        case TILE_256x256_W8T: return launch_v3_ranges<256>(g, upper, ranges, stream);
+        case TILE_256x192_W8: return launch_v3_ranges<192>(g, upper, ranges, stream);
         default: return hipErrorInvalidValue;
     }
 }

@@ -93,8 +93,9 @@ hipError_t launch_gemm_tn_f32(const float* A, int64_t lda, const float* B, int64
 
 // fp32 sums of the depth ranges of a 256 x 256 or 256 x 192 tiled product
 // (g.splits ranges requested; *ranges receives the number of non-empty ones),
-// range s at g.partial + s * R * splitk_ld(Cc); not combined.
-hipError_t launch_gemm_tn_bf16_v3_ranges(const GemmArgs& g, int* ranges, hipStream_t stream);
+// range s at g.partial + s * R * splitk_ld(Cc); not combined.  upper (square
+// 256 x 256 tiling only): just the tiles on and above the diagonal.
+hipError_t launch_gemm_tn_bf16_v3_ranges(const GemmArgs& g, bool upper, int* ranges, hipStream_t stream);
 
 // Calibration (autocorrelation of calibration tokens, principal components).
 int autocorr_ranges(int64_t M, int64_t K, bool f32);
