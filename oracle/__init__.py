@@ -18,6 +18,8 @@ from .espace_ref import (  # noqa: F401
     autocorrelation,
     principal_components,
     normalized_autocorrelation,
+    gomse_matrix,
+    principal_components_by_magnitude,
 )
 from .brute import (  # noqa: F401
     bf_fold,

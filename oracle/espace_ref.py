@@ -143,3 +143,27 @@ def principal_components(C, L):
     d, V = np.linalg.eigh(_f64(C))
     order = np.argsort(d)[::-1]
     return np.ascontiguousarray(V[:, order[:L]].T), d[order]
+
+
+# -- GO-MSE candidates (Section 3.3: Proposition 1, Theorem 2) -------------------
+
+def gomse_matrix(CX, CW):
+    """Theorem 2, GO-MSE bound: C = E[x xᵀ w wᵀ + w wᵀ x xᵀ].  For weights and
+    activations drawn independently the expectation factors into
+    C_X·C_W + C_W·C_X (proof of Theorem 2, Appendix), with C_X the activation
+    autocorrelation and C_W = E[w wᵀ] the weight autocorrelation (rows of the
+    stored W as the vectors w).  With the L2-normalised autocorrelations of
+    both it is the normalised variant Ĉ of the same section."""
+    CX = _f64(CX)
+    CW = _f64(CW)
+    return CX @ CW + CW @ CX
+
+
+def principal_components_by_magnitude(C, L):
+    """Theorem 2's selection for a C that need not be positive semi-definite:
+    the L eigenvectors whose eigenvalues are largest in absolute value (proof
+    of Theorem 2, Appendix); equal magnitudes: the positive eigenvalue first.
+    Returns (Pt[L][K], all eigenvalues in that order)."""
+    d, V = np.linalg.eigh(_f64(C))
+    order = np.lexsort((-d, -np.abs(d)))
+    return np.ascontiguousarray(V[:, order[:L]].T), d[order]

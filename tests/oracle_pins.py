@@ -5,7 +5,8 @@ AssertionError when the oracle disagrees with the fact.  The pins do not
 re-type the oracle's formulas: they compare it with brute-force loop sums,
 with a different formula for the same quantity (Eq. 6 instead of Eq. 3),
 with special cases that reduce to a plain product, with exact results of
-permutation matrices, and with the identities of Theorem 1 and Proposition 1.
+permutation matrices, and with the identities of Theorem 1, Proposition 1
+and Theorem 2.
 """
 import itertools
 
@@ -272,6 +273,79 @@ def pin_rel_fro(o):
     assert o.rel_fro(ref, ref) == 0.0
 
 
+def pin_gomse_expectation(o):
+    """Theorem 2: over independent draws of x (the tokens of X) and w (the rows
+    of W) the average of x xᵀ w wᵀ + w wᵀ x xᵀ, summed pair by pair, is the
+    oracle's C_X·C_W + C_W·C_X; with unit-norm x and w, its normalised Ĉ."""
+    rng = _rng(1100)
+    K, N, M = 5, 7, 6
+    X = rng.standard_normal((N, K))
+    W = rng.standard_normal((M, K))
+    acc = np.zeros((K, K))
+    accn = np.zeros((K, K))
+    for n in range(N):
+        x = X[n]
+        xn = x / np.sqrt(sum(v * v for v in x))
+        for m in range(M):
+            w = W[m]
+            wn = w / np.sqrt(sum(v * v for v in w))
+            for i in range(K):
+                for j in range(K):
+                    # (x xᵀ w wᵀ)_ij = x_i (x·w) w_j, and its transpose
+                    xw = sum(x[k] * w[k] for k in range(K))
+                    acc[i, j] += x[i] * xw * w[j] + w[i] * xw * x[j]
+                    xwn = sum(xn[k] * wn[k] for k in range(K))
+                    accn[i, j] += xn[i] * xwn * wn[j] + wn[i] * xwn * xn[j]
+    _close(o.gomse_matrix(o.autocorrelation([X]), o.autocorrelation([W])), acc / (N * M),
+           rtol=1e-12, what="GO-MSE matrix")
+    _close(o.gomse_matrix(o.normalized_autocorrelation([X]), o.normalized_autocorrelation([W])),
+           accn / (N * M), rtol=1e-12, what="normalised GO-MSE matrix")
+
+
+def pin_gomse_bound_identity(o):
+    """Theorem 2's derivation: for any orthonormal P, the mean over pairs of
+    2<w,x><w,x̃> (the part of Proposition 1's bound that P controls) equals
+    Σ_i p_iᵀ C p_i; and when C's largest eigenvalues are also its largest in
+    magnitude, the selected P maximises it (no random orthonormal P does
+    better), i.e. minimises the bound."""
+    rng = _rng(1200)
+    K, N, M, L = 5, 40, 30, 2
+    X = rng.standard_normal((N, K)) @ rng.standard_normal((K, K))
+    W = rng.standard_normal((M, K)) @ rng.standard_normal((K, K))
+    C = o.gomse_matrix(o.autocorrelation([X]), o.autocorrelation([W]))
+
+    def q_pairs(Pt):
+        Xt = o.reconstruct(Pt, X)
+        return float(np.mean(2 * (X @ W.T) * (Xt @ W.T)))
+
+    def q_form(Pt):
+        return float(sum(p @ C @ p for p in np.asarray(Pt)))
+
+    for _ in range(20):
+        Pr = _orthonormal(K, L, rng).T.copy()
+        _close(q_pairs(Pr), q_form(Pr), rtol=1e-11, what="bound term vs quadratic form")
+    d = np.linalg.eigvalsh(C)
+    assert abs(d[0]) < d[-1] and abs(d[1]) < d[-2], "test matrix: top eigenvalues not the largest in magnitude"
+    Pt, _ = o.principal_components_by_magnitude(C, L)
+    best = q_pairs(Pt)
+    for _ in range(3000):
+        assert q_pairs(_orthonormal(K, L, rng).T.copy()) <= best + 1e-9, "random P beats Theorem 2"
+
+
+def pin_magnitude_order(o):
+    """Selection by absolute eigenvalue on a matrix of known spectrum: a
+    rotated diagonal with eigenvalues 3, -5, 1, -0.9, 0.5 gives -5, 3, 1,
+    -0.9, 0.5, and the rotated unit vectors."""
+    rng = _rng(1300)
+    Q = _orthonormal(5, 5, rng)
+    lam = np.array([3.0, -5.0, 1.0, -0.9, 0.5])
+    C = (Q * lam[None, :]) @ Q.T
+    Pt, d = o.principal_components_by_magnitude((C + C.T) / 2, 4)
+    _close(d, [-5.0, 3.0, 1.0, -0.9, 0.5], rtol=1e-12, what="order")
+    for row, col in zip(Pt, [1, 0, 2, 3]):
+        assert abs(abs(row @ Q[:, col]) - 1.0) < 1e-12, "eigenvector"
+
+
 ALL_PINS = [
     pin_brute_force,
     pin_associativity,
@@ -286,4 +360,7 @@ ALL_PINS = [
     pin_norm_and_bound,
     pin_sampled,
     pin_rel_fro,
+    pin_gomse_expectation,
+    pin_gomse_bound_identity,
+    pin_magnitude_order,
 ]

@@ -73,6 +73,20 @@ def _fold_skips_projection(W, Pt):
     return W[:, :L].copy()
 
 
+def _gomse_one_sided(CX, CW):
+    return np.asarray(CX, float) @ np.asarray(CW, float) * 2
+
+
+def _by_value(C, L):
+    return R.principal_components(C, L)
+
+
+def _by_magnitude_ascending(C, L):
+    d, V = np.linalg.eigh(np.asarray(C, float))
+    order = np.argsort(np.abs(d), kind="stable")
+    return np.ascontiguousarray(V[:, order[:L]].T), d[order]
+
+
 MUTANTS = {
     "fold uses Pt for P": {"fold": _fold_transposed_p},
     "fold ignores P": {"fold": _fold_skips_projection},
@@ -85,6 +99,9 @@ MUTANTS = {
     "autocorrelation pooled, not batch-averaged": {"autocorrelation": _autocorr_pooled},
     "reconstruct drops a term": {"reconstruct": _reconstruct_drops_term},
     "normalised autocorrelation not normalised": {"normalized_autocorrelation": _normalized_plain},
+    "GO-MSE matrix one-sided": {"gomse_matrix": _gomse_one_sided},
+    "selection by value, not magnitude": {"principal_components_by_magnitude": _by_value},
+    "selection by smallest magnitude": {"principal_components_by_magnitude": _by_magnitude_ascending},
 }
 
 
