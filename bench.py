@@ -330,9 +330,10 @@ def calibration_lines(E, Xs, dev, stream, args):
     """Calibration of P for the Llama2-7B QKV layer (Section 3.1, Eq. 5;
     Theorem 1): one autocorrelation update over a batch of 16384 tokens
     (K=4096; the benchmark's 4096 synthetic tokens repeated four times), plain
-    and input-normalised, then the L=1536 principal components of C.  The
-    product is symmetric: its algorithmic work is each distinct entry once,
-    K·(K+1)·N flops."""
+    and input-normalised, then the L=1536 principal components of C, and
+    Theorem 2's GO-MSE matrix C_X·C_W + C_W·C_X (an fp32 K×K×K product).  The
+    autocorrelation product is symmetric: its algorithmic work is each
+    distinct entry once, K·(K+1)·N flops."""
     import torch
     K = Xs.shape[1]
     L = 1536
@@ -359,6 +360,11 @@ def calibration_lines(E, Xs, dev, stream, args):
         Pt, ev, info = E.espace_principal_components(C, L, workspace=wsp)
         torch.cuda.synchronize()
         pca.append(time.perf_counter() - t0)
+    Cs = E.padded_empty(K, K, torch.float32, dev, 4)
+    wss = torch.empty(E.espace_workspace_bytes(E.OP_SYMPRODUCT, 0, K, 0, 0, torch.float32), dtype=torch.uint8,
+                      device=dev)
+    ms_sym = time_calls(lambda i: E.espace_symmetrized_product(C, C, Cs, wss), 1, 3, 1, stream)
+    del Cs, wss
     flops = float(K) * (K + 1) * Nc
     tf = flops / (ms * 1e-3) / 1e12
     return {
@@ -370,6 +376,8 @@ def calibration_lines(E, Xs, dev, stream, args):
         "pca_ms": round(pca[1] * 1e3, 1),
         "pca_first_call_ms": round(pca[0] * 1e3, 1),
         "pca_info": int(info.item()),
+        "gomse_product_ms": round(ms_sym, 2),
+        "gomse_product_tflops_f32": round(2.0 * K ** 3 / (ms_sym * 1e-3) / 1e12, 1),
         "eigenvalue_range": [float(ev[0]), float(ev[-1])],
     }
 

@@ -61,7 +61,7 @@
 extern "C" {
 #endif
 
-#define ESPACE_ABI_VERSION 2
+#define ESPACE_ABI_VERSION 3
 
 typedef enum {
     ESPACE_F32 = 0,
@@ -87,7 +87,8 @@ typedef enum {
     ESPACE_OP_PROJECTED_LINEAR = 3,
     ESPACE_OP_DENSE = 4,
     ESPACE_OP_AUTOCORR = 5,    /* espace_autocorrelation_update: uses K, N */
-    ESPACE_OP_PCA = 6          /* espace_principal_components: uses K, L */
+    ESPACE_OP_PCA = 6,         /* espace_principal_components: uses K, L */
+    ESPACE_OP_SYMPRODUCT = 7   /* espace_symmetrized_product: uses K */
 } espace_op;
 
 /* Folded weight Wf = W·P (Section 2.2: the paper's PᵀW, "pre-computed before
@@ -173,14 +174,31 @@ espace_status espace_autocorrelation_update(const void* X, int64_t ldx,
                                             void* workspace, size_t workspace_bytes,
                                             hipStream_t stream);
 
-/* Principal activation components (Theorem 1; Corollary 1 with Ĉ_X): row l
- * of Pt is the eigenvector of the l-th largest eigenvalue of the symmetric
- * C, for l < L, signed so that its entry of largest magnitude (the first
- * such on ties) is positive.  Only the upper triangle of C (c >= r) is read.
+/* GO-MSE candidate matrix (Section 3.3, Theorem 2): C = A·Bᵀ + B·Aᵀ, which
+ * for the symmetric autocorrelations A = C_X and B = C_W (the weight
+ * autocorrelation: espace_autocorrelation_update over the rows of W) is
+ * Theorem 2's C_X·C_W + C_W·C_X; with both normalised, its Ĉ.
+ * C[r][c] = Σ_k A[r][k]·B[c][k] + Σ_k B[r][k]·A[c][k], float32 throughout
+ * (one fp32 product, added to its transpose: C is exactly symmetric).
+ * In: A, B [K][K] (lda, ldb, float32).  Out: C [K][K] (ldc, float32).
+ * Needs espace_workspace_bytes(ESPACE_OP_SYMPRODUCT, 0, K, 0, 0, ESPACE_F32). */
+espace_status espace_symmetrized_product(const float* A, int64_t lda,
+                                         const float* B, int64_t ldb,
+                                         float* C, int64_t ldc, int64_t K,
+                                         void* workspace, size_t workspace_bytes,
+                                         hipStream_t stream);
+
+/* Principal activation components (Theorem 1; Corollary 1 with Ĉ_X;
+ * Theorem 2 with by_magnitude): row l of Pt is the eigenvector of the l-th
+ * largest eigenvalue of the symmetric C — with by_magnitude != 0, of the
+ * l-th largest in absolute value (the rule Theorem 2's proof gives when C is
+ * not positive semi-definite; equal magnitudes: the larger value first) —
+ * for l < L, signed so that its entry of largest magnitude (the first such on
+ * ties) is positive.  Only the upper triangle of C (c >= r) is read.
  * The decomposition runs in float64 (rocSOLVER's divide-and-conquer dsyevd,
  * loaded at the first call; ESPACE_ERR_HIP if it cannot be loaded).
  * In: C [K][K] (ldc, float32).  Out: Pt [L][K] (ldp, dt); eigenvalues: all K
- * in decreasing order (float32, device, may be NULL); info: one device int
+ * in the selection order (float32, device, may be NULL); info: one device int
  * (may be NULL), 0 on success, > 0 when the solver did not converge.
  * Exception to the conventions above: the first call on a device creates a
  * rocBLAS handle, and the solver may allocate device scratch of its own
@@ -190,7 +208,7 @@ espace_status espace_autocorrelation_update(const void* X, int64_t ldx,
 espace_status espace_principal_components(const float* C, int64_t ldc,
                                           void* Pt, int64_t ldp,
                                           float* eigenvalues, int* info,
-                                          int64_t K, int64_t L,
+                                          int64_t K, int64_t L, int by_magnitude,
                                           espace_dtype dt,
                                           void* workspace, size_t workspace_bytes,
                                           hipStream_t stream);

@@ -15,6 +15,7 @@ from ._lib import (  # noqa: F401
     OP_FOLD,
     OP_PROJECT,
     OP_PCA,
+    OP_SYMPRODUCT,
     OP_PROJECTED_LINEAR,
     EspaceError,
     espace_autocorrelation_update,
@@ -24,6 +25,7 @@ from ._lib import (  # noqa: F401
     espace_principal_components,
     espace_project,
     espace_projected_linear,
+    espace_symmetrized_product,
     espace_workspace_bytes,
     header_functions,
     lib,

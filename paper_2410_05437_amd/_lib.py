@@ -18,7 +18,7 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "espace.h")
 
 F32 = 0
 BF16 = 1
-OP_FOLD, OP_PROJECT, OP_EXPAND, OP_PROJECTED_LINEAR, OP_DENSE, OP_AUTOCORR, OP_PCA = range(7)
+OP_FOLD, OP_PROJECT, OP_EXPAND, OP_PROJECTED_LINEAR, OP_DENSE, OP_AUTOCORR, OP_PCA, OP_SYMPRODUCT = range(8)
 
 _c_i64 = ctypes.c_int64
 _c_p = ctypes.c_void_p
@@ -39,8 +39,9 @@ _SIGS = {
                              _c_int, _c_p, _c_sz, _c_p], _c_int),
     "espace_autocorrelation_update": ([_c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_i64, _c_int, ctypes.c_float,
                                        _c_int, _c_p, _c_sz, _c_p], _c_int),
-    "espace_principal_components": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_p, _c_i64, _c_i64, _c_int, _c_p,
-                                     _c_sz, _c_p], _c_int),
+    "espace_principal_components": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_p, _c_i64, _c_i64, _c_int, _c_int,
+                                     _c_p, _c_sz, _c_p], _c_int),
+    "espace_symmetrized_product": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_p, _c_sz, _c_p], _c_int),
     "espace_workspace_bytes": ([_c_int, _c_i64, _c_i64, _c_i64, _c_i64, _c_int], _c_sz),
     "espace_status_string": ([_c_int], ctypes.c_char_p),
     "espace_last_error": ([], ctypes.c_char_p),
@@ -239,12 +240,33 @@ def espace_autocorrelation_update(X, C, alpha, normalize=False, workspace=None):
     return C
 
 
+def espace_symmetrized_product(A, B, C=None, workspace=None):
+    """C = A·Bᵀ + B·Aᵀ for float32 [K][K] A and B: with the autocorrelations
+    C_X and C_W, Theorem 2's GO-MSE matrix C_X·C_W + C_W·C_X."""
+    K = A.shape[0]
+    for t, n in ((A, "A"), (B, "B")):
+        if t.dtype != torch.float32 or tuple(t.shape) != (K, K):
+            raise ValueError(f"{n} must be a float32 {K}x{K} tensor")
+    if C is None:
+        C = padded_empty(K, K, torch.float32, A.device, 4)
+    ws, wsb = _ws(workspace, espace_workspace_bytes(OP_SYMPRODUCT, 0, K, 0, 0, torch.float32), A.device)
+    pa, lda = _mat(A, "A")
+    pb, ldb = _mat(B, "B")
+    pc, ldc = _mat(C, "C")
+    with torch.cuda.device(A.device):
+        _check(lib.espace_symmetrized_product(pa, lda, pb, ldb, pc, ldc, K,
+                                              ctypes.c_void_p(ws.data_ptr() if ws is not None else 0), wsb,
+                                              _stream(A.device)))
+    return C
+
+
 def espace_principal_components(C, L, dtype=torch.bfloat16, Pt=None, eigenvalues=None, info=None,
-                                workspace=None):
+                                workspace=None, by_magnitude=False):
     """Pt [L][K]: the eigenvectors of the L largest eigenvalues of the
-    symmetric float32 C [K][K] (Theorem 1), each signed so that its entry of
-    largest magnitude is positive.  Returns (Pt, eigenvalues [K] decreasing,
-    info: a one-element int32 tensor, 0 on success)."""
+    symmetric float32 C [K][K] (Theorem 1) — largest in absolute value with
+    `by_magnitude` (Theorem 2) — each signed so that its entry of largest
+    magnitude is positive.  Returns (Pt, eigenvalues [K] in the selection
+    order, info: a one-element int32 tensor, 0 on success)."""
     K = C.shape[0]
     if C.dtype != torch.float32 or tuple(C.shape) != (K, K):
         raise ValueError("C must be a square float32 tensor")
@@ -261,7 +283,8 @@ def espace_principal_components(C, L, dtype=torch.bfloat16, Pt=None, eigenvalues
     pp, ldp = _mat(Pt, "Pt")
     with torch.cuda.device(C.device):
         _check(lib.espace_principal_components(pc, ldc, pp, ldp, ctypes.c_void_p(eigenvalues.data_ptr()),
-                                               ctypes.c_void_p(info.data_ptr()), K, L, _dt(Pt),
+                                               ctypes.c_void_p(info.data_ptr()), K, L, 1 if by_magnitude else 0,
+                                               _dt(Pt),
                                                ctypes.c_void_p(ws.data_ptr() if ws is not None else 0), wsb,
                                                _stream(C.device)))
     return Pt, eigenvalues, info

@@ -11,12 +11,17 @@
 //    symmetric, so (bf16) only the 256 x 256 tiles on and above the diagonal
 //    are computed, and a last pass adds alpha times the sum of the ranges to
 //    C in fixed order, reading the mirrored entry below the diagonal tiles.
+//  * GO-MSE candidate (Theorem 2): C = A·Bᵀ + B·Aᵀ, for the symmetric
+//    autocorrelations A = C_X and B = C_W the matrix C_X·C_W + C_W·C_X: one
+//    fp32 "TN" product A·Bᵀ, then C[r][c] = P[r][c] + P[c][r] (64 x 64 tiles
+//    of P and of its transpose through LDS), exactly symmetric.
 //  * Principal components: C (fp32, upper triangle read) is widened to fp64
 //    and handed to rocSOLVER's symmetric divide-and-conquer eigensolver
 //    (dsyevd, loaded at the first call: the library is large and only
-//    calibration needs it); the eigenvectors of the L largest eigenvalues
-//    become the rows of Pt, each with the sign that makes its entry of largest
-//    magnitude positive.
+//    calibration needs it); the eigenvectors of the L largest eigenvalues (or
+//    largest in magnitude, Theorem 2's rule for an indefinite C) become the
+//    rows of Pt, each with the sign that makes its entry of largest magnitude
+//    positive.
 #include <dlfcn.h>
 #include <math.h>
 #include <mutex>
@@ -112,18 +117,50 @@ __global__ __launch_bounds__(256) void widen_kernel(const float* __restrict__ C,
     }
 }
 
-// Row l of Pt: the eigenvector of the l-th largest eigenvalue (column K-1-l
-// of the solver's column-major V, contiguous), signed so that its entry of
-// largest magnitude (the first such) is positive.  One workgroup per row;
-// workgroup 0 also writes the eigenvalues in decreasing order.
+// C[r][c] = P[r][c] + P[c][r] for r, c < K: a 64 x 64 tile of P and the
+// mirrored tile, the latter read row-contiguously and transposed in LDS.
+__global__ __launch_bounds__(256) void symmetrize_kernel(const float* __restrict__ P, int64_t ldp,
+                                                         float* __restrict__ C, int64_t ldc, int K) {
+    __shared__ float t[64][65];
+    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+#pragma unroll 4
+    for (int i = 0; i < 16; ++i) {
+        const int rr = c0 + ty * 16 + i, cc = r0 + tx;      // P[c0 + i'][r0 + j']
+        t[ty * 16 + i][tx] = (rr < K && cc < K) ? P[(int64_t)rr * ldp + cc] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int i = 0; i < 16; ++i) {
+        const int r = r0 + ty * 16 + i, c = c0 + tx;
+        if (r < K && c < K) C[(int64_t)r * ldc + c] = P[(int64_t)r * ldp + c] + t[tx][ty * 16 + i];
+    }
+}
+
+// The order in which eigenvalues D (ascending, from the solver) are taken:
+// decreasing value, or decreasing magnitude (by_magnitude; from both ends of
+// D, the larger magnitude first, the upper end on ties).  One thread.
+__global__ void order_kernel(const double* __restrict__ D, int K, int by_magnitude, int* __restrict__ idx) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    int lo = 0, hi = K - 1;
+    for (int l = 0; l < K; ++l) {
+        if (!by_magnitude || fabs(D[hi]) >= fabs(D[lo])) idx[l] = hi--;
+        else idx[l] = lo++;
+    }
+}
+
+// Row l of Pt: the eigenvector of eigenvalue idx[l] (column idx[l] of the
+// solver's column-major V, contiguous), signed so that its entry of largest
+// magnitude (the first such) is positive.  One workgroup per row; workgroup
+// 0 also writes the eigenvalues in the order of idx.
 template <typename T>
 __global__ __launch_bounds__(256) void select_kernel(const double* __restrict__ V, const double* __restrict__ D,
-                                                     int K, int L, T* __restrict__ Pt, int64_t ldp,
-                                                     float* __restrict__ evals) {
+                                                     const int* __restrict__ idx, int K, int L,
+                                                     T* __restrict__ Pt, int64_t ldp, float* __restrict__ evals) {
     __shared__ double best_v[256];
     __shared__ int best_i[256];
     const int l = blockIdx.x;
-    const double* v = V + (int64_t)(K - 1 - l) * K;
+    const double* v = V + (int64_t)idx[l] * K;
     double bv = -1.0;
     int bi = K;
     for (int k = threadIdx.x; k < K; k += 256) {
@@ -147,7 +184,7 @@ __global__ __launch_bounds__(256) void select_kernel(const double* __restrict__ 
     const double sign = v[best_i[0]] < 0.0 ? -1.0 : 1.0;
     for (int k = threadIdx.x; k < K; k += 256) store_f(Pt + (int64_t)l * ldp + k, (float)(sign * v[k]));
     if (l == 0 && evals)
-        for (int i = threadIdx.x; i < K; i += 256) evals[i] = (float)D[K - 1 - i];
+        for (int i = threadIdx.x; i < K; i += 256) evals[i] = (float)D[idx[i]];
 }
 
 inline int ceil_div_i(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
@@ -273,13 +310,27 @@ size_t pca_workspace_bytes(int64_t K) {
     size_t b = (size_t)K * K * 8;          // the matrix, then its eigenvectors
     b += (size_t)K * 8 * 2;                // eigenvalues, off-diagonal scratch
     b += 256;                              // solver status
+    b += (size_t)K * 4;                    // selection order
     return (b + 255) / 256 * 256;
+}
+
+size_t symprod_workspace_bytes(int64_t K) { return (size_t)K * splitk_ld((int)K) * 4; }
+
+hipError_t launch_symmetrized_product(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
+                                      int64_t ldc, int K, void* workspace, hipStream_t stream) {
+    float* P = static_cast<float*>(workspace);
+    const int64_t ldp = splitk_ld(K);
+    hipError_t e = launch_gemm_tn_f32(A, lda, B, ldb, P, ldp, K, K, K, stream);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(symmetrize_kernel, dim3(ceil_div_i(K, 64), ceil_div_i(K, 64)), dim3(256), 0, stream, P,
+                       ldp, C, ldc, K);
+    return hipGetLastError();
 }
 
 bool pca_available() { return solver().ok; }
 
-hipError_t launch_principal_components(const float* C, int64_t ldc, int K, int L, void* Pt, int64_t ldp,
-                                       bool f32, float* evals, int* info, void* workspace,
+hipError_t launch_principal_components(const float* C, int64_t ldc, int K, int L, bool by_magnitude, void* Pt,
+                                       int64_t ldp, bool f32, float* evals, int* info, void* workspace,
                                        hipStream_t stream) {
     Solver& s = solver();
     if (!s.ok) return hipErrorSharedObjectInitFailed;
@@ -292,6 +343,7 @@ hipError_t launch_principal_components(const float* C, int64_t ldc, int K, int L
     double* D = A + (int64_t)K * K;
     double* E = D + K;
     rocblas_int* st = reinterpret_cast<rocblas_int*>(E + K);
+    int* idx = reinterpret_cast<int*>(reinterpret_cast<unsigned char*>(st) + 256);
     const int64_t total = (int64_t)K * K;
     const int blocks = (int)(total / 256 < 4096 ? (total + 255) / 256 : 4096);
     hipLaunchKernelGGL(widen_kernel, dim3(blocks), dim3(256), 0, stream, C, ldc, A, K);
@@ -312,11 +364,12 @@ hipError_t launch_principal_components(const float* C, int64_t ldc, int K, int L
         const rocblas_status rs = s.dsyevd(h, rocblas_evect_original, rocblas_fill_lower, K, A, K, D, E, st);
         if (rs != rocblas_status_success) return hipErrorLaunchFailure;
     }
+    hipLaunchKernelGGL(order_kernel, dim3(1), dim3(64), 0, stream, D, K, by_magnitude ? 1 : 0, idx);
     if (f32)
-        hipLaunchKernelGGL(select_kernel<float>, dim3(L), dim3(256), 0, stream, A, D, K, L,
+        hipLaunchKernelGGL(select_kernel<float>, dim3(L), dim3(256), 0, stream, A, D, idx, K, L,
                            static_cast<float*>(Pt), ldp, evals);
     else
-        hipLaunchKernelGGL(select_kernel<uint16_t>, dim3(L), dim3(256), 0, stream, A, D, K, L,
+        hipLaunchKernelGGL(select_kernel<uint16_t>, dim3(L), dim3(256), 0, stream, A, D, idx, K, L,
                            static_cast<uint16_t*>(Pt), ldp, evals);
     e = hipGetLastError();
     if (e != hipSuccess) return e;

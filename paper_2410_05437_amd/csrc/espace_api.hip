@@ -298,6 +298,7 @@ size_t ws_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int64_t N, espace
         case ESPACE_OP_DENSE: return (N && M) ? align_ws(plan_tn(N, M, K, dt).partial_bytes) : 0;
         case ESPACE_OP_AUTOCORR: return N ? align_ws(espace::autocorr_workspace_bytes(N, K, dt == ESPACE_F32)) : 0;
         case ESPACE_OP_PCA: return align_ws(espace::pca_workspace_bytes(K));
+        case ESPACE_OP_SYMPRODUCT: return align_ws(espace::symprod_workspace_bytes(K));
         case ESPACE_OP_PROJECTED_LINEAR: {
             if (!N || !M) return 0;
             size_t a = plan_tn(N, L, K, dt).partial_bytes;
@@ -395,6 +396,7 @@ bool autocorr_fits(int64_t K, int64_t N) {
 }
 
 constexpr int64_t kMaxPcaDim = 32768;
+constexpr int64_t kMaxSymDim = 46340;        // K·round_up(K, 8) < 2^31
 
 #define ESPACE_TRY(x)                       \
     do {                                    \
@@ -480,6 +482,10 @@ size_t espace_workspace_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int
     if (op == ESPACE_OP_PCA) {
         if (K < 1 || K > kMaxPcaDim || L < 1 || L > K) return SIZE_MAX;
         return ws_bytes(op, 0, K, L, 0, dt);
+    }
+    if (op == ESPACE_OP_SYMPRODUCT) {
+        if (K < 1 || K > kMaxSymDim) return SIZE_MAX;
+        return ws_bytes(op, 0, K, 0, 0, dt);
     }
     const bool has_L = op != ESPACE_OP_DENSE;
     int64_t Kc = K;
@@ -635,9 +641,28 @@ espace_status espace_autocorrelation_update(const void* X, int64_t ldx, float* C
     return ok();
 }
 
+espace_status espace_symmetrized_product(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
+                                         int64_t ldc, int64_t K, void* workspace, size_t workspace_bytes,
+                                         hipStream_t stream) {
+    ESPACE_TRY(check_dims(0, K, 1, 0, false));
+    if (K > kMaxSymDim) return fail(ESPACE_ERR_SHAPE, "K=%lld above %lld", (long long)K, (long long)kMaxSymDim);
+    ESPACE_TRY(check_mat("A", A, K, K, lda, ESPACE_F32));
+    ESPACE_TRY(check_mat("B", B, K, K, ldb, ESPACE_F32));
+    ESPACE_TRY(check_mat("C", C, K, K, ldc, ESPACE_F32));
+    const size_t need = ws_bytes(ESPACE_OP_SYMPRODUCT, 0, K, 0, 0, ESPACE_F32);
+    ESPACE_TRY(check_workspace(workspace, workspace_bytes, need));
+    const Range ins[] = {mat_range("A", A, K, lda, ESPACE_F32), mat_range("B", B, K, ldb, ESPACE_F32),
+                         Range{"workspace", (uintptr_t)workspace, (uintptr_t)workspace + workspace_bytes}};
+    ESPACE_TRY(check_alias(mat_range("C", C, K, ldc, ESPACE_F32), ins, 3));
+    ESPACE_TRY(check_device());
+    const hipError_t e = espace::launch_symmetrized_product(A, lda, B, ldb, C, ldc, (int)K, workspace, stream);
+    if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "symmetrized product: %s", hipGetErrorString(e));
+    return ok();
+}
+
 espace_status espace_principal_components(const float* C, int64_t ldc, void* Pt, int64_t ldp, float* eigenvalues,
-                                          int* info, int64_t K, int64_t L, espace_dtype dt, void* workspace,
-                                          size_t workspace_bytes, hipStream_t stream) {
+                                          int* info, int64_t K, int64_t L, int by_magnitude, espace_dtype dt,
+                                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
     ESPACE_TRY(check_dtype(dt));
     ESPACE_TRY(check_dims(0, K, L, 0, true));
     if (K > kMaxPcaDim) return fail(ESPACE_ERR_SHAPE, "K=%lld above %lld", (long long)K, (long long)kMaxPcaDim);
@@ -664,8 +689,8 @@ espace_status espace_principal_components(const float* C, int64_t ldc, void* Pt,
     }
     ESPACE_TRY(check_device());
     if (!espace::pca_available()) return fail(ESPACE_ERR_HIP, "rocSOLVER (librocsolver.so.0) could not be loaded");
-    const hipError_t e = espace::launch_principal_components(C, ldc, (int)K, (int)L, Pt, ldp, dt == ESPACE_F32,
-                                                             eigenvalues, info, workspace, stream);
+    const hipError_t e = espace::launch_principal_components(C, ldc, (int)K, (int)L, by_magnitude != 0, Pt, ldp,
+                                                             dt == ESPACE_F32, eigenvalues, info, workspace, stream);
     if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "principal components: %s", hipGetErrorString(e));
     return ok();
 }

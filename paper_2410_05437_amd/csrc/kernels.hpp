@@ -104,8 +104,11 @@ hipError_t launch_autocorr_update(const void* X, int64_t ldx, int M, int K, bool
                                   float alpha, float* C, int64_t ldc, void* workspace, hipStream_t stream);
 size_t pca_workspace_bytes(int64_t K);
 bool pca_available();
-hipError_t launch_principal_components(const float* C, int64_t ldc, int K, int L, void* Pt, int64_t ldp,
-                                       bool f32, float* evals, int* info, void* workspace,
+hipError_t launch_principal_components(const float* C, int64_t ldc, int K, int L, bool by_magnitude, void* Pt,
+                                       int64_t ldp, bool f32, float* evals, int* info, void* workspace,
                                        hipStream_t stream);
+size_t symprod_workspace_bytes(int64_t K);
+hipError_t launch_symmetrized_product(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
+                                      int64_t ldc, int K, void* workspace, hipStream_t stream);
 
 }  // namespace espace

@@ -20,10 +20,10 @@ def test_exports_every_declared_function():
         "espace_fold_weights", "espace_project", "espace_expand", "espace_projected_linear",
         "espace_dense_linear", "espace_workspace_bytes", "espace_status_string",
         "espace_last_error", "espace_abi_version", "espace_autocorrelation_update",
-        "espace_principal_components"}
+        "espace_principal_components", "espace_symmetrized_product"}
     for n in names:
         assert hasattr(L, n)
-    assert E.ABI_VERSION == 2
+    assert E.ABI_VERSION == 3
 
 
 def _fold(W=P16, ldw=64, Pt=P16b, ldp=64, Wf=P16c, ldwf=16, M=32, K=64, Lc=16, dt=1,
@@ -96,9 +96,13 @@ def _ac(X=P16, ldx=64, C=P16b, ldc=64, K=64, N=100, norm=0, alpha=1.0, dt=1,
     return L.espace_autocorrelation_update(X, ldx, C, ldc, K, N, norm, alpha, dt, ws, wsb, NULL)
 
 
-def _pca(C=P16, ldc=64, Pt=P16b, ldp=64, ev=P16c, info=ctypes.c_void_p(0x50000000), K=64, Lc=16, dt=1,
+def _pca(C=P16, ldc=64, Pt=P16b, ldp=64, ev=P16c, info=ctypes.c_void_p(0x50000000), K=64, Lc=16, mag=0, dt=1,
          ws=ctypes.c_void_p(0x70000000), wsb=1 << 24):
-    return L.espace_principal_components(C, ldc, Pt, ldp, ev, info, K, Lc, dt, ws, wsb, NULL)
+    return L.espace_principal_components(C, ldc, Pt, ldp, ev, info, K, Lc, mag, dt, ws, wsb, NULL)
+
+
+def _sym(A=P16, lda=64, B=P16b, ldb=64, C=P16c, ldc=64, K=64, ws=ctypes.c_void_p(0x70000000), wsb=1 << 24):
+    return L.espace_symmetrized_product(A, lda, B, ldb, C, ldc, K, ws, wsb, NULL)
 
 
 def test_calibration_validation():
@@ -125,7 +129,16 @@ def test_calibration_validation():
     assert _pca(Pt=ctypes.c_void_p(0x10000 + 64)) == 5                  # Pt inside C
     assert _pca(ev=ctypes.c_void_p(0x70000000)) == 5                    # eigenvalues in the workspace
     assert _pca(ws=NULL, wsb=0) == 6
+    assert _sym(A=NULL) == 1
+    assert _sym(K=0) == 2
+    assert _sym(ldc=62) == 2
+    assert _sym(ldb=66) == 3
+    assert _sym(C=ctypes.c_void_p(0x20000000 + 64)) == 5                # C inside B
+    assert _sym(ws=NULL, wsb=0) == 6
+    assert _sym(K=50000, lda=50000, ldb=50000, ldc=50000) == 2
     # every argument valid: the library asks the runtime for the device
+    assert _sym() in (7, 8)
+    assert _pca(mag=1) in (7, 8)
     assert _ac() in (7, 8)
     assert _pca() in (7, 8)
     assert _pca(ev=NULL, info=NULL) in (7, 8)
@@ -144,3 +157,6 @@ def test_calibration_workspace_sizes():
     assert ws(6, 0, K, 1536, 0, bf16) >= K * K * 8 + 2 * K * 8
     assert ws(6, 0, K, K + 1, 0, bf16) == ctypes.c_size_t(-1).value
     assert ws(6, 0, K, 0, 0, bf16) == ctypes.c_size_t(-1).value
+    # the symmetrised product keeps one fp32 K x K product
+    assert ws(7, 0, K, 0, 0, f32) == K * K * 4
+    assert ws(7, 0, 0, 0, 0, f32) == ctypes.c_size_t(-1).value

@@ -242,3 +242,81 @@ def test_llama2_7b_calibration_size(E):
     for l in [0, 1, 10, 100, 1000, L - 1]:
         r = C64 @ P[l] - e[l] * P[l]
         assert np.linalg.norm(r) <= 1e-5 * e[0], (l, float(np.linalg.norm(r)))
+
+
+# ---- GO-MSE candidates (Theorem 2) ------------------------------------------
+
+SYM_SIZES = [64, 300, 517, 1000]
+
+
+@pytest.mark.parametrize("K", SYM_SIZES)
+def test_symmetrized_product(E, K):
+    """C = A·Bᵀ + B·Aᵀ on symmetric A, B (float32 inputs given to both sides)
+    against the oracle's C_X·C_W + C_W·C_X, entry by entry within the fp32
+    rounding bound (K + 1)·2^-24·(S_ij + S_ji) + 2^-24·|C_ij|, S = |A|·|B|ᵀ
+    (the product's K fused multiply-adds, then one addition); the result is
+    exactly symmetric."""
+    dev = need_gpu()
+    A32 = synth.symmetric_with_spectrum(K, np.linspace(2.0, 0.01, K), 200 + K).astype(np.float32)
+    B32 = synth.symmetric_with_spectrum(K, 1.0 / (1.0 + np.arange(K)), 300 + K).astype(np.float32)
+    C = E.espace_symmetrized_product(dev_mat(A32, "f32", dev), dev_mat(B32, "f32", dev))
+    torch.cuda.synchronize()
+    got = host64(C)
+    A, B = A32.astype(np.float64), B32.astype(np.float64)
+    ref = oracle.gomse_matrix(A, B)
+    S = np.abs(A) @ np.abs(B).T
+    tol = (K + 1) * U32 * (S + S.T) + U32 * np.abs(ref)
+    assert (np.abs(got - ref) <= tol).all()
+    assert (got == got.T).all()
+
+
+def _mixed_spectrum(K, L):
+    lam = np.empty(K)
+    i = np.arange(L)
+    lam[:L] = (1.0 / (1.0 + i)) * np.where(i % 3 == 1, -1.0, 1.0)     # distinct magnitudes, mixed signs
+    lam[L:] = 1e-3 / (1.0 + np.arange(K - L)) * np.where(np.arange(K - L) % 2, -1.0, 1.0)
+    return lam
+
+
+@pytest.mark.parametrize("case", [(64, 16), (300, 40), (517, 100)], ids=lambda c: "K%d_L%d" % c)
+def test_principal_components_by_magnitude(E, case):
+    dev = need_gpu()
+    K, L = case
+    C32 = synth.symmetric_with_spectrum(K, _mixed_spectrum(K, L), 400 + K).astype(np.float32)
+    Pt, ev, info = E.espace_principal_components(dev_mat(C32, "f32", dev), L, dtype=torch.float32,
+                                                 by_magnitude=True)
+    torch.cuda.synchronize()
+    assert int(info.item()) == 0
+    Pt_ref, d_ref = oracle.principal_components_by_magnitude(C32.astype(np.float64), L)
+    got_ev = ev.cpu().numpy().astype(np.float64)
+    assert np.allclose(got_ev[:L], d_ref[:L], rtol=2 * U32, atol=1e-12)
+    assert np.all(np.diff(np.abs(got_ev[:L])) <= 0)
+    assert np.abs(host64(Pt) - _sign_fixed(Pt_ref)).max() <= 1e-6
+
+
+@pytest.mark.parametrize("normalize", [False, True], ids=["GO-MSE", "GO-MSE_hat"])
+def test_gomse_projection_end_to_end(E, normalize):
+    """Theorem 2 end to end on the GPU: C_X from the tokens, C_W from the rows
+    of W, C = C_X·C_W + C_W·C_X, P its L components of largest |eigenvalue|.
+    The oracle evaluates the part of Proposition 1's bound that P controls,
+    Σ_i p_iᵀ C p_i with its own C, for that P and for its own selection."""
+    dev = need_gpu()
+    K, M, N, L = 256, 512, 2000, 48
+    w = synth.Workload(cfg=-1, name="gomse", K=K, M=M, L=1, N=N, dtype="bf16", recipe="gaussian",
+                       lam_floor=1e-4, proj="leading", cov_key=5001, w_key=5002)
+    inp = synth.make_inputs(w)
+    CX = torch.zeros(K, K, dtype=torch.float32, device=dev)
+    CW = torch.zeros(K, K, dtype=torch.float32, device=dev)
+    E.espace_autocorrelation_update(dev_mat(inp.X_s, "bf16", dev), CX, 1.0 / N, normalize=normalize)
+    E.espace_autocorrelation_update(dev_mat(inp.W_s, "bf16", dev), CW, 1.0 / M, normalize=normalize)
+    C = E.espace_symmetrized_product(CX, CW)
+    Pt, ev, info = E.espace_principal_components(C, L, dtype=torch.float32, by_magnitude=True)
+    torch.cuda.synchronize()
+    assert int(info.item()) == 0
+    ac = oracle.normalized_autocorrelation if normalize else oracle.autocorrelation
+    Cref = oracle.gomse_matrix(ac([inp.X]), ac([inp.W]))
+    Pref, _ = oracle.principal_components_by_magnitude(Cref, L)
+    P = host64(Pt)
+    q = float(np.einsum("lk,kj,lj->", P, Cref, P))
+    qref = float(np.einsum("lk,kj,lj->", Pref, Cref, Pref))
+    assert abs(q - qref) <= 1e-4 * abs(qref), (q, qref)
