@@ -53,8 +53,20 @@ SHAPES = [
 ]
 
 
+# degenerate sizes: depth 1 (every step a masked tail), one output feature,
+# one token, L = K, a single partial tile
+DEGENERATE = [
+    (1, 1, 1, 1),
+    (1, 7, 1, 40),
+    (8, 3, 8, 33),
+    (64, 1, 1, 100),
+    (7, 100, 3, 1),
+    (32, 40, 32, 64),
+]
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "K%d_M%d_L%d_N%d" % s)
+@pytest.mark.parametrize("shape", SHAPES + DEGENERATE, ids=lambda s: "K%d_M%d_L%d_N%d" % s)
 def test_each_entry_point(E, dtype, shape):
     dev = need_gpu()
     K, M, L, N = shape
