@@ -20,6 +20,8 @@ from .espace_ref import (  # noqa: F401
     normalized_autocorrelation,
     gomse_matrix,
     principal_components_by_magnitude,
+    train_forward,
+    train_backward,
 )
 from .brute import (  # noqa: F401
     bf_fold,

@@ -167,3 +167,25 @@ def principal_components_by_magnitude(C, L):
     d, V = np.linalg.eigh(_f64(C))
     order = np.lexsort((-d, -np.abs(d)))
     return np.ascontiguousarray(V[:, order[:L]].T), d[order]
+
+
+# -- training view (Section 2.2, "during training/finetuning") -----------------
+
+def train_forward(X, Pt, W):
+    """The training view of the layer: W acts on the reconstructed activations,
+    Y = Wᵀ(PPᵀX) (Section 2.2, Eq. 3 read left to right), with P static and W
+    trainable.  Returns Y[N][M] and X̃[N][K] = (PPᵀX)ᵀ."""
+    Xt = reconstruct(Pt, X)
+    return Xt @ _f64(W).T, Xt
+
+
+def train_backward(dY, X, Pt, W):
+    """Gradients of the training view for an upstream gradient dY[N][M] = ∂ℓ/∂Y:
+    with X̃ = PPᵀX (P fixed), ∂ℓ/∂W = dYᵀ·X̃ (paper orientation: X̃·dYᵀ) and
+    ∂ℓ/∂X = PPᵀ·(W·dY) (PPᵀ is symmetric).  Returns (dX[N][K], dW[M][K])."""
+    dY = _f64(dY)
+    W = _f64(W)
+    Xt = reconstruct(Pt, X)
+    dW = dY.T @ Xt
+    dX = reconstruct(Pt, dY @ W)
+    return dX, dW

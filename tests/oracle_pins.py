@@ -346,6 +346,36 @@ def pin_magnitude_order(o):
         assert abs(abs(row @ Q[:, col]) - 1.0) < 1e-12, "eigenvector"
 
 
+def pin_training_gradients(o):
+    """The training view's gradients against central finite differences of the
+    scalar loss ℓ = Σ R ⊙ Y(X, W) (so ∂ℓ/∂Y = R), entry by entry, and its
+    forward against the inference form (PᵀW)ᵀ(PᵀX) (associativity)."""
+    rng = _rng(1400)
+    K, M, L, N = 6, 4, 3, 5
+    X = rng.standard_normal((N, K))
+    W = rng.standard_normal((M, K))
+    Pt = _orthonormal(K, L, rng).T.copy()
+    R = rng.standard_normal((N, M))
+    Y, _ = o.train_forward(X, Pt, W)
+    _close(Y, o.projected_linear_from_weights(X, Pt, W), rtol=1e-12, what="training forward")
+    dX, dW = o.train_backward(R, X, Pt, W)
+
+    def loss(Xv, Wv):
+        return float(np.sum(R * o.train_forward(Xv, Pt, Wv)[0]))
+
+    h = 1e-6
+    for (n, k) in itertools.product(range(N), range(K)):
+        Xp, Xm = X.copy(), X.copy()
+        Xp[n, k] += h
+        Xm[n, k] -= h
+        assert abs((loss(Xp, W) - loss(Xm, W)) / (2 * h) - dX[n, k]) < 1e-7, ("dX", n, k)
+    for (m, k) in itertools.product(range(M), range(K)):
+        Wp, Wm = W.copy(), W.copy()
+        Wp[m, k] += h
+        Wm[m, k] -= h
+        assert abs((loss(X, Wp) - loss(X, Wm)) / (2 * h) - dW[m, k]) < 1e-7, ("dW", m, k)
+
+
 ALL_PINS = [
     pin_brute_force,
     pin_associativity,
@@ -363,4 +393,5 @@ ALL_PINS = [
     pin_gomse_expectation,
     pin_gomse_bound_identity,
     pin_magnitude_order,
+    pin_training_gradients,
 ]

@@ -87,6 +87,18 @@ def _by_magnitude_ascending(C, L):
     return np.ascontiguousarray(V[:, order[:L]].T), d[order]
 
 
+def _train_bwd_no_projection(dY, X, Pt, W):
+    dY = np.asarray(dY, float)
+    W = np.asarray(W, float)
+    Xt = R.reconstruct(Pt, X)
+    return dY @ W, dY.T @ Xt
+
+
+def _train_bwd_dw_raw_x(dY, X, Pt, W):
+    dX, _ = R.train_backward(dY, X, Pt, W)
+    return dX, np.asarray(dY, float).T @ np.asarray(X, float)
+
+
 MUTANTS = {
     "fold uses Pt for P": {"fold": _fold_transposed_p},
     "fold ignores P": {"fold": _fold_skips_projection},
@@ -102,6 +114,8 @@ MUTANTS = {
     "GO-MSE matrix one-sided": {"gomse_matrix": _gomse_one_sided},
     "selection by value, not magnitude": {"principal_components_by_magnitude": _by_value},
     "selection by smallest magnitude": {"principal_components_by_magnitude": _by_magnitude_ascending},
+    "training dX skips the projection": {"train_backward": _train_bwd_no_projection},
+    "training dW from unprojected X": {"train_backward": _train_bwd_dw_raw_x},
 }
 
 
