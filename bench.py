@@ -49,6 +49,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-calibration", action="store_true")
+    ap.add_argument("--no-training", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--kernel-probe", action="store_true",
@@ -296,6 +297,8 @@ def main():
         detail["decode"] = decode_lines(E, acc, synth, dev, stream, args)
     if not args.no_calibration:
         detail["calibration"] = calibration_lines(E, Xs, dev, stream, args)
+    if not args.no_training:
+        detail["training"] = training_lines(E, Xs, Pts, Ws, dev, stream, args)
 
     cpu = None
     if not args.no_cpu:
@@ -324,6 +327,51 @@ def main():
         "detail": detail,
     }
     print(json.dumps(out), flush=True)
+
+
+def training_lines(E, Xs, Pts, Ws, dev, stream, args):
+    """One training step of the Llama2-7B QKV layer in the training view
+    (Section 2.2; P fixed, W learnt): fold W·P, project, expand, then the
+    gradients dX and dW; against the dense layer's step (forward, dX, dW), both
+    on this library's kernels, with a synthetic upstream gradient."""
+    import torch
+    N, K = Xs.shape
+    M, L = Ws.shape[0], Pts.shape[0]
+    bf = torch.bfloat16
+    dY = E.padded_empty(N, M, bf, dev)
+    dY.copy_(torch.randn(N, M, device=dev) / M ** 0.5)
+    Wf = E.padded_empty(M, L, bf, dev)
+    Z = E.padded_empty(N, L, bf, dev)
+    Y = E.padded_empty(N, M, bf, dev)
+    dX = E.padded_empty(N, K, bf, dev)
+    dW = E.padded_empty(M, K, bf, dev)
+    ws = {op: torch.empty(max(E.espace_workspace_bytes(op, M, K, L, N, bf), 1), dtype=torch.uint8, device=dev)
+          for op in (E.OP_FOLD, E.OP_PROJECT, E.OP_EXPAND, E.OP_BACKWARD, E.OP_DENSE, E.OP_DENSE_BACKWARD)}
+
+    def espace_step(i):
+        E.espace_fold_weights(Ws, Pts, Wf, ws[E.OP_FOLD])
+        E.espace_project(Pts, Xs, Z, ws[E.OP_PROJECT])
+        E.espace_expand(Z, Wf, Y, ws[E.OP_EXPAND])
+        E.espace_projected_linear_backward(dY, Z, Pts, Wf, dX, dW, workspace=ws[E.OP_BACKWARD])
+
+    def dense_step(i):
+        E.espace_dense_linear(Xs, Ws, Y, ws[E.OP_DENSE])
+        E.espace_dense_linear_backward(dY, Xs, Ws, dX, dW, workspace=ws[E.OP_DENSE_BACKWARD])
+
+    n = max(5, args.steps // 5)
+    ms_e = time_calls(espace_step, 1, n, 2, stream)
+    ms_d = time_calls(dense_step, 1, n, 2, stream)
+    fl_e = 2.0 * (M * K * L + N * L * K + N * M * L) + 2.0 * (N * M * L + N * L * K + M * N * L + M * L * K)
+    fl_d = 3 * 2.0 * M * K * N
+    return {
+        "espace_step_us": round(ms_e * 1e3, 1),
+        "dense_step_us": round(ms_d * 1e3, 1),
+        "speedup_vs_dense": round(ms_d / ms_e, 3),
+        "step_time_reduction": round(1 - ms_e / ms_d, 4),
+        "espace_step_tflops": round(fl_e / (ms_e * 1e-3) / 1e12, 1),
+        "dense_step_tflops": round(fl_d / (ms_d * 1e-3) / 1e12, 1),
+        "paper": "up to 15% lower training iteration time for 50%-compressed models (whole model, Section 2.2)",
+    }
 
 
 def calibration_lines(E, Xs, dev, stream, args):

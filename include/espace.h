@@ -61,7 +61,7 @@
 extern "C" {
 #endif
 
-#define ESPACE_ABI_VERSION 3
+#define ESPACE_ABI_VERSION 4
 
 typedef enum {
     ESPACE_F32 = 0,
@@ -88,7 +88,9 @@ typedef enum {
     ESPACE_OP_DENSE = 4,
     ESPACE_OP_AUTOCORR = 5,    /* espace_autocorrelation_update: uses K, N */
     ESPACE_OP_PCA = 6,         /* espace_principal_components: uses K, L */
-    ESPACE_OP_SYMPRODUCT = 7   /* espace_symmetrized_product: uses K */
+    ESPACE_OP_SYMPRODUCT = 7,  /* espace_symmetrized_product: uses K */
+    ESPACE_OP_BACKWARD = 8,    /* espace_projected_linear_backward: uses M, K, L, N */
+    ESPACE_OP_DENSE_BACKWARD = 9   /* espace_dense_linear_backward: uses M, K, N */
 } espace_op;
 
 /* Folded weight Wf = W·P (Section 2.2: the paper's PᵀW, "pre-computed before
@@ -148,6 +150,44 @@ espace_status espace_dense_linear(const void* X, int64_t ldx,
                                   espace_dtype dt,
                                   void* workspace, size_t workspace_bytes,
                                   hipStream_t stream);
+
+/* ---- Training view (Section 2.2, "during training/finetuning") -----------
+ *
+ * While training, the layer is Y = W·(P·Pᵀ·X): P stays fixed, W is learnt.
+ * The forward pass is espace_fold_weights (Wf = W·P, every step) followed by
+ * espace_project (Z, kept for the backward pass) and espace_expand.
+ * Gradients for an upstream gradient dY = ∂ℓ/∂Y [N][M]:
+ *     dX = (dY·Wf)·Pt         dX[n][k] = Σ_l (Σ_m dY[n][m]·Wf[m][l])·Pt[l][k]
+ *     dW = (dYᵀ·Z)·Pt         dW[m][k] = Σ_l (Σ_n dY[n][m]·Z[n][l])·Pt[l][k]
+ * i.e. ∂ℓ/∂X = P·Pᵀ·(Wᵀ-side gradient) and ∂ℓ/∂W = dYᵀ·X̃ with X̃ = P·Pᵀ·X.
+ * bf16: the intermediate products dY·Wf and dYᵀ·Z are rounded to bf16 (as Z
+ * in the forward pass).  In: dY [N][M], Z [N][L] (for dW), Pt [L][K], Wf
+ * [M][L] (for dX).  Out: dX [N][K] and/or dW [M][K] (either may be NULL).
+ * Needs espace_workspace_bytes(ESPACE_OP_BACKWARD, M, K, L, N, dt). */
+espace_status espace_projected_linear_backward(const void* dY, int64_t lddy,
+                                               const void* Z, int64_t ldz,
+                                               const void* Pt, int64_t ldp,
+                                               const void* Wf, int64_t ldwf,
+                                               void* dX, int64_t lddx,
+                                               void* dW, int64_t lddw,
+                                               int64_t M, int64_t K, int64_t L, int64_t N,
+                                               espace_dtype dt,
+                                               void* workspace, size_t workspace_bytes,
+                                               hipStream_t stream);
+
+/* Gradients of the dense layer Y = W·X it replaces (the baseline):
+ * dX = dY·W, dW = dYᵀ·X.  In: dY [N][M], X [N][K] (for dW), W [M][K] (for
+ * dX).  Out: dX [N][K] and/or dW [M][K] (either may be NULL).
+ * Needs espace_workspace_bytes(ESPACE_OP_DENSE_BACKWARD, M, K, 0, N, dt). */
+espace_status espace_dense_linear_backward(const void* dY, int64_t lddy,
+                                           const void* X, int64_t ldx,
+                                           const void* W, int64_t ldw,
+                                           void* dX, int64_t lddx,
+                                           void* dW, int64_t lddw,
+                                           int64_t M, int64_t K, int64_t N,
+                                           espace_dtype dt,
+                                           void* workspace, size_t workspace_bytes,
+                                           hipStream_t stream);
 
 /* ---- Calibration of P (before deployment) --------------------------------
  *

@@ -22,6 +22,7 @@ from .espace_ref import (  # noqa: F401
     principal_components_by_magnitude,
     train_forward,
     train_backward,
+    dense_backward,
 )
 from .brute import (  # noqa: F401
     bf_fold,

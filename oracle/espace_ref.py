@@ -189,3 +189,11 @@ def train_backward(dY, X, Pt, W):
     dW = dY.T @ Xt
     dX = reconstruct(Pt, dY @ W)
     return dX, dW
+
+
+def dense_backward(dY, X, W):
+    """Gradients of the dense layer Y = WᵀX (Section 2.1, Eq. 1) for an
+    upstream gradient dY[N][M]: ∂ℓ/∂X = dY·W, ∂ℓ/∂W = dYᵀ·X (storage
+    orientation).  Returns (dX[N][K], dW[M][K])."""
+    dY = _f64(dY)
+    return dY @ _f64(W), dY.T @ _f64(X)

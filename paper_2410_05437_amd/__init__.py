@@ -10,7 +10,9 @@ from ._lib import (  # noqa: F401
     BF16,
     F32,
     OP_AUTOCORR,
+    OP_BACKWARD,
     OP_DENSE,
+    OP_DENSE_BACKWARD,
     OP_EXPAND,
     OP_FOLD,
     OP_PROJECT,
@@ -20,11 +22,13 @@ from ._lib import (  # noqa: F401
     EspaceError,
     espace_autocorrelation_update,
     espace_dense_linear,
+    espace_dense_linear_backward,
     espace_expand,
     espace_fold_weights,
     espace_principal_components,
     espace_project,
     espace_projected_linear,
+    espace_projected_linear_backward,
     espace_symmetrized_product,
     espace_workspace_bytes,
     header_functions,

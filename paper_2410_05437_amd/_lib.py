@@ -18,7 +18,8 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "espace.h")
 
 F32 = 0
 BF16 = 1
-OP_FOLD, OP_PROJECT, OP_EXPAND, OP_PROJECTED_LINEAR, OP_DENSE, OP_AUTOCORR, OP_PCA, OP_SYMPRODUCT = range(8)
+(OP_FOLD, OP_PROJECT, OP_EXPAND, OP_PROJECTED_LINEAR, OP_DENSE, OP_AUTOCORR, OP_PCA, OP_SYMPRODUCT, OP_BACKWARD,
+ OP_DENSE_BACKWARD) = range(10)
 
 _c_i64 = ctypes.c_int64
 _c_p = ctypes.c_void_p
@@ -42,6 +43,8 @@ _SIGS = {
     "espace_principal_components": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_p, _c_i64, _c_i64, _c_int, _c_int,
                                      _c_p, _c_sz, _c_p], _c_int),
     "espace_symmetrized_product": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_p, _c_sz, _c_p], _c_int),
+    "espace_projected_linear_backward": ([_c_p, _c_i64] * 6 + [_c_i64] * 4 + [_c_int, _c_p, _c_sz, _c_p], _c_int),
+    "espace_dense_linear_backward": ([_c_p, _c_i64] * 5 + [_c_i64] * 3 + [_c_int, _c_p, _c_sz, _c_p], _c_int),
     "espace_workspace_bytes": ([_c_int, _c_i64, _c_i64, _c_i64, _c_i64, _c_int], _c_sz),
     "espace_status_string": ([_c_int], ctypes.c_char_p),
     "espace_last_error": ([], ctypes.c_char_p),
@@ -288,3 +291,52 @@ def espace_principal_components(C, L, dtype=torch.bfloat16, Pt=None, eigenvalues
                                                ctypes.c_void_p(ws.data_ptr() if ws is not None else 0), wsb,
                                                _stream(C.device)))
     return Pt, eigenvalues, info
+
+
+def _opt_out(t, rows, cols, like, name, want):
+    if not want:
+        return None, ctypes.c_void_p(0), 0
+    t = _out(t, rows, cols, like, name)
+    p, ld = _mat(t, name)
+    return t, p, ld
+
+
+def espace_projected_linear_backward(dY, Z, Pt, Wf, dX=None, dW=None, want_dx=True, want_dw=True,
+                                     workspace=None):
+    """Gradients of the training view Y = W·(P·Pᵀ·X) (Section 2.2) for an
+    upstream gradient dY [N][M]: dX = (dY·Wf)·Pt [N][K] and dW = (dYᵀ·Z)·Pt
+    [M][K], from the forward pass's Z = Pᵀ·X [N][L] and Wf = W·P [M][L].
+    Returns (dX, dW); either is None when not wanted."""
+    N, M = dY.shape
+    L, K = Pt.shape
+    dX, pdx, lddx = _opt_out(dX, N, K, dY, "dX", want_dx)
+    dW, pdw, lddw = _opt_out(dW, M, K, dY, "dW", want_dw)
+    ws, wsb = _ws(workspace, espace_workspace_bytes(OP_BACKWARD, M, K, L, N, dY.dtype), dY.device)
+    pdy, lddy = _mat(dY, "dY")
+    pz, ldz = _mat(Z, "Z")
+    pp, ldp = _mat(Pt, "Pt")
+    pw, ldw = _mat(Wf, "Wf")
+    with torch.cuda.device(dY.device):
+        _check(lib.espace_projected_linear_backward(pdy, lddy, pz, ldz, pp, ldp, pw, ldw, pdx, lddx, pdw, lddw,
+                                                    M, K, L, N, _dt(dY),
+                                                    ctypes.c_void_p(ws.data_ptr() if ws is not None else 0), wsb,
+                                                    _stream(dY.device)))
+    return dX, dW
+
+
+def espace_dense_linear_backward(dY, X, W, dX=None, dW=None, want_dx=True, want_dw=True, workspace=None):
+    """Gradients of the dense layer Y = W·X: dX = dY·W [N][K], dW = dYᵀ·X
+    [M][K].  Returns (dX, dW); either is None when not wanted."""
+    N, M = dY.shape
+    K = W.shape[1]
+    dX, pdx, lddx = _opt_out(dX, N, K, dY, "dX", want_dx)
+    dW, pdw, lddw = _opt_out(dW, M, K, dY, "dW", want_dw)
+    ws, wsb = _ws(workspace, espace_workspace_bytes(OP_DENSE_BACKWARD, M, K, 1, N, dY.dtype), dY.device)
+    pdy, lddy = _mat(dY, "dY")
+    px, ldx = _mat(X, "X")
+    pw, ldw = _mat(W, "W")
+    with torch.cuda.device(dY.device):
+        _check(lib.espace_dense_linear_backward(pdy, lddy, px, ldx, pw, ldw, pdx, lddx, pdw, lddw, M, K, N,
+                                                _dt(dY), ctypes.c_void_p(ws.data_ptr() if ws is not None else 0),
+                                                wsb, _stream(dY.device)))
+    return dX, dW

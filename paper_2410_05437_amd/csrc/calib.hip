@@ -306,6 +306,19 @@ hipError_t launch_autocorr_update(const void* X, int64_t ldx, int M, int K, bool
     return hipGetLastError();
 }
 
+hipError_t launch_transpose(const void* src, int64_t lds, int rows, int cols, void* dst, int64_t ldd, bool f32,
+                            hipStream_t stream) {
+    const dim3 grid(ceil_div_i(rows, 64), ceil_div_i(cols, 64));
+    if (f32)
+        hipLaunchKernelGGL(transpose_scale_kernel<float>, grid, dim3(256), 0, stream, static_cast<const float*>(src),
+                           lds, nullptr, static_cast<float*>(dst), ldd, rows, cols);
+    else
+        hipLaunchKernelGGL(transpose_scale_kernel<uint16_t>, grid, dim3(256), 0, stream,
+                           static_cast<const uint16_t*>(src), lds, nullptr, static_cast<uint16_t*>(dst), ldd, rows,
+                           cols);
+    return hipGetLastError();
+}
+
 size_t pca_workspace_bytes(int64_t K) {
     size_t b = (size_t)K * K * 8;          // the matrix, then its eigenvectors
     b += (size_t)K * 8 * 2;                // eigenvalues, off-diagonal scratch

@@ -12,6 +12,7 @@
 #include <atomic>
 #include <cstdlib>
 #include <cstring>
+#include <algorithm>
 #include <mutex>
 #include <random>
 #include <string>
@@ -290,6 +291,48 @@ size_t z_bytes(int64_t N, int64_t L, espace_dtype dt) {
     return align_ws((size_t)N * z_ld(L, dt) * elem_size(dt));
 }
 
+// Workspace of the training-view gradients: transposed operands (the GEMM
+// kernels reduce over the contiguous dimension of both operands), the
+// intermediate products, and the GEMMs' partial sums (used one after the
+// other).  Leading dimensions: multiples of 8 elements.
+struct BwdLayout {
+    size_t a, b, c, d, e, f, part, total;
+};
+
+int64_t ld8(int64_t c) { return (c + 7) / 8 * 8; }
+
+BwdLayout bwd_layout(int64_t M, int64_t K, int64_t L, int64_t N, espace_dtype dt) {
+    const size_t es = elem_size(dt);
+    BwdLayout b{};
+    size_t o = 0;
+    b.a = o; o = align_ws(o + (size_t)L * ld8(M) * es);   // Wfᵀ  [L][M]
+    b.b = o; o = align_ws(o + (size_t)K * ld8(L) * es);   // P    [K][L]
+    b.c = o; o = align_ws(o + (size_t)M * ld8(N) * es);   // dYᵀ  [M][N]
+    b.d = o; o = align_ws(o + (size_t)L * ld8(N) * es);   // Zᵀ   [L][N]
+    b.e = o; o = align_ws(o + (size_t)N * ld8(L) * es);   // dZ   [N][L]
+    b.f = o; o = align_ws(o + (size_t)M * ld8(L) * es);   // G    [M][L]
+    b.part = o;
+    size_t part = plan_tn(N, L, M, dt).partial_bytes;
+    part = std::max(part, plan_tn(N, K, L, dt).partial_bytes);
+    part = std::max(part, plan_tn(M, L, N, dt).partial_bytes);
+    part = std::max(part, plan_tn(M, K, L, dt).partial_bytes);
+    b.total = align_ws(o + part);
+    return b;
+}
+
+BwdLayout dense_bwd_layout(int64_t M, int64_t K, int64_t N, espace_dtype dt) {
+    const size_t es = elem_size(dt);
+    BwdLayout b{};
+    size_t o = 0;
+    b.a = o; o = align_ws(o + (size_t)K * ld8(M) * es);   // Wᵀ   [K][M]
+    b.c = o; o = align_ws(o + (size_t)M * ld8(N) * es);   // dYᵀ  [M][N]
+    b.d = o; o = align_ws(o + (size_t)K * ld8(N) * es);   // Xᵀ   [K][N]
+    b.part = o;
+    const size_t part = std::max(plan_tn(N, K, M, dt).partial_bytes, plan_tn(M, K, N, dt).partial_bytes);
+    b.total = align_ws(o + part);
+    return b;
+}
+
 size_t ws_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int64_t N, espace_dtype dt) {
     switch (op) {
         case ESPACE_OP_FOLD: return M ? align_ws(plan_tn(M, L, K, dt).partial_bytes) : 0;
@@ -299,6 +342,8 @@ size_t ws_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int64_t N, espace
         case ESPACE_OP_AUTOCORR: return N ? align_ws(espace::autocorr_workspace_bytes(N, K, dt == ESPACE_F32)) : 0;
         case ESPACE_OP_PCA: return align_ws(espace::pca_workspace_bytes(K));
         case ESPACE_OP_SYMPRODUCT: return align_ws(espace::symprod_workspace_bytes(K));
+        case ESPACE_OP_BACKWARD: return (N && M) ? bwd_layout(M, K, L, N, dt).total : 0;
+        case ESPACE_OP_DENSE_BACKWARD: return (N && M) ? dense_bwd_layout(M, K, N, dt).total : 0;
         case ESPACE_OP_PROJECTED_LINEAR: {
             if (!N || !M) return 0;
             size_t a = plan_tn(N, L, K, dt).partial_bytes;
@@ -487,6 +532,12 @@ size_t espace_workspace_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int
         if (K < 1 || K > kMaxSymDim) return SIZE_MAX;
         return ws_bytes(op, 0, K, 0, 0, dt);
     }
+    if (op == ESPACE_OP_BACKWARD || op == ESPACE_OP_DENSE_BACKWARD) {
+        const bool hl = op == ESPACE_OP_BACKWARD;
+        if (M < 0 || N < 0 || K < 1 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return SIZE_MAX;
+        if (hl && (L < 1 || L > K)) return SIZE_MAX;
+        return ws_bytes(op, M, K, hl ? L : 0, N, dt);
+    }
     const bool has_L = op != ESPACE_OP_DENSE;
     int64_t Kc = K;
     if (op == ESPACE_OP_EXPAND) Kc = L;       // expand has no K; L bounds itself
@@ -615,6 +666,117 @@ espace_status espace_dense_linear(const void* X, int64_t ldx, const void* W, int
     ESPACE_TRY(check_alias(mat_range("Y", Y, N, ldy, dt), ins, 3));
     ESPACE_TRY(check_device());
     ESPACE_TRY(run_tn(X, ldx, W, ldw, Y, ldy, N, M, K, dt, workspace, stream));
+    return ok();
+}
+
+espace_status espace_projected_linear_backward(const void* dY, int64_t lddy, const void* Z, int64_t ldz,
+                                               const void* Pt, int64_t ldp, const void* Wf, int64_t ldwf, void* dX,
+                                               int64_t lddx, void* dW, int64_t lddw, int64_t M, int64_t K,
+                                               int64_t L, int64_t N, espace_dtype dt, void* workspace,
+                                               size_t workspace_bytes, hipStream_t stream) {
+    ESPACE_TRY(check_dtype(dt));
+    ESPACE_TRY(check_dims(M, K, L, N, true));
+    if (M == 0 || N == 0 || (!dX && !dW)) return ok();
+    ESPACE_TRY(check_mat("dY", dY, N, M, lddy, dt));
+    ESPACE_TRY(check_mat("Pt", Pt, L, K, ldp, dt));
+    if (dX) {
+        ESPACE_TRY(check_mat("Wf", Wf, M, L, ldwf, dt));
+        ESPACE_TRY(check_mat("dX", dX, N, K, lddx, dt));
+    }
+    if (dW) {
+        ESPACE_TRY(check_mat("Z", Z, N, L, ldz, dt));
+        ESPACE_TRY(check_mat("dW", dW, M, K, lddw, dt));
+    }
+    const BwdLayout b = bwd_layout(M, K, L, N, dt);
+    ESPACE_TRY(check_workspace(workspace, workspace_bytes, b.total));
+    const Range ws{"workspace", (uintptr_t)workspace, (uintptr_t)workspace + workspace_bytes};
+    const Range ins[] = {mat_range("dY", dY, N, lddy, dt), mat_range("Pt", Pt, L, ldp, dt),
+                         dX ? mat_range("Wf", Wf, M, ldwf, dt) : Range{"Wf", 0, 0},
+                         dW ? mat_range("Z", Z, N, ldz, dt) : Range{"Z", 0, 0}, ws};
+    if (dX) ESPACE_TRY(check_alias(mat_range("dX", dX, N, lddx, dt), ins, 5));
+    if (dW) ESPACE_TRY(check_alias(mat_range("dW", dW, M, lddw, dt), ins, 5));
+    if (dX && dW) {
+        const Range o[] = {mat_range("dX", dX, N, lddx, dt)};
+        ESPACE_TRY(check_alias(mat_range("dW", dW, M, lddw, dt), o, 1));
+    }
+    ESPACE_TRY(check_device());
+    unsigned char* w = static_cast<unsigned char*>(workspace);
+    const bool f32 = dt == ESPACE_F32;
+    void* P = w + b.b;
+    void* part = w + b.part;
+    hipError_t e = espace::launch_transpose(Pt, ldp, (int)L, (int)K, P, ld8(L), f32, stream);
+    if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "transpose: %s", hipGetErrorString(e));
+    if (dX) {
+        // dZ = dY·Wf (reduced over M), dX = dZ·Pt (reduced over L)
+        void* WfT = w + b.a;
+        void* dZ = w + b.e;
+        e = espace::launch_transpose(Wf, ldwf, (int)M, (int)L, WfT, ld8(M), f32, stream);
+        if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "transpose: %s", hipGetErrorString(e));
+        ESPACE_TRY(run_tn(dY, lddy, WfT, ld8(M), dZ, ld8(L), N, L, M, dt, part, stream));
+        ESPACE_TRY(run_tn(dZ, ld8(L), P, ld8(L), dX, lddx, N, K, L, dt, part, stream));
+    }
+    if (dW) {
+        // G = dYᵀ·Z (reduced over N), dW = G·Pt (reduced over L)
+        void* dYT = w + b.c;
+        void* ZT = w + b.d;
+        void* G = w + b.f;
+        e = espace::launch_transpose(dY, lddy, (int)N, (int)M, dYT, ld8(N), f32, stream);
+        if (e == hipSuccess) e = espace::launch_transpose(Z, ldz, (int)N, (int)L, ZT, ld8(N), f32, stream);
+        if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "transpose: %s", hipGetErrorString(e));
+        ESPACE_TRY(run_tn(dYT, ld8(N), ZT, ld8(N), G, ld8(L), M, L, N, dt, part, stream));
+        ESPACE_TRY(run_tn(G, ld8(L), P, ld8(L), dW, lddw, M, K, L, dt, part, stream));
+    }
+    return ok();
+}
+
+espace_status espace_dense_linear_backward(const void* dY, int64_t lddy, const void* X, int64_t ldx, const void* W,
+                                           int64_t ldw, void* dX, int64_t lddx, void* dW, int64_t lddw, int64_t M,
+                                           int64_t K, int64_t N, espace_dtype dt, void* workspace,
+                                           size_t workspace_bytes, hipStream_t stream) {
+    ESPACE_TRY(check_dtype(dt));
+    ESPACE_TRY(check_dims(M, K, 1, N, false));
+    if (M == 0 || N == 0 || (!dX && !dW)) return ok();
+    ESPACE_TRY(check_mat("dY", dY, N, M, lddy, dt));
+    if (dX) {
+        ESPACE_TRY(check_mat("W", W, M, K, ldw, dt));
+        ESPACE_TRY(check_mat("dX", dX, N, K, lddx, dt));
+    }
+    if (dW) {
+        ESPACE_TRY(check_mat("X", X, N, K, ldx, dt));
+        ESPACE_TRY(check_mat("dW", dW, M, K, lddw, dt));
+    }
+    const BwdLayout b = dense_bwd_layout(M, K, N, dt);
+    ESPACE_TRY(check_workspace(workspace, workspace_bytes, b.total));
+    const Range ws{"workspace", (uintptr_t)workspace, (uintptr_t)workspace + workspace_bytes};
+    const Range ins[] = {mat_range("dY", dY, N, lddy, dt), dX ? mat_range("W", W, M, ldw, dt) : Range{"W", 0, 0},
+                         dW ? mat_range("X", X, N, ldx, dt) : Range{"X", 0, 0}, ws};
+    if (dX) ESPACE_TRY(check_alias(mat_range("dX", dX, N, lddx, dt), ins, 4));
+    if (dW) ESPACE_TRY(check_alias(mat_range("dW", dW, M, lddw, dt), ins, 4));
+    if (dX && dW) {
+        const Range o[] = {mat_range("dX", dX, N, lddx, dt)};
+        ESPACE_TRY(check_alias(mat_range("dW", dW, M, lddw, dt), o, 1));
+    }
+    ESPACE_TRY(check_device());
+    unsigned char* w = static_cast<unsigned char*>(workspace);
+    const bool f32 = dt == ESPACE_F32;
+    void* part = w + b.part;
+    hipError_t e;
+    if (dX) {
+        // dX = dY·W (reduced over M)
+        void* WT = w + b.a;
+        e = espace::launch_transpose(W, ldw, (int)M, (int)K, WT, ld8(M), f32, stream);
+        if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "transpose: %s", hipGetErrorString(e));
+        ESPACE_TRY(run_tn(dY, lddy, WT, ld8(M), dX, lddx, N, K, M, dt, part, stream));
+    }
+    if (dW) {
+        // dW = dYᵀ·X (reduced over N)
+        void* dYT = w + b.c;
+        void* XT = w + b.d;
+        e = espace::launch_transpose(dY, lddy, (int)N, (int)M, dYT, ld8(N), f32, stream);
+        if (e == hipSuccess) e = espace::launch_transpose(X, ldx, (int)N, (int)K, XT, ld8(N), f32, stream);
+        if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "transpose: %s", hipGetErrorString(e));
+        ESPACE_TRY(run_tn(dYT, ld8(N), XT, ld8(N), dW, lddw, M, K, N, dt, part, stream));
+    }
     return ok();
 }
 

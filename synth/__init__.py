@@ -12,6 +12,7 @@ from .generate import (  # noqa: F401
     index_pattern,
     spectrum,
     symmetric_with_spectrum,
+    upstream_gradient,
     gaussian_tokens,
     structured_tokens,
     silu_gated_tokens,

@@ -16,7 +16,7 @@ elements, block b drawn by a numpy Generator seeded with
 SeedSequence([241005437, k, s, b]) (blocks are independent, so large arrays
 are drawn by several threads); s = 0 (Q), 1 (evaluation tokens), 2 (W), 4/5
 (a/b evaluation), 6/7 (a/b calibration), 8 (rotation of a symmetric test
-matrix with a given spectrum).  Tokens are drawn token by token, so
+matrix with a given spectrum), 9 (upstream gradients of the training view).  Tokens are drawn token by token, so
 the first n tokens of a larger draw equal a draw of n tokens.
 
 For K >= 4096 on a machine with a GPU, the dense float64 linear algebra of the
@@ -165,6 +165,12 @@ def symmetric_with_spectrum(K, lam, key):
     Q = haar_orthogonal(K, rng_for(key, 8))
     C = (Q * np.asarray(lam, dtype=np.float64)[None, :]) @ Q.T
     return (C + C.T) / 2
+
+
+def upstream_gradient(N, M, key):
+    """An upstream gradient dY [N][M] for the training-view tests: iid
+    N(0, 1/M) entries from stream 9 of `key` (float64)."""
+    return rng_for(key, 9).standard_normal((N, M)) / np.sqrt(M)
 
 
 def spectrum(K, floor=0.0):

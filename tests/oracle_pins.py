@@ -363,6 +363,10 @@ def pin_training_gradients(o):
     def loss(Xv, Wv):
         return float(np.sum(R * o.train_forward(Xv, Pt, Wv)[0]))
 
+    # with a full-rank P (PPᵀ = I) the training view is the dense layer
+    Pf = _orthonormal(K, K, rng).T.copy()
+    for a, b, what in zip(o.train_backward(R, X, Pf, W), o.dense_backward(R, X, W), ("dX", "dW")):
+        _close(a, b, rtol=1e-11, what="full-rank training gradient " + what)
     h = 1e-6
     for (n, k) in itertools.product(range(N), range(K)):
         Xp, Xm = X.copy(), X.copy()

@@ -20,10 +20,11 @@ def test_exports_every_declared_function():
         "espace_fold_weights", "espace_project", "espace_expand", "espace_projected_linear",
         "espace_dense_linear", "espace_workspace_bytes", "espace_status_string",
         "espace_last_error", "espace_abi_version", "espace_autocorrelation_update",
-        "espace_principal_components", "espace_symmetrized_product"}
+        "espace_principal_components", "espace_symmetrized_product", "espace_projected_linear_backward",
+        "espace_dense_linear_backward"}
     for n in names:
         assert hasattr(L, n)
-    assert E.ABI_VERSION == 3
+    assert E.ABI_VERSION == 4
 
 
 def _fold(W=P16, ldw=64, Pt=P16b, ldp=64, Wf=P16c, ldwf=16, M=32, K=64, Lc=16, dt=1,
@@ -79,7 +80,7 @@ def test_workspace_sizes():
     assert ws(4, 12288, 4096, 0, 4096, bf16) == 0
     assert ws(3, 12288, 4096, 1536, 0, bf16) == 0
     assert ws(3, 12288, 4096, 5000, 4096, bf16) == ctypes.c_size_t(-1).value
-    assert ws(9, 1, 1, 1, 1, bf16) == ctypes.c_size_t(-1).value
+    assert ws(99, 1, 1, 1, 1, bf16) == ctypes.c_size_t(-1).value
     assert ws(3, 256, 256, 64, 128, f32) == 128 * 64 * 4
     # ragged L: Z rows padded to a multiple of 64 elements
     assert ws(3, 6144, 24576, 2458, 8192, bf16) >= 8192 * 2496 * 2
@@ -160,3 +161,33 @@ def test_calibration_workspace_sizes():
     # the symmetrised product keeps one fp32 K x K product
     assert ws(7, 0, K, 0, 0, f32) == K * K * 4
     assert ws(7, 0, 0, 0, 0, f32) == ctypes.c_size_t(-1).value
+
+
+def _bwd(dY=P16, lddy=32, Z=P16b, ldz=16, Pt=P16c, ldp=64, Wf=ctypes.c_void_p(0x50000000), ldwf=16,
+         dX=ctypes.c_void_p(0x60000000), lddx=64, dW=ctypes.c_void_p(0x68000000), lddw=64, M=32, K=64, Lc=16,
+         N=8, dt=1, ws=ctypes.c_void_p(0x70000000), wsb=1 << 24):
+    return L.espace_projected_linear_backward(dY, lddy, Z, ldz, Pt, ldp, Wf, ldwf, dX, lddx, dW, lddw, M, K, Lc, N,
+                                              dt, ws, wsb, NULL)
+
+
+def test_backward_validation():
+    assert _bwd(dY=NULL) == 1
+    assert _bwd(Lc=65) == 2
+    assert _bwd(lddx=60) == 2
+    assert _bwd(dX=ctypes.c_void_p(0x10000 + 32)) == 5                  # dX over dY
+    assert _bwd(dW=ctypes.c_void_p(0x60000000 + 64)) == 5               # dW over dX
+    assert _bwd(ws=NULL, wsb=0) == 6
+    # only what is asked for is checked: dW alone needs no Wf
+    assert _bwd(dX=NULL, Wf=NULL) in (7, 8)
+    assert _bwd(dW=NULL, Z=NULL) in (7, 8)
+    assert _bwd(dX=NULL, dW=NULL, dY=NULL, Z=NULL, Pt=NULL, Wf=NULL, ws=NULL, wsb=0) == 0   # nothing asked
+    assert _bwd(N=0, dY=NULL, Z=NULL, dX=NULL, ws=NULL, wsb=0) == 0
+    d = L.espace_dense_linear_backward
+    assert d(P16, 32, P16b, 64, P16c, 64, ctypes.c_void_p(0x60000000), 64, ctypes.c_void_p(0x68000000), 64,
+             32, 64, 8, 1, ctypes.c_void_p(0x70000000), 1 << 24, NULL) in (7, 8)
+    assert d(NULL, 32, P16b, 64, P16c, 64, ctypes.c_void_p(0x60000000), 64, NULL, 64,
+             32, 64, 8, 1, ctypes.c_void_p(0x70000000), 1 << 24, NULL) == 1
+    ws = L.espace_workspace_bytes
+    assert ws(8, 12288, 4096, 1536, 4096, 1) > 0
+    assert ws(8, 12288, 4096, 5000, 4096, 1) == ctypes.c_size_t(-1).value
+    assert ws(9, 12288, 4096, 0, 4096, 1) >= 4096 * 12288 * 2

@@ -99,6 +99,11 @@ def _train_bwd_dw_raw_x(dY, X, Pt, W):
     return dX, np.asarray(dY, float).T @ np.asarray(X, float)
 
 
+def _dense_bwd_transposed(dY, X, W):
+    dX, dW = R.dense_backward(dY, X, W)
+    return dX, dW[::-1].copy()
+
+
 MUTANTS = {
     "fold uses Pt for P": {"fold": _fold_transposed_p},
     "fold ignores P": {"fold": _fold_skips_projection},
@@ -116,6 +121,7 @@ MUTANTS = {
     "selection by smallest magnitude": {"principal_components_by_magnitude": _by_magnitude_ascending},
     "training dX skips the projection": {"train_backward": _train_bwd_no_projection},
     "training dW from unprojected X": {"train_backward": _train_bwd_dw_raw_x},
+    "dense dW rows permuted": {"dense_backward": _dense_bwd_transposed},
 }
 
 
