@@ -87,6 +87,44 @@ __global__ __launch_bounds__(256) void transpose_scale_kernel(const T* __restric
     }
 }
 
+// dst[c][r] = src[r][c] for bfloat16: 64 x 64 tiles, 16-byte loads and
+// stores.  A thread loads 8 consecutive elements of a source row into the
+// LDS tile and stores 8 consecutive source rows of one column as a 16-byte
+// piece of a destination row.  Rows of both matrices are padded to a
+// multiple of 8 elements (16 bytes), so a piece that starts inside a row
+// stays inside it; the destination's padding may be written (the caller's
+// own scratch), its rows beyond `cols` are not.
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ src, int64_t lds,
+                                                             uint16_t* __restrict__ dst, int64_t ldd, int rows,
+                                                             int cols) {
+    __shared__ uint16_t t[64][66];
+    const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+    const int part = threadIdx.x & 7, line = threadIdx.x >> 3;    // 8 pieces of 8 elements, 32 lines
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int r = line + 32 * h;
+        u32x4_t v = {0u, 0u, 0u, 0u};
+        if (r0 + r < rows && c0 + part * 8 < cols)
+            v = *reinterpret_cast<const u32x4_t*>(src + (int64_t)(r0 + r) * lds + c0 + part * 8);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            t[r][part * 8 + 2 * e] = (uint16_t)(v[e] & 0xffffu);
+            t[r][part * 8 + 2 * e + 1] = (uint16_t)(v[e] >> 16);
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int c = line + 32 * h;
+        if (c0 + c >= cols || r0 + part * 8 >= rows) continue;
+        u32x4_t v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            v[e] = (uint32_t)t[part * 8 + 2 * e][c] | ((uint32_t)t[part * 8 + 2 * e + 1][c] << 16);
+        *reinterpret_cast<u32x4_t*>(dst + (int64_t)(c0 + c) * ldd + r0 + part * 8) = v;
+    }
+}
+
 // C[r][c] += alpha · Σ_s P_s[r][c], the depth ranges added in order.  With
 // tile > 0 only the tiles on and above the diagonal of P (tile x tile) hold
 // sums: an entry below them is read from its mirror P[c][r].
@@ -313,9 +351,8 @@ hipError_t launch_transpose(const void* src, int64_t lds, int rows, int cols, vo
         hipLaunchKernelGGL(transpose_scale_kernel<float>, grid, dim3(256), 0, stream, static_cast<const float*>(src),
                            lds, nullptr, static_cast<float*>(dst), ldd, rows, cols);
     else
-        hipLaunchKernelGGL(transpose_scale_kernel<uint16_t>, grid, dim3(256), 0, stream,
-                           static_cast<const uint16_t*>(src), lds, nullptr, static_cast<uint16_t*>(dst), ldd, rows,
-                           cols);
+        hipLaunchKernelGGL(transpose_bf16_kernel, grid, dim3(256), 0, stream, static_cast<const uint16_t*>(src), lds,
+                           static_cast<uint16_t*>(dst), ldd, rows, cols);
     return hipGetLastError();
 }
 

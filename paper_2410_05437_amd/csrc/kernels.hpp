@@ -108,7 +108,9 @@ hipError_t launch_principal_components(const float* C, int64_t ldc, int K, int L
                                        int64_t ldp, bool f32, float* evals, int* info, void* workspace,
                                        hipStream_t stream);
 size_t symprod_workspace_bytes(int64_t K);
-// dst[c][r] = src[r][c] for r < rows, c < cols (bf16 or fp32; values copied exactly)
+// dst[c][r] = src[r][c] for r < rows, c < cols (bf16 or fp32; values copied
+// exactly).  Both leading dimensions are multiples of 8 elements; the bf16
+// kernel may write the padding columns of dst's rows (scratch only).
 hipError_t launch_transpose(const void* src, int64_t lds, int rows, int cols, void* dst, int64_t ldd, bool f32,
                             hipStream_t stream);
 hipError_t launch_symmetrized_product(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
