@@ -383,3 +383,36 @@ def test_pair_combine_under_graph_replay(E, shape):
         assert torch.equal(got, ref), rep
         if rep < 3:
             assert oracle.rel_fro(host64(got), oracle.project(inps[0].Pt, inps[rep].X)) <= TOL["bf16"]
+
+
+def test_prefill_layer_under_graph_replay(E):
+    """A prefill layer call (tiled GEMMs, Z in the workspace) captured once in
+    a HIP graph and replayed with new inputs copied in between: every replay
+    equals the eager call bitwise, and the oracle on the first input."""
+    dev = need_gpu()
+    K, M, L, N = 1024, 4096, 256, 2048
+    inps = [_inputs(K, M, L, N, "bf16", seed=70 + i) for i in range(2)]
+    X, Pt, W = _dev_inputs(inps[0], dev)
+    Wf = E.espace_fold_weights(W, Pt)
+    Y = out_mat(N, M, "bf16", dev)
+    ws = torch.empty(max(E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, M, K, L, N, torch.bfloat16), 1),
+                     dtype=torch.uint8, device=dev)
+    E.espace_projected_linear(X, Pt, Wf, Y, ws)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        E.espace_projected_linear(X, Pt, Wf, Y, ws)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        X.copy_(dev_mat(inps[rep % 2].X_s, "bf16", dev))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = Y.clone()
+        ref = E.espace_projected_linear(X, Pt, Wf)
+        torch.cuda.synchronize()
+        assert torch.equal(got, ref), rep
+    X.copy_(dev_mat(inps[0].X_s, "bf16", dev))
+    g.replay()
+    torch.cuda.synchronize()
+    assert oracle.rel_fro(host64(Y), oracle.projected_linear_from_weights(inps[0].X, inps[0].Pt, inps[0].W)) <= 1e-2
