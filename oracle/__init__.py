@@ -19,6 +19,7 @@ from .espace_ref import (  # noqa: F401
     principal_components,
     normalized_autocorrelation,
     gomse_matrix,
+    nlmse_matrix,
     principal_components_by_magnitude,
     train_forward,
     train_backward,

@@ -197,3 +197,25 @@ def dense_backward(dY, X, W):
     orientation).  Returns (dX[N][K], dW[M][K])."""
     dY = _f64(dY)
     return dY @ _f64(W), dY.T @ _f64(X)
+
+
+def nlmse_matrix(pairs, normalized=False):
+    """Theorem 2, NL-MSE bound: C = E[x xᵀ ∇ ∇ᵀ + ∇ ∇ᵀ x xᵀ] with ∇ the loss
+    gradient with respect to the activation vector, calibrated as the proof of
+    Theorem 2 describes (Appendix): per sequence i, with its activations X^(i)
+    and gradients G^(i) (M_i vectors each, as rows here),
+    C^(i) = (X Xᵀ G Gᵀ + G Gᵀ X Xᵀ)/M_i², averaged over the B sequences.
+    normalized: the L2-normalised variant Ĉ, each activation and each gradient
+    vector scaled to unit norm (Section 3.3)."""
+    C = None
+    for X, G in pairs:
+        X = _f64(X)
+        G = _f64(G)
+        if normalized:
+            X = X / np.linalg.norm(X, axis=1, keepdims=True)
+            G = G / np.linalg.norm(G, axis=1, keepdims=True)
+        M = X.shape[0]
+        Xp, Gp = X.T, G.T                          # K×M: vectors as columns
+        Ci = (Xp @ Xp.T @ Gp @ Gp.T + Gp @ Gp.T @ Xp @ Xp.T) / (M * M)
+        C = Ci if C is None else C + Ci
+    return C / len(pairs)

@@ -302,6 +302,34 @@ def pin_gomse_expectation(o):
            accn / (N * M), rtol=1e-12, what="normalised GO-MSE matrix")
 
 
+def pin_nlmse_expectation(o):
+    """Theorem 2's NL-MSE matrix as its proof calibrates it: per sequence, the
+    average over all (activation, gradient) pairs of the sequence of
+    x xᵀ g gᵀ + g gᵀ x xᵀ, summed pair by pair, then the mean over sequences;
+    the normalised variant with unit vectors."""
+    rng = _rng(1500)
+    K = 4
+    seqs = [(rng.standard_normal((5, K)), rng.standard_normal((5, K))),
+            (rng.standard_normal((3, K)), rng.standard_normal((3, K)))]
+    for normalized in (False, True):
+        tot = np.zeros((K, K))
+        for X, G in seqs:
+            acc = np.zeros((K, K))
+            for x in X:
+                if normalized:
+                    x = x / np.sqrt(sum(v * v for v in x))
+                for g in G:
+                    if normalized:
+                        g = g / np.sqrt(sum(v * v for v in g))
+                    xg = sum(x[k] * g[k] for k in range(K))
+                    for i in range(K):
+                        for j in range(K):
+                            acc[i, j] += x[i] * xg * g[j] + g[i] * xg * x[j]
+            tot += acc / (len(X) * len(G))
+        _close(o.nlmse_matrix(seqs, normalized=normalized), tot / len(seqs), rtol=1e-12,
+               what="NL-MSE matrix" + (" (normalised)" if normalized else ""))
+
+
 def pin_gomse_bound_identity(o):
     """Theorem 2's derivation: for any orthonormal P, the mean over pairs of
     2<w,x><w,x̃> (the part of Proposition 1's bound that P controls) equals
@@ -395,6 +423,7 @@ ALL_PINS = [
     pin_sampled,
     pin_rel_fro,
     pin_gomse_expectation,
+    pin_nlmse_expectation,
     pin_gomse_bound_identity,
     pin_magnitude_order,
     pin_training_gradients,

@@ -104,6 +104,16 @@ def _dense_bwd_transposed(dY, X, W):
     return dX, dW[::-1].copy()
 
 
+def _nlmse_pooled(pairs, normalized=False):
+    X = np.concatenate([np.asarray(a, float) for a, _ in pairs])
+    G = np.concatenate([np.asarray(b, float) for _, b in pairs])
+    return R.nlmse_matrix([(X, G)], normalized)
+
+
+def _nlmse_unnormalised(pairs, normalized=False):
+    return R.nlmse_matrix(pairs, False)
+
+
 MUTANTS = {
     "fold uses Pt for P": {"fold": _fold_transposed_p},
     "fold ignores P": {"fold": _fold_skips_projection},
@@ -122,6 +132,8 @@ MUTANTS = {
     "training dX skips the projection": {"train_backward": _train_bwd_no_projection},
     "training dW from unprojected X": {"train_backward": _train_bwd_dw_raw_x},
     "dense dW rows permuted": {"dense_backward": _dense_bwd_transposed},
+    "NL-MSE pooled across sequences": {"nlmse_matrix": _nlmse_pooled},
+    "NL-MSE normalised variant not normalised": {"nlmse_matrix": _nlmse_unnormalised},
 }
 
 
