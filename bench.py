@@ -411,7 +411,7 @@ def calibration_lines(E, Xs, dev, stream, args):
     Cs = E.padded_empty(K, K, torch.float32, dev, 4)
     wss = torch.empty(E.espace_workspace_bytes(E.OP_SYMPRODUCT, 0, K, 0, 0, torch.float32), dtype=torch.uint8,
                       device=dev)
-    ms_sym = time_calls(lambda i: E.espace_symmetrized_product(C, C, Cs, wss), 1, 3, 1, stream)
+    ms_sym = time_calls(lambda i: E.espace_symmetrized_product(C, C, Cs, wss), 1, 3, 1, stream)   # alpha 1, beta 0
     del Cs, wss
     flops = float(K) * (K + 1) * Nc
     tf = flops / (ms * 1e-3) / 1e12

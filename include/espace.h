@@ -61,7 +61,7 @@
 extern "C" {
 #endif
 
-#define ESPACE_ABI_VERSION 4
+#define ESPACE_ABI_VERSION 5
 
 typedef enum {
     ESPACE_F32 = 0,
@@ -214,17 +214,25 @@ espace_status espace_autocorrelation_update(const void* X, int64_t ldx,
                                             void* workspace, size_t workspace_bytes,
                                             hipStream_t stream);
 
-/* GO-MSE candidate matrix (Section 3.3, Theorem 2): C = A·Bᵀ + B·Aᵀ, which
- * for the symmetric autocorrelations A = C_X and B = C_W (the weight
- * autocorrelation: espace_autocorrelation_update over the rows of W) is
- * Theorem 2's C_X·C_W + C_W·C_X; with both normalised, its Ĉ.
- * C[r][c] = Σ_k A[r][k]·B[c][k] + Σ_k B[r][k]·A[c][k], float32 throughout
- * (one fp32 product, added to its transpose: C is exactly symmetric).
- * In: A, B [K][K] (lda, ldb, float32).  Out: C [K][K] (ldc, float32).
+/* GO-MSE and NL-MSE candidate matrices (Section 3.3, Theorem 2):
+ *
+ *        C = beta·C + alpha·(A·Bᵀ + B·Aᵀ)
+ *
+ * C[r][c] = beta·C[r][c] + alpha·(Σ_k A[r][k]·B[c][k] + Σ_k B[r][k]·A[c][k]),
+ * float32 throughout (one fp32 product added to its transpose: exactly
+ * symmetric when beta·C is); C is not read when beta == 0.  For the
+ * symmetric autocorrelations A = C_X and B = C_W (espace_autocorrelation_update
+ * over the rows of W) with alpha = 1, beta = 0 this is Theorem 2's GO-MSE
+ * matrix C_X·C_W + C_W·C_X; with both normalised, its Ĉ.  The NL-MSE matrix
+ * is accumulated per calibration sequence i (the proof of Theorem 2): A and B
+ * the autocorrelations of the sequence's activations and of their loss
+ * gradients (alpha = 1/M_i in each update), then alpha = 1/B, beta = 1.
+ * In: A, B [K][K] (lda, ldb, float32).  In/out: C [K][K] (ldc, float32).
  * Needs espace_workspace_bytes(ESPACE_OP_SYMPRODUCT, 0, K, 0, 0, ESPACE_F32). */
 espace_status espace_symmetrized_product(const float* A, int64_t lda,
                                          const float* B, int64_t ldb,
                                          float* C, int64_t ldc, int64_t K,
+                                         float alpha, float beta,
                                          void* workspace, size_t workspace_bytes,
                                          hipStream_t stream);
 

@@ -42,7 +42,8 @@ _SIGS = {
                                        _c_int, _c_p, _c_sz, _c_p], _c_int),
     "espace_principal_components": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_p, _c_i64, _c_i64, _c_int, _c_int,
                                      _c_p, _c_sz, _c_p], _c_int),
-    "espace_symmetrized_product": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_p, _c_sz, _c_p], _c_int),
+    "espace_symmetrized_product": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_i64, ctypes.c_float,
+                                    ctypes.c_float, _c_p, _c_sz, _c_p], _c_int),
     "espace_projected_linear_backward": ([_c_p, _c_i64] * 6 + [_c_i64] * 4 + [_c_int, _c_p, _c_sz, _c_p], _c_int),
     "espace_dense_linear_backward": ([_c_p, _c_i64] * 5 + [_c_i64] * 3 + [_c_int, _c_p, _c_sz, _c_p], _c_int),
     "espace_workspace_bytes": ([_c_int, _c_i64, _c_i64, _c_i64, _c_i64, _c_int], _c_sz),
@@ -243,21 +244,25 @@ def espace_autocorrelation_update(X, C, alpha, normalize=False, workspace=None):
     return C
 
 
-def espace_symmetrized_product(A, B, C=None, workspace=None):
-    """C = A·Bᵀ + B·Aᵀ for float32 [K][K] A and B: with the autocorrelations
-    C_X and C_W, Theorem 2's GO-MSE matrix C_X·C_W + C_W·C_X."""
+def espace_symmetrized_product(A, B, C=None, workspace=None, alpha=1.0, beta=0.0):
+    """C = beta·C + alpha·(A·Bᵀ + B·Aᵀ) for float32 [K][K] A and B: with the
+    autocorrelations C_X and C_W, Theorem 2's GO-MSE matrix C_X·C_W +
+    C_W·C_X; accumulated over calibration sequences (beta = 1) with the
+    gradients' autocorrelation in place of C_W, its NL-MSE matrix."""
     K = A.shape[0]
     for t, n in ((A, "A"), (B, "B")):
         if t.dtype != torch.float32 or tuple(t.shape) != (K, K):
             raise ValueError(f"{n} must be a float32 {K}x{K} tensor")
     if C is None:
+        if beta != 0.0:
+            raise ValueError("beta != 0 needs C")
         C = padded_empty(K, K, torch.float32, A.device, 4)
     ws, wsb = _ws(workspace, espace_workspace_bytes(OP_SYMPRODUCT, 0, K, 0, 0, torch.float32), A.device)
     pa, lda = _mat(A, "A")
     pb, ldb = _mat(B, "B")
     pc, ldc = _mat(C, "C")
     with torch.cuda.device(A.device):
-        _check(lib.espace_symmetrized_product(pa, lda, pb, ldb, pc, ldc, K,
+        _check(lib.espace_symmetrized_product(pa, lda, pb, ldb, pc, ldc, K, float(alpha), float(beta),
                                               ctypes.c_void_p(ws.data_ptr() if ws is not None else 0), wsb,
                                               _stream(A.device)))
     return C

@@ -11,10 +11,12 @@
 //    symmetric, so (bf16) only the 256 x 256 tiles on and above the diagonal
 //    are computed, and a last pass adds alpha times the sum of the ranges to
 //    C in fixed order, reading the mirrored entry below the diagonal tiles.
-//  * GO-MSE candidate (Theorem 2): C = A·Bᵀ + B·Aᵀ, for the symmetric
-//    autocorrelations A = C_X and B = C_W the matrix C_X·C_W + C_W·C_X: one
-//    fp32 "TN" product A·Bᵀ, then C[r][c] = P[r][c] + P[c][r] (64 x 64 tiles
-//    of P and of its transpose through LDS), exactly symmetric.
+//  * GO-MSE / NL-MSE candidates (Theorem 2): C = beta·C + alpha·(A·Bᵀ + B·Aᵀ),
+//    for the symmetric autocorrelations A = C_X and B = C_W (or, per
+//    calibration sequence, C_G of the activation gradients) the matrix
+//    C_X·C_W + C_W·C_X: one fp32 "TN" product A·Bᵀ, then C[r][c] =
+//    beta·C[r][c] + alpha·(P[r][c] + P[c][r]) (64 x 64 tiles of P and of its
+//    transpose through LDS), exactly symmetric.
 //  * Principal components: C (fp32, upper triangle read) is widened to fp64
 //    and handed to rocSOLVER's symmetric divide-and-conquer eigensolver
 //    (dsyevd, loaded at the first call: the library is large and only
@@ -155,10 +157,12 @@ __global__ __launch_bounds__(256) void widen_kernel(const float* __restrict__ C,
     }
 }
 
-// C[r][c] = P[r][c] + P[c][r] for r, c < K: a 64 x 64 tile of P and the
-// mirrored tile, the latter read row-contiguously and transposed in LDS.
+// C[r][c] = beta·C[r][c] + alpha·(P[r][c] + P[c][r]) for r, c < K (C is not
+// read when beta == 0): a 64 x 64 tile of P and the mirrored tile, the latter
+// read row-contiguously and transposed in LDS.
 __global__ __launch_bounds__(256) void symmetrize_kernel(const float* __restrict__ P, int64_t ldp,
-                                                         float* __restrict__ C, int64_t ldc, int K) {
+                                                         float* __restrict__ C, int64_t ldc, int K, float alpha,
+                                                         float beta) {
     __shared__ float t[64][65];
     const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
@@ -171,7 +175,11 @@ __global__ __launch_bounds__(256) void symmetrize_kernel(const float* __restrict
 #pragma unroll 4
     for (int i = 0; i < 16; ++i) {
         const int r = r0 + ty * 16 + i, c = c0 + tx;
-        if (r < K && c < K) C[(int64_t)r * ldc + c] = P[(int64_t)r * ldp + c] + t[tx][ty * 16 + i];
+        if (r < K && c < K) {
+            const float v = alpha * (P[(int64_t)r * ldp + c] + t[tx][ty * 16 + i]);
+            float* o = C + (int64_t)r * ldc + c;
+            *o = beta != 0.f ? fmaf(beta, *o, v) : v;
+        }
     }
 }
 
@@ -367,13 +375,14 @@ size_t pca_workspace_bytes(int64_t K) {
 size_t symprod_workspace_bytes(int64_t K) { return (size_t)K * splitk_ld((int)K) * 4; }
 
 hipError_t launch_symmetrized_product(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
-                                      int64_t ldc, int K, void* workspace, hipStream_t stream) {
+                                      int64_t ldc, int K, float alpha, float beta, void* workspace,
+                                      hipStream_t stream) {
     float* P = static_cast<float*>(workspace);
     const int64_t ldp = splitk_ld(K);
     hipError_t e = launch_gemm_tn_f32(A, lda, B, ldb, P, ldp, K, K, K, stream);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(symmetrize_kernel, dim3(ceil_div_i(K, 64), ceil_div_i(K, 64)), dim3(256), 0, stream, P,
-                       ldp, C, ldc, K);
+                       ldp, C, ldc, K, alpha, beta);
     return hipGetLastError();
 }
 

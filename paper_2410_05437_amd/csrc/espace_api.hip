@@ -804,8 +804,8 @@ espace_status espace_autocorrelation_update(const void* X, int64_t ldx, float* C
 }
 
 espace_status espace_symmetrized_product(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
-                                         int64_t ldc, int64_t K, void* workspace, size_t workspace_bytes,
-                                         hipStream_t stream) {
+                                         int64_t ldc, int64_t K, float alpha, float beta, void* workspace,
+                                         size_t workspace_bytes, hipStream_t stream) {
     ESPACE_TRY(check_dims(0, K, 1, 0, false));
     if (K > kMaxSymDim) return fail(ESPACE_ERR_SHAPE, "K=%lld above %lld", (long long)K, (long long)kMaxSymDim);
     ESPACE_TRY(check_mat("A", A, K, K, lda, ESPACE_F32));
@@ -817,7 +817,8 @@ espace_status espace_symmetrized_product(const float* A, int64_t lda, const floa
                          Range{"workspace", (uintptr_t)workspace, (uintptr_t)workspace + workspace_bytes}};
     ESPACE_TRY(check_alias(mat_range("C", C, K, ldc, ESPACE_F32), ins, 3));
     ESPACE_TRY(check_device());
-    const hipError_t e = espace::launch_symmetrized_product(A, lda, B, ldb, C, ldc, (int)K, workspace, stream);
+    const hipError_t e =
+        espace::launch_symmetrized_product(A, lda, B, ldb, C, ldc, (int)K, alpha, beta, workspace, stream);
     if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "symmetrized product: %s", hipGetErrorString(e));
     return ok();
 }

@@ -114,6 +114,7 @@ size_t symprod_workspace_bytes(int64_t K);
 hipError_t launch_transpose(const void* src, int64_t lds, int rows, int cols, void* dst, int64_t ldd, bool f32,
                             hipStream_t stream);
 hipError_t launch_symmetrized_product(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
-                                      int64_t ldc, int K, void* workspace, hipStream_t stream);
+                                      int64_t ldc, int K, float alpha, float beta, void* workspace,
+                                      hipStream_t stream);
 
 }  // namespace espace

@@ -24,7 +24,7 @@ def test_exports_every_declared_function():
         "espace_dense_linear_backward"}
     for n in names:
         assert hasattr(L, n)
-    assert E.ABI_VERSION == 4
+    assert E.ABI_VERSION == 5
 
 
 def _fold(W=P16, ldw=64, Pt=P16b, ldp=64, Wf=P16c, ldwf=16, M=32, K=64, Lc=16, dt=1,
@@ -103,7 +103,7 @@ def _pca(C=P16, ldc=64, Pt=P16b, ldp=64, ev=P16c, info=ctypes.c_void_p(0x5000000
 
 
 def _sym(A=P16, lda=64, B=P16b, ldb=64, C=P16c, ldc=64, K=64, ws=ctypes.c_void_p(0x70000000), wsb=1 << 24):
-    return L.espace_symmetrized_product(A, lda, B, ldb, C, ldc, K, ws, wsb, NULL)
+    return L.espace_symmetrized_product(A, lda, B, ldb, C, ldc, K, 1.0, 0.0, ws, wsb, NULL)
 
 
 def test_calibration_validation():

@@ -320,3 +320,36 @@ def test_gomse_projection_end_to_end(E, normalize):
     q = float(np.einsum("lk,kj,lj->", P, Cref, P))
     qref = float(np.einsum("lk,kj,lj->", Pref, Cref, Pref))
     assert abs(q - qref) <= 1e-4 * abs(qref), (q, qref)
+
+
+@pytest.mark.parametrize("normalize", [False, True], ids=["NL-MSE", "NL-MSE_hat"])
+def test_nlmse_matrix_over_sequences(E, normalize):
+    """Theorem 2's NL-MSE matrix, calibrated per sequence as its proof
+    describes: for each of three sequences the autocorrelations of the
+    activations and of their gradients (alpha = 1/M_i), then accumulated with
+    alpha = 1/B, beta = 1.  Against the oracle: relative Frobenius error below
+    (N + K)·2^-24 ≈ 1e-4 (fp32 sums of the exact bf16 products, then an fp32
+    K-term product), or 2·2^-8 when the normalised vectors are rounded to
+    bf16."""
+    dev = need_gpu()
+    K = 200
+    seqs = []
+    for i, M in enumerate((300, 500, 250)):
+        X, Xs = _tokens(K, M, "bf16", seed=60 + i)
+        g = synth.upstream_gradient(M, K, 9000 + i)
+        bits = synth.bf16_bits_from_f64(g)
+        seqs.append((X, Xs, synth.f64_from_bf16_bits(bits).reshape(M, K), bits.reshape(M, K)))
+    C = torch.zeros(K, K, dtype=torch.float32, device=dev)
+    for i, (X, Xs, G, Gs) in enumerate(seqs):
+        M = X.shape[0]
+        A = torch.zeros(K, K, dtype=torch.float32, device=dev)
+        B = torch.zeros(K, K, dtype=torch.float32, device=dev)
+        E.espace_autocorrelation_update(dev_mat(Xs, "bf16", dev), A, 1.0 / M, normalize=normalize)
+        E.espace_autocorrelation_update(dev_mat(Gs, "bf16", dev), B, 1.0 / M, normalize=normalize)
+        E.espace_symmetrized_product(A, B, C, alpha=1.0 / len(seqs), beta=0.0 if i == 0 else 1.0)
+    torch.cuda.synchronize()
+    ref = oracle.nlmse_matrix([(X, G) for X, _, G, _ in seqs], normalized=normalize)
+    tol = 2 * 2.0 ** -8 if normalize else (1000 + K) * U32
+    assert oracle.rel_fro(host64(C), ref) <= tol
+    got = host64(C)
+    assert (got == got.T).all()
