@@ -50,6 +50,7 @@ def parse():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-calibration", action="store_true")
     ap.add_argument("--no-training", action="store_true")
+    ap.add_argument("--no-workloads", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--kernel-probe", action="store_true",
@@ -65,6 +66,15 @@ def to_dev(storage, device):
     t = E.padded_empty(R, C, torch.bfloat16, device)
     t.copy_(torch.from_numpy(np.ascontiguousarray(storage).view(np.int16)).view(torch.bfloat16))
     return t
+
+
+def clone_padded(t):
+    """A copy with the same padded leading dimension (torch's clone of a
+    padded view would be contiguous)."""
+    import paper_2410_05437_amd as E
+    c = E.padded_empty(t.shape[0], t.shape[1], t.dtype, t.device)
+    c.copy_(t)
+    return c
 
 
 def copies(nbytes_one):
@@ -203,9 +213,9 @@ def main():
 
     one = (Xs.numel() + Pts.numel() + Wf0.numel()) * 2
     R = copies(one)
-    Xr = [Xs] + [Xs.clone() for _ in range(R - 1)]
-    Pr = [Pts] + [Pts.clone() for _ in range(R - 1)]
-    Wfr = [Wf0] + [Wf0.clone() for _ in range(R - 1)]
+    Xr = [Xs] + [clone_padded(Xs) for _ in range(R - 1)]
+    Pr = [Pts] + [clone_padded(Pts) for _ in range(R - 1)]
+    Wfr = [Wf0] + [clone_padded(Wf0) for _ in range(R - 1)]
     Y = E.padded_empty(N, M, torch.bfloat16, dev)
     ws_bytes = E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, M, K, L, N, torch.bfloat16)
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
@@ -257,7 +267,7 @@ def main():
 
     # dense baseline with the same library, same rotation
     Rd = copies((Xs.numel() + Ws.numel()) * 2)
-    Wr = [Ws] + [Ws.clone() for _ in range(Rd - 1)]
+    Wr = [Ws] + [clone_padded(Ws) for _ in range(Rd - 1)]
     Xd = [Xr[i % R] for i in range(Rd)]
     wsd = torch.empty(max(E.espace_workspace_bytes(E.OP_DENSE, M, K, 1, N, torch.bfloat16), 1),
                       dtype=torch.uint8, device=dev)
@@ -299,6 +309,8 @@ def main():
         detail["calibration"] = calibration_lines(E, Xs, dev, stream, args)
     if not args.no_training:
         detail["training"] = training_lines(E, Xs, Pts, Ws, dev, stream, args)
+    if not args.no_workloads:
+        detail["workloads"] = workload_lines(E, acc, dev, stream, args)
 
     cpu = None
     if not args.no_cpu:
@@ -327,6 +339,66 @@ def main():
         "detail": detail,
     }
     print(json.dumps(out), flush=True)
+
+
+# prefill layers of the other workloads: (name, K, M, L, N)
+OTHER_LAYERS = [
+    ("llama2_7b_ffn_upgate", 4096, 22016, 1536, 4096),
+    ("llama2_7b_ffn_down", 11008, 4096, 1536, 4096),
+    ("gpt3_22b_ffn_up_L2458", 6144, 24576, 2458, 8192),
+    ("gpt3_22b_ffn_down_L2458", 24576, 6144, 2458, 8192),
+    ("gpt3_22b_ffn_up_L3686", 6144, 24576, 3686, 8192),
+    ("gpt3_22b_ffn_up_L1966", 6144, 24576, 1966, 8192),
+]
+
+
+def workload_lines(E, acc, dev, stream, args):
+    """The prefill layers of the other workloads (Llama2-7B FFN, GPT3-22B FFN
+    at 25/50/60% compression): µs per layer, TFLOP/s and MFMA fraction, and
+    the dense layer on the same kernels.  Random bf16 operands of the layer's
+    shape (the parity tests cover these shapes against the oracle), rotated
+    over copies larger than the last-level cache."""
+    import torch
+    bf = torch.bfloat16
+    out = {}
+    n = max(3, args.steps // 10)
+    for name, K, M, L, N in OTHER_LAYERS:
+        def mk(r, c, scale):
+            t = E.padded_empty(r, c, bf, dev)
+            t.copy_(torch.randn(r, c, device=dev) * scale)
+            return t
+        X0, Pt0, W0 = mk(N, K, 1.0), mk(L, K, K ** -0.5), mk(M, K, K ** -0.5)
+        Wf0 = E.espace_fold_weights(W0, Pt0)
+        R = copies((X0.numel() + Pt0.numel() + Wf0.numel()) * 2)
+        Xr = [X0] + [clone_padded(X0) for _ in range(R - 1)]
+        Pr = [Pt0] + [clone_padded(Pt0) for _ in range(R - 1)]
+        Wfr = [Wf0] + [clone_padded(Wf0) for _ in range(R - 1)]
+        Y = E.padded_empty(N, M, bf, dev)
+        ws = torch.empty(max(E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, M, K, L, N, bf), 1), dtype=torch.uint8,
+                         device=dev)
+        ms = time_calls(lambda i: E.espace_projected_linear(Xr[i], Pr[i], Wfr[i], Y, ws), R, n, 2, stream)
+        del Pr, Wfr
+        Rd = copies((X0.numel() + W0.numel()) * 2)
+        Wr = [W0] + [clone_padded(W0) for _ in range(Rd - 1)]
+        wsd = torch.empty(max(E.espace_workspace_bytes(E.OP_DENSE, M, K, 1, N, bf), 1), dtype=torch.uint8,
+                          device=dev)
+        ms_d = time_calls(lambda i: E.espace_dense_linear(Xr[i % R], Wr[i], Y, wsd), Rd, n, 2, stream)
+        tf = acc.projected_flops(K, M, L, N) / (ms * 1e-3) / 1e12
+        tfd = acc.dense_flops(K, M, N) / (ms_d * 1e-3) / 1e12
+        out[name] = {
+            "K": K, "M": M, "L": L, "N": N,
+            "compression": round(acc.compression(K, M, L), 4),
+            "us_per_layer": round(ms * 1e3, 1),
+            "tflops": round(tf, 1),
+            "mfma_frac": round(tf / PEAK_BF16_TFLOPS, 4),
+            "dense_us": round(ms_d * 1e3, 1),
+            "dense_mfma_frac": round(tfd / PEAK_BF16_TFLOPS, 4),
+            "speedup_vs_dense": round(ms_d / ms, 3),
+            "ideal_speedup": round(acc.ideal_speedup(K, M, L), 3),
+        }
+        del Xr, Wr, Y, ws, wsd, X0, Pt0, W0, Wf0
+        torch.cuda.empty_cache()
+    return out
 
 
 def training_lines(E, Xs, Pts, Ws, dev, stream, args):
@@ -443,10 +515,10 @@ def decode_lines(E, acc, synth, dev, stream, args):
     Wf = E.espace_fold_weights(Ws, Ps)
     Xall = to_dev(inp.X_s, dev)
     R = copies((Ps.numel() + Wf.numel()) * 2)
-    Pr = [Ps] + [Ps.clone() for _ in range(R - 1)]
-    Wfr = [Wf] + [Wf.clone() for _ in range(R - 1)]
+    Pr = [Ps] + [clone_padded(Ps) for _ in range(R - 1)]
+    Wfr = [Wf] + [clone_padded(Wf) for _ in range(R - 1)]
     Rd = copies(Ws.numel() * 2)
-    Wr = [Ws] + [Ws.clone() for _ in range(Rd - 1)]
+    Wr = [Ws] + [clone_padded(Ws) for _ in range(Rd - 1)]
     for N in (1, 16):
         X = Xall[:N]
         Y = E.padded_empty(N, M, torch.bfloat16, dev)
