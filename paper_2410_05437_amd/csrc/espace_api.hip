@@ -66,9 +66,15 @@ int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 Plan plan_skinny(int R, int Cc, int D) {
     // Measured on the decode layers (N <= 32): a launch costs a few µs
     // whatever its size, so the depth is split only when the tokens make
-    // each workgroup's loads heavy; 8 waves with 6 loads in flight fit
-    // 48-step depths exactly; 32-row groups halve the token re-reads from L2
-    // when there are 9 or more tokens.
+    // each workgroup's loads heavy or the depth is very large; 8 waves with
+    // 6 loads in flight fit 48-step depths exactly; 32-row groups halve the
+    // token re-reads from L2 when there are 9 or more tokens.  With at most 8
+    // tokens and fewer 16-row groups than half the CUs (the projection,
+    // L = 1536 rows), two depth segments per MFMA operand double the
+    // workgroups in one launch (K = 4096: 5.6 against 7.5 µs; K = 11008:
+    // 12.5 against 17.6 µs with a three-way split); with 128 or more groups
+    // one depth range is fastest up to 256 steps (K = 6144, L = 3686: 12.3
+    // against 17.6 µs with two ranges).
     Plan p;
     p.kind = KIND_SKINNY;
     const int nb1 = ceil_div(Cc, 16);
@@ -77,10 +83,13 @@ Plan plan_skinny(int R, int Cc, int D) {
     if (nb1 >= target) {
         if (R > 8) p.tile = espace::SKINNY_RG2_W4;
         else p.tile = (steps <= 48) ? espace::SKINNY_RG1_W8_U6 : espace::SKINNY_RG1_W8_U8;
+    } else if (R <= 8 && nb1 < kNumCUs / 2 && steps <= 384) {
+        p.tile = steps <= 128 ? espace::SKINNY_SEG2_W8_U8 : espace::SKINNY_SEG2_W16_U4;
     } else {
         p.tile = espace::SKINNY_RG1_W8_U8;
         int s = R > 8 ? 2 : 1;
-        const int by_depth = ceil_div(steps, 128);   // at most 128 KB of each 16 rows per workgroup
+        // at most 128 KB of each 16 rows per workgroup beyond 256 steps
+        const int by_depth = (R > 8 || steps > 256) ? ceil_div(steps, 128) : 1;
         if (by_depth > s) s = by_depth;
         if (s > 1 && steps / s < 32) s = steps / 32 > 1 ? steps / 32 : 1;   // >= 4 steps per wave
         p.splits = s;
@@ -203,7 +212,7 @@ const Override& tile_override() {
         if (const char* s = std::getenv("ESPACE_VARIANT")) r.variant = std::atoi(s);
         if (const char* s = std::getenv("ESPACE_SKINNY")) {
             const int v = std::atoi(s);
-            if (v >= espace::SKINNY_RG1_W4 && v <= espace::SKINNY_RG1_W16_U4) r.skinny = v;
+            if (v >= espace::SKINNY_RG1_W4 && v <= espace::SKINNY_SEG2_W16_U4) r.skinny = v;
         }
         return r;
     }();
@@ -217,6 +226,11 @@ Plan plan_tn(int64_t R, int64_t Cc, int64_t D, espace_dtype dt) {
         const Override& o = tile_override();
         if (!o.applies(R, Cc, D)) return p;
         if (o.skinny >= 0) p.tile = o.skinny;
+        if (p.tile >= espace::SKINNY_SEG2_W8_U4) {   // segmented kernels take one depth range
+            p.splits = 1;
+            p.partial_bytes = 0;
+            return p;
+        }
         if (o.splits > 0) {
             p.splits = o.splits < ceil_div(D, 32) ? o.splits : (int)ceil_div(D, 32);
             p.partial_bytes = p.splits > 1 ? (size_t)p.splits * R * espace::splitk_ld(Cc) * sizeof(float) : 0;

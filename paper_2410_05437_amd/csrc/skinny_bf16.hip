@@ -14,6 +14,17 @@
 // are reduced through LDS in a fixed order; several depth ranges (split > 1)
 // write fp32 partials that a second kernel sums in a fixed order, so results
 // do not depend on scheduling.
+//
+// Depth segments (SEG = 2 or 4, at most 16/SEG tokens).  With few rows of B
+// (the projection, L rows) 16-row groups leave most CUs idle, and a depth
+// split costs a second launch.  Instead the 16 rows of the MFMA operand are
+// 16/SEG rows of B times SEG depth segments: operand row r is row r/SEG of
+// the group over segment r%SEG, and token column c is token c/SEG over
+// segment c%SEG.  The diagonal blocks (row segment = column segment) of the
+// 16x16 result hold the per-segment partial dot products; the SEG of them
+// for one (row, token) sit in SEG neighbouring lanes and are summed with
+// lane exchanges in a fixed order.  A workgroup then owns 16/SEG rows, so
+// SEG times as many workgroups share the stream, in one launch.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -23,32 +34,38 @@ namespace {
 
 constexpr int STEP = 32;   // reduced elements per MFMA
 
-template <int RG, int TG, int WAVES, int UNROLL>
+template <int RG, int TG, int WAVES, int UNROLL, int SEG>
 __global__ __launch_bounds__(WAVES * 64)
 void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
                            const uint16_t* __restrict__ B, int64_t ldb,
                            void* __restrict__ Cout, int64_t ldc,
                            int R, int Cc, int D, int steps_per_split,
                            int out_f32, int64_t split_stride) {
+    static_assert(SEG == 1 || (TG == 1 && (SEG == 2 || SEG == 4)), "segments: 2 or 4, one token group");
+    constexpr int GROWS = 16 / SEG;    // rows of B per 16-row operand
     __shared__ f32x4_t red[WAVES - 1][RG * TG][64];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int j0 = blockIdx.x * (16 * RG);
-    const int nsteps = (D + STEP - 1) / STEP;
+    const int j0 = blockIdx.x * (GROWS * RG);
+    // steps per depth segment (the whole depth when SEG == 1)
+    const int nsteps = ((D + STEP - 1) / STEP + SEG - 1) / SEG;
     const int s_begin = blockIdx.y * steps_per_split;
     int s_end = s_begin + steps_per_split;
     s_end = s_end < nsteps ? s_end : nsteps;
-    // steps whose 32 elements all lie below D
-    const int s_fast_end = s_end < D / STEP ? s_end : D / STEP;
 
-    const int lr = lane & 15;          // B row / token inside a 16-wide group
+    const int lr = lane & 15;          // operand row / token column inside a 16-wide group
     const int lk = (lane >> 4) * 8;    // element offset of this lane's chunk
+    const int seg = lr % SEG;          // depth segment of this lane's row and column
+    const int koff = seg * nsteps * STEP + lk;
+    // steps whose 32 elements lie below D in every segment
+    const int dlast = D - (SEG - 1) * nsteps * STEP;
+    const int s_fast_end = dlast <= 0 ? 0 : (s_end < dlast / STEP ? s_end : dlast / STEP);
 
     const uint16_t* brow[RG];
 #pragma unroll
     for (int g = 0; g < RG; ++g) {
-        int j = j0 + g * 16 + lr;
+        int j = j0 + g * GROWS + lr / SEG;
         j = j < Cc ? j : Cc - 1;
         brow[g] = B + (int64_t)j * ldb;
     }
@@ -57,7 +74,7 @@ void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
     uint32_t amask[TG];
 #pragma unroll
     for (int t = 0; t < TG; ++t) {
-        const int n = t * 16 + lr;
+        const int n = t * 16 + lr / SEG;
         amask[t] = n < R ? 0xffffffffu : 0u;
         arow[t] = A + (int64_t)(n < R ? n : 0) * lda;
     }
@@ -76,7 +93,7 @@ void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
         u32x4_t va[UNROLL][TG];
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
-            const int k = (s0 + u * WAVES) * STEP + lk;
+            const int k = (s0 + u * WAVES) * STEP + koff;
 #pragma unroll
             for (int g = 0; g < RG; ++g) vb[u][g] = *reinterpret_cast<const u32x4_t*>(brow[g] + k);
 #pragma unroll
@@ -101,7 +118,7 @@ void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
             const int s = s0 + u * WAVES;
-            const int k = s * STEP + lk;
+            const int k = s * STEP + koff;
             valid[u] = s < s_end ? D - k : 0;
             const int kk = valid[u] > 0 ? k : 0;
 #pragma unroll
@@ -143,6 +160,48 @@ void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
 #pragma unroll
             for (int t = 0; t < TG; ++t) acc[g][t] += red[w][g * TG + t][lane];
 
+    if (SEG > 1) {
+        // Lane l holds operand rows 4*(l/16) + i (i < 4), that is rows
+        // 4*(l/16)/SEG + i/SEG of the group over segments i%SEG, and token
+        // column l%16.  Its diagonal entries are i = seg + SEG*c, for the
+        // 4/SEG consecutive rows c; the SEG lanes of one token add theirs.
+        constexpr int OUTS = 4 / SEG;
+        const int n = lr / SEG;
+#pragma unroll
+        for (int g = 0; g < RG; ++g) {
+            float d[OUTS];
+#pragma unroll
+            for (int c = 0; c < OUTS; ++c) {
+                float v = acc[g][0][SEG * c];
+#pragma unroll
+                for (int h = 1; h < SEG; ++h) v = seg == h ? acc[g][0][SEG * c + h] : v;
+                d[c] = v;
+            }
+#pragma unroll
+            for (int m = 1; m < SEG; m <<= 1)
+#pragma unroll
+                for (int c = 0; c < OUTS; ++c) d[c] += __shfl_xor(d[c], m);
+            if (seg != 0 || n >= R) continue;
+            const int jb = j0 + g * GROWS + (lane >> 4) * OUTS;
+            if (out_f32) {
+                float* C = reinterpret_cast<float*>(Cout) + (int64_t)n * ldc;
+#pragma unroll
+                for (int c = 0; c < OUTS; ++c)
+                    if (jb + c < Cc) C[jb + c] = d[c];
+            } else {
+                uint16_t* C = reinterpret_cast<uint16_t*>(Cout) + (int64_t)n * ldc;
+                if (OUTS == 2 && jb + 1 < Cc) {
+                    *reinterpret_cast<uint32_t*>(C + jb) = pack_bf16x2(d[0], d[OUTS - 1]);
+                } else {
+#pragma unroll
+                    for (int c = 0; c < OUTS; ++c)
+                        if (jb + c < Cc) C[jb + c] = (uint16_t)bf16_rne(d[c]);
+                }
+            }
+        }
+        return;
+    }
+
     // accumulator i of lane l holds B row 4*(l/16) + i and token l%16 of its
     // 16x16 tile: four consecutive output columns of one token row
 #pragma unroll
@@ -174,22 +233,24 @@ void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
     }
 }
 
-template <int RG, int TG, int WAVES, int UNROLL>
+template <int RG, int TG, int WAVES, int UNROLL, int SEG = 1>
 hipError_t launch_skinny_cfg(const GemmArgs& g, hipStream_t stream) {
-    const int nsteps = (g.D + STEP - 1) / STEP;
+    const int nsteps = ((g.D + STEP - 1) / STEP + SEG - 1) / SEG;
     const int S = g.splits;
+    if (SEG > 1 && (S != 1 || g.R > 16 / SEG)) return hipErrorInvalidValue;
     const int sps = (nsteps + S - 1) / S;
-    dim3 grid((g.Cc + 16 * RG - 1) / (16 * RG), S);
+    const int rows = 16 / SEG * RG;
+    dim3 grid((g.Cc + rows - 1) / rows, S);
     dim3 block(WAVES * 64);
     if (S == 1) {
-        hipLaunchKernelGGL((skinny_tn_bf16_kernel<RG, TG, WAVES, UNROLL>), grid, block, 0, stream,
+        hipLaunchKernelGGL((skinny_tn_bf16_kernel<RG, TG, WAVES, UNROLL, SEG>), grid, block, 0, stream,
                            g.A, g.lda, g.B, g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, sps, g.c_f32,
                            (int64_t)0);
         return hipGetLastError();
     }
     const int64_t ldp = splitk_ld(g.Cc);
     const int64_t split_stride = (int64_t)g.R * ldp;
-    hipLaunchKernelGGL((skinny_tn_bf16_kernel<RG, TG, WAVES, UNROLL>), grid, block, 0, stream,
+    hipLaunchKernelGGL((skinny_tn_bf16_kernel<RG, TG, WAVES, UNROLL, SEG>), grid, block, 0, stream,
                        g.A, g.lda, g.B, g.ldb, (void*)g.partial, ldp, g.R, g.Cc, g.D, sps, 1,
                        split_stride);
     hipError_t e = hipGetLastError();
@@ -221,6 +282,12 @@ hipError_t launch_skinny_tn_bf16(const GemmArgs& g, hipStream_t stream) {
         case SKINNY_RG2_W4_U6: return launch_skinny_tg<2, 4, 6>(g, stream);
         case SKINNY_RG1_W16_U8: return launch_skinny_tg<1, 16, 8>(g, stream);
         case SKINNY_RG1_W16_U4: return launch_skinny_tg<1, 16, 4>(g, stream);
+        case SKINNY_SEG2_W8_U4: return launch_skinny_cfg<1, 1, 8, 4, 2>(g, stream);
+        case SKINNY_SEG2_W8_U8: return launch_skinny_cfg<1, 1, 8, 8, 2>(g, stream);
+        case SKINNY_SEG4_W8_U4: return launch_skinny_cfg<1, 1, 8, 4, 4>(g, stream);
+        case SKINNY_SEG4_W4_U8: return launch_skinny_cfg<1, 1, 4, 8, 4>(g, stream);
+        case SKINNY_SEG4_W4_U4: return launch_skinny_cfg<1, 1, 4, 4, 4>(g, stream);
+        case SKINNY_SEG2_W16_U4: return launch_skinny_cfg<1, 1, 16, 4, 2>(g, stream);
         default: return hipErrorInvalidValue;
     }
 }

@@ -65,6 +65,20 @@ def stats(args):
         d = sorted(_dur_us(r) for r in rs)
         if d:
             lines.append(f"| {name} | {len(d)} | {sum(d) / len(d):.1f} | {d[len(d) // 2]:.1f} |")
+    # decode at N = 1 (Llama2-7B FFN up+gate, K=4096, M=22016, L=1536): each
+    # kernel streams one weight-sized operand once; identified by template and grid
+    dec = [("projection: Pt, 1536 x 4096", "skinny_tn_bf16_kernel<1, 1, 8, 8>", "49152 x 1", 1536 * 4096 * 2),
+           ("expansion: Wf, 22016 x 1536", "skinny_tn_bf16_kernel<1, 1, 8, 6>", "704512 x 1", 22016 * 1536 * 2),
+           ("dense: W, 22016 x 4096", "skinny_tn_bf16_kernel<1, 1, 8, 8>", "704512 x 1", 22016 * 4096 * 2)]
+    lines += ["", "Decode kernels at N = 1 (Llama2-7B FFN up+gate), bytes of the streamed operand over the "
+              "median duration:", "", "| kernel | streamed bytes | median (us) | GB/s | HBM fraction (8 TB/s) |",
+              "|---|---|---|---|---|"]
+    for name, k, grid, nbytes in dec:
+        v = sorted(d for (gk, gg), ds in groups.items() if gk.endswith(k) and gg == grid for d in ds)
+        if v:
+            med = v[len(v) // 2]
+            lines.append(f"| {name} | {nbytes} | {med:.1f} | {nbytes / med / 1e3:.0f} | "
+                         f"{nbytes / med / 1e3 / 8000:.2f} |")
     open(args.out, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
 

@@ -65,12 +65,33 @@ DEGENERATE = [
 ]
 
 
+# bfloat16 decode plans at N <= 8 (the sizes of the Llama2-7B projection and
+# beyond): two depth segments per MFMA operand with 16 waves (the projection,
+# 9 or 96 row groups over 141 steps) and with 8 waves (the expansion, 57 row
+# groups over 5 steps); one depth range of 132 steps for 132 row groups.
+DECODE_PLANS = [
+    (4500, 900, 136, 8),
+    (4500, 900, 136, 1),
+    (4500, 700, 1536, 2),
+    (4500, 2100, 4200, 3),
+]
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("shape", SHAPES + DEGENERATE, ids=lambda s: "K%d_M%d_L%d_N%d" % s)
 def test_each_entry_point(E, dtype, shape):
+    _check_entry_points(E, dtype, shape)
+
+
+@pytest.mark.parametrize("shape", DECODE_PLANS, ids=lambda s: "K%d_M%d_L%d_N%d" % s)
+def test_decode_plans(E, shape):
+    _check_entry_points(E, "bf16", shape, seed=45)
+
+
+def _check_entry_points(E, dtype, shape, seed=0):
     dev = need_gpu()
     K, M, L, N = shape
-    inp = _inputs(K, M, L, N, dtype)
+    inp = _inputs(K, M, L, N, dtype, seed=seed)
     X, Pt, W = _dev_inputs(inp, dev)
     tol = TOL[dtype]
 
