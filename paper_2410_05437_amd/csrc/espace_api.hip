@@ -226,7 +226,7 @@ Plan plan_tn(int64_t R, int64_t Cc, int64_t D, espace_dtype dt) {
         const Override& o = tile_override();
         if (!o.applies(R, Cc, D)) return p;
         if (o.skinny >= 0) p.tile = o.skinny;
-        if (p.tile >= espace::SKINNY_SEG2_W8_U4) {   // segmented kernels take one depth range
+        if (p.tile >= espace::SKINNY_SEG2_W8_U8) {   // segmented kernels take one depth range
             p.splits = 1;
             p.partial_bytes = 0;
             return p;
@@ -267,7 +267,15 @@ Plan plan_tn_logged(int64_t R, int64_t Cc, int64_t D, espace_dtype dt) {
     return p;
 }
 
-int64_t z_ld(int64_t L, espace_dtype dt) { return round_up(L, dt == ESPACE_BF16 ? 64 : 32); }
+// Leading dimension of Z in the workspace.  For decode (N <= 32, bf16) the
+// rows are offset by a further 64 bytes: every workgroup of the expansion
+// reads the same few Z rows at the same depth, and rows 3 KB apart (L = 1536)
+// meet in the same memory channels (measured on the Llama2-7B up+gate
+// expansion: 19.9 -> 19.1 µs at 16 tokens, 24.3 -> 22.5 µs at 32).
+int64_t z_ld(int64_t L, int64_t N, espace_dtype dt) {
+    if (dt != ESPACE_BF16) return round_up(L, 32);
+    return round_up(L, 64) + (N <= 32 ? 32 : 0);
+}
 
 // One-launch decode path (bf16, N <= 32).  It is selected per call with
 // ESPACE_DECODE=fused; by default the two-launch path runs, which is faster
@@ -302,7 +310,7 @@ size_t fused_sync_bytes(int64_t N, int64_t L, espace_dtype dt) {
 
 
 size_t z_bytes(int64_t N, int64_t L, espace_dtype dt) {
-    return align_ws((size_t)N * z_ld(L, dt) * elem_size(dt));
+    return align_ws((size_t)N * z_ld(L, N, dt) * elem_size(dt));
 }
 
 // Workspace of the training-view gradients: transposed operands (the GEMM
@@ -640,7 +648,7 @@ espace_status espace_projected_linear(const void* X, int64_t ldx, const void* Pt
     const Range wsr{"workspace", ws.lo, ws.lo + need};
     ESPACE_TRY(check_alias(wsr, ins, 3));
     ESPACE_TRY(check_device());
-    const int64_t ldz = z_ld(L, dt);
+    const int64_t ldz = z_ld(L, N, dt);
     void* Z = workspace;
     void* partial = (char*)workspace + z_bytes(N, L, dt);
     if (use_fused_decode(N, L, dt)) {

@@ -28,12 +28,8 @@ enum TileKind {
     SKINNY_RG2_W4_U6 = 19,
     SKINNY_RG1_W16_U8 = 20,  // 16 waves: one workgroup keeps 128 steps in flight
     SKINNY_RG1_W16_U4 = 21,
-    SKINNY_SEG2_W8_U4 = 22,  // 8 rows x 2 depth segments per MFMA operand, N <= 8
-    SKINNY_SEG2_W8_U8 = 23,
-    SKINNY_SEG4_W8_U4 = 24,  // 4 rows x 4 depth segments per MFMA operand, N <= 4
-    SKINNY_SEG4_W4_U8 = 25,
-    SKINNY_SEG4_W4_U4 = 26,
-    SKINNY_SEG2_W16_U4 = 27,
+    SKINNY_SEG2_W8_U8 = 22,  // 8 rows x 2 depth segments per MFMA operand, N <= 8
+    SKINNY_SEG2_W16_U4 = 23,
 };
 
 // One "TN" product C[r][c] = sum_k A[r][k] * B[c][k]  (bf16 in, fp32 accumulate).

@@ -282,11 +282,7 @@ hipError_t launch_skinny_tn_bf16(const GemmArgs& g, hipStream_t stream) {
         case SKINNY_RG2_W4_U6: return launch_skinny_tg<2, 4, 6>(g, stream);
         case SKINNY_RG1_W16_U8: return launch_skinny_tg<1, 16, 8>(g, stream);
         case SKINNY_RG1_W16_U4: return launch_skinny_tg<1, 16, 4>(g, stream);
-        case SKINNY_SEG2_W8_U4: return launch_skinny_cfg<1, 1, 8, 4, 2>(g, stream);
         case SKINNY_SEG2_W8_U8: return launch_skinny_cfg<1, 1, 8, 8, 2>(g, stream);
-        case SKINNY_SEG4_W8_U4: return launch_skinny_cfg<1, 1, 8, 4, 4>(g, stream);
-        case SKINNY_SEG4_W4_U8: return launch_skinny_cfg<1, 1, 4, 8, 4>(g, stream);
-        case SKINNY_SEG4_W4_U4: return launch_skinny_cfg<1, 1, 4, 4, 4>(g, stream);
         case SKINNY_SEG2_W16_U4: return launch_skinny_cfg<1, 1, 16, 4, 2>(g, stream);
         default: return hipErrorInvalidValue;
     }
