@@ -1,0 +1,172 @@
+// Bandwidth-oriented bfloat16 product for one or two tokens (decode):
+//
+//     C[n][j] = sum_k A[n][k] * B[j][k],   n < R <= 2 (tokens), j < Cc
+//
+// One wave streams whole rows of B: lane l reads the 8-element chunks l,
+// l + 64, l + 128, ... of a row, so every load instruction of a wave covers
+// 1 KB of contiguous memory (the MFMA kernel's loads cover 16 rows x 64 B,
+// which the memory system serves at a lower rate).  The tokens are staged
+// once per workgroup in LDS, zero beyond D and for token rows >= R.  The
+// arithmetic is on the vector ALU with bf16 pair dot products accumulating in
+// fp32 (with so few tokens the 16 columns of an MFMA operand would be mostly
+// empty): each lane adds its chunks in order, then a butterfly over the 64
+// lanes gives the sum, and the lane of a token writes it.  The order is fixed, so results do not depend on
+// scheduling.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace espace {
+
+namespace {
+
+constexpr int GV_WAVES = 4;
+constexpr int GV_MAX_UB = 8;                   // 1 KB loads in flight per wave
+constexpr int GV_LDS_MAX = 64 * 1024;          // token staging per workgroup
+constexpr int GV_TARGET_WAVES = 256 * 16;      // rows are spread over about this many waves
+
+int gv_tokens(int R) { return R <= 1 ? 1 : 2; }
+int gv_passes(int D) { return ((D + 7) / 8 + 63) / 64; }
+
+// acc + sum of the products of two chunks of 8 bfloat16 values, in element
+// order, two products per instruction (v_dot2c_f32_bf16: the product of two
+// bfloat16 values is exact in fp32).  The four words are named one by one:
+// a bit cast of a subscripted vector element inside a loop compiled to the
+// first element every time with this compiler.
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float acc) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b),
+                                           acc, false);
+}
+
+__device__ __forceinline__ float dot_chunk(u32x4_t a, u32x4_t b, float acc) {
+    acc = dot2(a.x, b.x, acc);
+    acc = dot2(a.y, b.y, acc);
+    acc = dot2(a.z, b.z, acc);
+    return dot2(a.w, b.w, acc);
+}
+
+template <int NT, int UB>
+__global__ __launch_bounds__(GV_WAVES * 64)
+void gemv_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
+                         const uint16_t* __restrict__ B, int64_t ldb,
+                         void* __restrict__ Cout, int64_t ldc,
+                         int R, int Cc, int D, int rows_per_wave, int out_f32) {
+    extern __shared__ u32x4_t tok[];    // [NT][ldt] chunks of 8 bf16
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int nch = (D + 7) >> 3;       // chunks per row
+    const int npass = (nch + 63) >> 6;  // 64-chunk passes per row
+    const int ldt = npass << 6;
+
+    // staging: four chunks per thread in flight; chunks outside the tokens
+    // load the first chunk of A and are zeroed
+    constexpr int SU = 4;
+    for (int i0 = threadIdx.x; i0 < NT * ldt; i0 += SU * GV_WAVES * 64) {
+        u32x4_t v[SU];
+        int valid[SU];
+#pragma unroll
+        for (int s = 0; s < SU; ++s) {
+            const int i = i0 + s * GV_WAVES * 64;
+            const int n = i / ldt;
+            const int c = i - n * ldt;
+            valid[s] = (i < NT * ldt && n < R && c < nch) ? D - 8 * c : 0;
+            v[s] = *reinterpret_cast<const u32x4_t*>(A + (valid[s] > 0 ? (int64_t)n * lda + 8 * c : 0));
+        }
+#pragma unroll
+        for (int s = 0; s < SU; ++s) {
+            const int i = i0 + s * GV_WAVES * 64;
+            if (i < NT * ldt) tok[i] = mask_chunk(v[s], valid[s]);
+        }
+    }
+    __syncthreads();
+
+    const int j_begin = (blockIdx.x * GV_WAVES + wave) * rows_per_wave;
+    const int j_end = j_begin + rows_per_wave < Cc ? j_begin + rows_per_wave : Cc;
+    for (int j = j_begin; j < j_end; ++j) {
+        const uint16_t* brow = B + (int64_t)j * ldb;
+        float acc[NT];
+#pragma unroll
+        for (int n = 0; n < NT; ++n) acc[n] = 0.f;
+        for (int p0 = 0; p0 < npass; p0 += UB) {
+            // UB passes of loads in flight; passes past the row load its
+            // first chunk and are masked
+            u32x4_t w[UB];
+            int valid[UB];
+#pragma unroll
+            for (int u = 0; u < UB; ++u) {
+                const int c = (p0 + u) * 64 + lane;
+                valid[u] = p0 + u < npass ? D - 8 * c : 0;
+                w[u] = *reinterpret_cast<const u32x4_t*>(brow + (valid[u] > 0 ? 8 * c : 0));
+            }
+            if ((p0 + UB) * 512 <= D) {
+                // every chunk of these passes lies inside the row
+#pragma unroll
+                for (int u = 0; u < UB; ++u)
+#pragma unroll
+                    for (int n = 0; n < NT; ++n)
+                        acc[n] = dot_chunk(w[u], tok[n * ldt + (p0 + u) * 64 + lane], acc[n]);
+            } else {
+#pragma unroll
+                for (int u = 0; u < UB; ++u) {
+                    const u32x4_t wv = mask_chunk(w[u], valid[u]);
+                    const uint32_t keep = valid[u] > 0 ? 0xffffffffu : 0u;
+                    const int c = valid[u] > 0 ? (p0 + u) * 64 + lane : 0;
+#pragma unroll
+                    for (int n = 0; n < NT; ++n) acc[n] = dot_chunk(wv, tok[n * ldt + c] & keep, acc[n]);
+                }
+            }
+        }
+        float out = 0.f;
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+            float v = acc[n];
+#pragma unroll
+            for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+            out = lane == n ? v : out;
+        }
+        if (lane < NT && lane < R) {
+            if (out_f32) reinterpret_cast<float*>(Cout)[(int64_t)lane * ldc + j] = out;
+            else reinterpret_cast<uint16_t*>(Cout)[(int64_t)lane * ldc + j] = (uint16_t)bf16_rne(out);
+        }
+    }
+}
+
+template <int NT, int UB>
+hipError_t launch_ub(const GemmArgs& g, int rows_per_wave, hipStream_t stream) {
+    const size_t lds = (size_t)NT * gv_passes(g.D) * 64 * 16;
+    const int waves = (g.Cc + rows_per_wave - 1) / rows_per_wave;
+    dim3 grid((waves + GV_WAVES - 1) / GV_WAVES), block(GV_WAVES * 64);
+    hipLaunchKernelGGL((gemv_tn_bf16_kernel<NT, UB>), grid, block, lds, stream, g.A, g.lda, g.B, g.ldb,
+                       g.C, g.ldc, g.R, g.Cc, g.D, rows_per_wave, g.c_f32);
+    return hipGetLastError();
+}
+
+template <int NT>
+hipError_t launch_nt(const GemmArgs& g, int rows_per_wave, hipStream_t stream) {
+    const int np = gv_passes(g.D);
+    switch (np < GV_MAX_UB ? np : GV_MAX_UB) {
+        case 1: return launch_ub<NT, 1>(g, rows_per_wave, stream);
+        case 2: return launch_ub<NT, 2>(g, rows_per_wave, stream);
+        case 3: return launch_ub<NT, 3>(g, rows_per_wave, stream);
+        case 4: return launch_ub<NT, 4>(g, rows_per_wave, stream);
+        case 5: return launch_ub<NT, 5>(g, rows_per_wave, stream);
+        case 6: return launch_ub<NT, 6>(g, rows_per_wave, stream);
+        case 7: return launch_ub<NT, 7>(g, rows_per_wave, stream);
+        default: return launch_ub<NT, 8>(g, rows_per_wave, stream);
+    }
+}
+
+}  // namespace
+
+bool gemv_supported(int R, int D) {
+    return R >= 1 && R <= 2 && D >= 1 && (int64_t)gv_tokens(R) * gv_passes(D) * 64 * 16 <= GV_LDS_MAX;
+}
+
+hipError_t launch_gemv_tn_bf16(const GemmArgs& g, hipStream_t stream) {
+    if (!gemv_supported(g.R, g.D) || g.Cc < 1) return hipErrorInvalidValue;
+    int rows_per_wave = (g.Cc + GV_TARGET_WAVES - 1) / GV_TARGET_WAVES;
+    if (rows_per_wave < 1) rows_per_wave = 1;
+    return gv_tokens(g.R) == 1 ? launch_nt<1>(g, rows_per_wave, stream) : launch_nt<2>(g, rows_per_wave, stream);
+}
+
+}  // namespace espace

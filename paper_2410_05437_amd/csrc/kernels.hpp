@@ -67,6 +67,10 @@ hipError_t launch_gemm_tn_bf16_pp(const GemmArgs& g, hipStream_t stream);
 // output, >= 2^31 elements).
 hipError_t launch_gemm_tn_bf16_v3(const GemmArgs& g, hipStream_t stream);
 hipError_t launch_skinny_tn_bf16(const GemmArgs& g, hipStream_t stream);
+// Vector-ALU product for 1 <= R <= 2 tokens with whole-row streaming (tile,
+// splits, partial unused); gemv_supported says whether the tokens fit its LDS.
+bool gemv_supported(int R, int D);
+hipError_t launch_gemv_tn_bf16(const GemmArgs& g, hipStream_t stream);
 hipError_t launch_splitk_reduce(const float* P, int S, int64_t split_stride, int64_t ldp,
                                 void* C, int64_t ldc, int R, int Cc, int out_bf16,
                                 hipStream_t stream);

@@ -66,14 +66,19 @@ DEGENERATE = [
 
 
 # bfloat16 decode plans at N <= 8 (the sizes of the Llama2-7B projection and
-# beyond): two depth segments per MFMA operand with 16 waves (the projection,
-# 9 or 96 row groups over 141 steps) and with 8 waves (the expansion, 57 row
-# groups over 5 steps); one depth range of 132 steps for 132 row groups.
+# beyond): whole-row streaming for one and two tokens (depth 4500: nine
+# 512-element passes, a full block of eight and a partial one; depths 131 and
+# 136 inside one pass), two depth segments per MFMA operand with 16 waves (the
+# projection at 8 tokens, 9 row groups over 141 steps) and with 8 waves (its
+# expansion, 57 row groups over 5 steps); one depth range of 132 steps for 132
+# row groups (3 and 5 tokens).
 DECODE_PLANS = [
     (4500, 900, 136, 8),
     (4500, 900, 136, 1),
     (4500, 700, 1536, 2),
     (4500, 2100, 4200, 3),
+    (4500, 2100, 4200, 5),
+    (1003, 517, 131, 2),
 ]
 
 
