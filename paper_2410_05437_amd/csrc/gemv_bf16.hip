@@ -5,13 +5,21 @@
 // One wave streams whole rows of B: lane l reads the 8-element chunks l,
 // l + 64, l + 128, ... of a row, so every load instruction of a wave covers
 // 1 KB of contiguous memory (the MFMA kernel's loads cover 16 rows x 64 B,
-// which the memory system serves at a lower rate).  The tokens are staged
-// once per workgroup in LDS, zero beyond D and for token rows >= R.  The
-// arithmetic is on the vector ALU with bf16 pair dot products accumulating in
-// fp32 (with so few tokens the 16 columns of an MFMA operand would be mostly
-// empty): each lane adds its chunks in order, then a butterfly over the 64
-// lanes gives the sum, and the lane of a token writes it.  The order is fixed, so results do not depend on
-// scheduling.
+// which the memory system serves at a lower rate).  The arithmetic is on the
+// vector ALU with bf16 pair dot products accumulating in fp32 (with so few
+// tokens the 16 columns of an MFMA operand would be mostly empty): each lane
+// adds its chunks in order, then a butterfly over the 64 lanes gives the sum,
+// and the lane of a token writes it.  The order is fixed, so results do not
+// depend on scheduling.
+//
+// Rows of at most 2048 elements (four 512-element passes) take the first
+// kernel: every lane keeps its chunks of the tokens in registers, loaded
+// once, so nothing waits for a workgroup-wide staging step, and a wave loads
+// two rows per iteration.  Longer rows take the second kernel, which stages
+// the tokens in LDS once per workgroup and walks each row in blocks of up to
+// eight passes (kept there from five passes on: at eight passes the register
+// form needs twice the registers and was slower, e.g. 34.7 against 33.6 µs
+// on a 22016 x 4096 weight at one token).
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -44,6 +52,99 @@ __device__ __forceinline__ float dot_chunk(u32x4_t a, u32x4_t b, float acc) {
     return dot2(a.w, b.w, acc);
 }
 
+// Sum over the wave of each token's partial sums (fixed butterfly), written
+// by the lane of the token.
+template <int NT>
+__device__ __forceinline__ void finish_row(const float (&acc)[NT], int lane, int R, int j,
+                                           void* __restrict__ Cout, int64_t ldc, int out_f32) {
+    float out = 0.f;
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+        float v = acc[n];
+#pragma unroll
+        for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+        out = lane == n ? v : out;
+    }
+    if (lane < NT && lane < R) {
+        if (out_f32) reinterpret_cast<float*>(Cout)[(int64_t)lane * ldc + j] = out;
+        else reinterpret_cast<uint16_t*>(Cout)[(int64_t)lane * ldc + j] = (uint16_t)bf16_rne(out);
+    }
+}
+
+// Rows of at most UB passes; RB rows per iteration.
+template <int NT, int UB, int RB>
+__global__ __launch_bounds__(GV_WAVES * 64)
+void gemv_rows_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
+                           const uint16_t* __restrict__ B, int64_t ldb,
+                           void* __restrict__ Cout, int64_t ldc,
+                           int R, int Cc, int D, int rows_per_wave, int out_f32) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int nfull = D >> 9;           // passes entirely inside the row
+
+    // chunk u of this lane: elements 8 * (64 * u + lane) ...; keep[u] masks
+    // the elements at or beyond D (passes past the row: all of them, and
+    // their loads read the row's first chunk)
+    int off[UB];
+    u32x4_t keep[UB];
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+        const int c = u * 64 + lane;
+        const int valid = D - 8 * c;
+        off[u] = valid > 0 ? 8 * c : 0;
+        keep[u] = mask_chunk(u32x4_t{0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu}, valid);
+    }
+    // Token chunks as loaded (masked where used, in the partial pass): these
+    // loads stay in flight with the first rows'.  Token rows >= R load row
+    // R - 1; their sums are never written.
+    u32x4_t t[NT][UB];
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+        const uint16_t* arow = A + (int64_t)min(n, R - 1) * lda;
+#pragma unroll
+        for (int u = 0; u < UB; ++u) t[n][u] = *reinterpret_cast<const u32x4_t*>(arow + off[u]);
+    }
+
+    const int j_begin = (blockIdx.x * GV_WAVES + wave) * rows_per_wave;
+    const int j_end = j_begin + rows_per_wave < Cc ? j_begin + rows_per_wave : Cc;
+    for (int j = j_begin; j < j_end; j += RB) {
+        u32x4_t w[RB][UB];
+#pragma unroll
+        for (int r = 0; r < RB; ++r) {
+            // rows past the wave's range load its last row (not used)
+            const int jr = j + r < j_end ? j + r : j_end - 1;
+            const uint16_t* brow = B + (int64_t)jr * ldb;
+#pragma unroll
+            for (int u = 0; u < UB; ++u) w[r][u] = *reinterpret_cast<const u32x4_t*>(brow + off[u]);
+        }
+        __builtin_amdgcn_sched_barrier(0);   // all loads of the iteration issue before the first use
+#pragma unroll
+        for (int r = 0; r < RB; ++r) {
+            float acc[NT];
+#pragma unroll
+            for (int n = 0; n < NT; ++n) acc[n] = 0.f;
+#pragma unroll
+            for (int u = 0; u < UB; ++u) {
+                if (u < nfull) {
+#pragma unroll
+                    for (int n = 0; n < NT; ++n) acc[n] = dot_chunk(w[r][u], t[n][u], acc[n]);
+                } else {
+                    // both operands masked: the padding after D may hold
+                    // anything.  The empty asm keeps the masked tokens from
+                    // being hoisted out of the loop, which would make the
+                    // prologue wait for the token loads.
+                    u32x4_t k = keep[u];
+                    asm volatile("" : "+v"(k));
+#pragma unroll
+                    for (int n = 0; n < NT; ++n) acc[n] = dot_chunk(w[r][u] & k, t[n][u] & k, acc[n]);
+                }
+            }
+            if (j + r < j_end) finish_row<NT>(acc, lane, R, j + r, Cout, ldc, out_f32);
+        }
+    }
+}
+
+// Rows longer than UB passes: tokens staged in LDS, blocks of UB passes.
 template <int NT, int UB>
 __global__ __launch_bounds__(GV_WAVES * 64)
 void gemv_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
@@ -53,7 +154,7 @@ void gemv_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
     extern __shared__ u32x4_t tok[];    // [NT][ldt] chunks of 8 bf16
 
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int nch = (D + 7) >> 3;       // chunks per row
     const int npass = (nch + 63) >> 6;  // 64-chunk passes per row
     const int ldt = npass << 6;
@@ -116,18 +217,7 @@ void gemv_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
                 }
             }
         }
-        float out = 0.f;
-#pragma unroll
-        for (int n = 0; n < NT; ++n) {
-            float v = acc[n];
-#pragma unroll
-            for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
-            out = lane == n ? v : out;
-        }
-        if (lane < NT && lane < R) {
-            if (out_f32) reinterpret_cast<float*>(Cout)[(int64_t)lane * ldc + j] = out;
-            else reinterpret_cast<uint16_t*>(Cout)[(int64_t)lane * ldc + j] = (uint16_t)bf16_rne(out);
-        }
+        finish_row<NT>(acc, lane, R, j, Cout, ldc, out_f32);
     }
 }
 
@@ -141,18 +231,28 @@ hipError_t launch_ub(const GemmArgs& g, int rows_per_wave, hipStream_t stream) {
     return hipGetLastError();
 }
 
+template <int NT, int UB, int RB>
+hipError_t launch_rows(const GemmArgs& g, int rows_per_wave, hipStream_t stream) {
+    rows_per_wave = (rows_per_wave + RB - 1) / RB * RB;
+    const int waves = (g.Cc + rows_per_wave - 1) / rows_per_wave;
+    dim3 grid((waves + GV_WAVES - 1) / GV_WAVES), block(GV_WAVES * 64);
+    hipLaunchKernelGGL((gemv_rows_bf16_kernel<NT, UB, RB>), grid, block, 0, stream, g.A, g.lda, g.B, g.ldb,
+                       g.C, g.ldc, g.R, g.Cc, g.D, rows_per_wave, g.c_f32);
+    return hipGetLastError();
+}
+
 template <int NT>
 hipError_t launch_nt(const GemmArgs& g, int rows_per_wave, hipStream_t stream) {
-    const int np = gv_passes(g.D);
-    switch (np < GV_MAX_UB ? np : GV_MAX_UB) {
-        case 1: return launch_ub<NT, 1>(g, rows_per_wave, stream);
-        case 2: return launch_ub<NT, 2>(g, rows_per_wave, stream);
-        case 3: return launch_ub<NT, 3>(g, rows_per_wave, stream);
-        case 4: return launch_ub<NT, 4>(g, rows_per_wave, stream);
+    switch (gv_passes(g.D)) {
+        case 1: return launch_rows<NT, 1, 2>(g, rows_per_wave, stream);
+        case 2: return launch_rows<NT, 2, 2>(g, rows_per_wave, stream);
+        case 3: return launch_rows<NT, 3, 2>(g, rows_per_wave, stream);
+        case 4: return launch_rows<NT, 4, 2>(g, rows_per_wave, stream);
         case 5: return launch_ub<NT, 5>(g, rows_per_wave, stream);
         case 6: return launch_ub<NT, 6>(g, rows_per_wave, stream);
         case 7: return launch_ub<NT, 7>(g, rows_per_wave, stream);
-        default: return launch_ub<NT, 8>(g, rows_per_wave, stream);
+        case 8: return launch_ub<NT, 8>(g, rows_per_wave, stream);
+        default: return launch_ub<NT, GV_MAX_UB>(g, rows_per_wave, stream);
     }
 }
 

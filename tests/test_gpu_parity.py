@@ -66,9 +66,10 @@ DEGENERATE = [
 
 
 # bfloat16 decode plans at N <= 8 (the sizes of the Llama2-7B projection and
-# beyond): whole-row streaming for one and two tokens (depth 4500: nine
-# 512-element passes, a full block of eight and a partial one; depths 131 and
-# 136 inside one pass), two depth segments per MFMA operand with 16 waves (the
+# beyond): whole-row streaming for one and two tokens (tokens in LDS: depth
+# 4500, nine 512-element passes, a full block of eight and a partial one, and
+# depth 3000, six passes with a partial last; tokens in registers: depths
+# 1003, 1536, 131 and 136), two depth segments per MFMA operand with 16 waves (the
 # projection at 8 tokens, 9 row groups over 141 steps) and with 8 waves (its
 # expansion, 57 row groups over 5 steps); one depth range of 132 steps for 132
 # row groups (3 and 5 tokens).
@@ -79,6 +80,7 @@ DECODE_PLANS = [
     (4500, 2100, 4200, 3),
     (4500, 2100, 4200, 5),
     (1003, 517, 131, 2),
+    (3000, 700, 136, 1),
 ]
 
 
