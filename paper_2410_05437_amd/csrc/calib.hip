@@ -43,6 +43,30 @@ __device__ __forceinline__ float load_f(const float* p) { return *p; }
 __device__ __forceinline__ void store_f(uint16_t* p, float v) { *p = (uint16_t)bf16_rne(v); }
 __device__ __forceinline__ void store_f(float* p, float v) { *p = v; }
 
+// 1 / ||x_n|| for each token of a bfloat16 X (0 for a zero token), the sum of
+// squares in fp64.  One wave per token, 16-byte loads: lane l adds the
+// squares of chunks l, l + 64, ... in order, then a fixed butterfly.
+__global__ __launch_bounds__(256) void token_inv_norm_bf16_kernel(const uint16_t* __restrict__ X, int64_t ldx,
+                                                                  int M, int K, float* __restrict__ inv) {
+    const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (n >= M) return;
+    const uint16_t* row = X + (int64_t)n * ldx;
+    double s = 0.0;
+    for (int k = lane * 8; k < K; k += 512) {
+        const u32x4_t v = mask_chunk(*reinterpret_cast<const u32x4_t*>(row + k), K - k);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const double lo = (double)bf16_to_f32(v[e] & 0xffffu), hi = (double)bf16_to_f32(v[e] >> 16);
+            s += lo * lo;
+            s += hi * hi;
+        }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+    if (lane == 0) inv[n] = s > 0.0 ? (float)(1.0 / sqrt(s)) : 0.f;
+}
+
 // 1 / ||x_n|| for each token (0 for a zero token), the sum of squares in fp64.
 // One wave per token.
 template <typename T>
@@ -127,22 +151,84 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __r
     }
 }
 
+// Xt[k][n] = bf16(X[n][k] · inv[n]) for bfloat16 X: the 16-byte transpose
+// below with each token's scale applied as its row is loaded (the product in
+// fp32, rounded to nearest even, as the element-wise kernel above does).
+__global__ __launch_bounds__(256) void transpose_scale_bf16_kernel(const uint16_t* __restrict__ src, int64_t lds,
+                                                                   const float* __restrict__ inv,
+                                                                   uint16_t* __restrict__ dst, int64_t ldd,
+                                                                   int rows, int cols) {
+    __shared__ uint16_t t[64][66];
+    const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+    const int part = threadIdx.x & 7, line = threadIdx.x >> 3;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int r = line + 32 * h;
+        u32x4_t v = {0u, 0u, 0u, 0u};
+        if (r0 + r < rows && c0 + part * 8 < cols) {
+            v = *reinterpret_cast<const u32x4_t*>(src + (int64_t)(r0 + r) * lds + c0 + part * 8);
+            const float sc = inv[r0 + r];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                v[e] = pack_bf16x2(bf16_to_f32(v[e] & 0xffffu) * sc, bf16_to_f32(v[e] >> 16) * sc);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            t[r][part * 8 + 2 * e] = (uint16_t)(v[e] & 0xffffu);
+            t[r][part * 8 + 2 * e + 1] = (uint16_t)(v[e] >> 16);
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int c = line + 32 * h;
+        if (c0 + c >= cols || r0 + part * 8 >= rows) continue;
+        u32x4_t v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            v[e] = (uint32_t)t[part * 8 + 2 * e][c] | ((uint32_t)t[part * 8 + 2 * e + 1][c] << 16);
+        *reinterpret_cast<u32x4_t*>(dst + (int64_t)(c0 + c) * ldd + r0 + part * 8) = v;
+    }
+}
+
 // C[r][c] += alpha · Σ_s P_s[r][c], the depth ranges added in order.  With
-// tile > 0 only the tiles on and above the diagonal of P (tile x tile) hold
-// sums: an entry below them is read from its mirror P[c][r].
+// tile > 0 only the tiles on and above the diagonal of P (tile x tile, a
+// multiple of 64) hold sums: a 64 x 64 block below them reads its mirror
+// block of P row by row and transposes the sums through LDS.
 __global__ __launch_bounds__(256) void accumulate_kernel(const float* __restrict__ P, int S, int64_t stride,
                                                          int64_t ldp, float* __restrict__ C, int64_t ldc,
                                                          int R, int Cc, float alpha, int tile) {
-    const int64_t total = (int64_t)R * Cc;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        const int r = (int)(i / Cc), c = (int)(i % Cc);
-        const bool mirror = tile > 0 && r / tile > c / tile;
-        const int64_t at = mirror ? (int64_t)c * ldp + r : (int64_t)r * ldp + c;
+    __shared__ float t[64][65];
+    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    const bool mirror = tile > 0 && r0 / tile > c0 / tile;    // uniform over the block
+    if (!mirror) {
+        for (int i = ty; i < 64; i += 4) {
+            const int r = r0 + i, c = c0 + tx;
+            if (r >= R || c >= Cc) continue;
+            const int64_t at = (int64_t)r * ldp + c;
+            float s = 0.f;
+            for (int q = 0; q < S; ++q) s += P[q * stride + at];
+            float* o = C + (int64_t)r * ldc + c;
+            *o = fmaf(alpha, s, *o);
+        }
+        return;
+    }
+    for (int i = ty; i < 64; i += 4) {
+        const int pr = c0 + i, pc = r0 + tx;    // P[pr][pc] is the mirror of C[pc][pr]
         float s = 0.f;
-        for (int q = 0; q < S; ++q) s += P[q * stride + at];
+        if (pr < Cc && pc < R) {
+            const int64_t at = (int64_t)pr * ldp + pc;
+            for (int q = 0; q < S; ++q) s += P[q * stride + at];
+        }
+        t[i][tx] = s;
+    }
+    __syncthreads();
+    for (int i = ty; i < 64; i += 4) {
+        const int r = r0 + i, c = c0 + tx;
+        if (r >= R || c >= Cc) continue;
         float* o = C + (int64_t)r * ldc + c;
-        *o = fmaf(alpha, s, *o);
+        *o = fmaf(alpha, t[tx][i], *o);
     }
 }
 
@@ -311,17 +397,19 @@ hipError_t launch_autocorr_update(const void* X, int64_t ldx, int M, int K, bool
             hipLaunchKernelGGL(token_inv_norm_kernel<float>, dim3(ceil_div_i(M, 4)), dim3(256), 0, stream,
                                static_cast<const float*>(X), ldx, M, K, inv);
         else
-            hipLaunchKernelGGL(token_inv_norm_kernel<uint16_t>, dim3(ceil_div_i(M, 4)), dim3(256), 0, stream,
+            hipLaunchKernelGGL(token_inv_norm_bf16_kernel, dim3(ceil_div_i(M, 4)), dim3(256), 0, stream,
                                static_cast<const uint16_t*>(X), ldx, M, K, inv);
     }
     const dim3 tgrid(ceil_div_i(M, 64), ceil_div_i(K, 64));
     if (f32)
         hipLaunchKernelGGL(transpose_scale_kernel<float>, tgrid, dim3(256), 0, stream, static_cast<const float*>(X),
                            ldx, normalize ? inv : nullptr, reinterpret_cast<float*>(ws), ldt, M, K);
+    else if (normalize)
+        hipLaunchKernelGGL(transpose_scale_bf16_kernel, tgrid, dim3(256), 0, stream,
+                           static_cast<const uint16_t*>(X), ldx, inv, reinterpret_cast<uint16_t*>(ws), ldt, M, K);
     else
-        hipLaunchKernelGGL(transpose_scale_kernel<uint16_t>, tgrid, dim3(256), 0, stream,
-                           static_cast<const uint16_t*>(X), ldx, normalize ? inv : nullptr,
-                           reinterpret_cast<uint16_t*>(ws), ldt, M, K);
+        hipLaunchKernelGGL(transpose_bf16_kernel, tgrid, dim3(256), 0, stream, static_cast<const uint16_t*>(X),
+                           ldx, reinterpret_cast<uint16_t*>(ws), ldt, M, K);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
 
@@ -345,10 +433,8 @@ hipError_t launch_autocorr_update(const void* X, int64_t ldx, int M, int K, bool
         if (e == hipSuccess && used != S) return hipErrorInvalidValue;
     }
     if (e != hipSuccess) return e;
-    const int64_t total = (int64_t)K * K;
-    const int blocks = (int)(total / 256 < 4096 ? (total + 255) / 256 : 4096);
-    hipLaunchKernelGGL(accumulate_kernel, dim3(blocks), dim3(256), 0, stream, part, S, (int64_t)K * ldp, ldp, C,
-                       ldc, K, K, alpha, f32 ? 0 : 256);
+    hipLaunchKernelGGL(accumulate_kernel, dim3(ceil_div_i(K, 64), ceil_div_i(K, 64)), dim3(256), 0, stream, part,
+                       S, (int64_t)K * ldp, ldp, C, ldc, K, K, alpha, f32 ? 0 : 256);
     return hipGetLastError();
 }
 
