@@ -81,15 +81,20 @@ def copies(nbytes_one):
     return max(1, int(np.ceil(ROTATE_BYTES / max(nbytes_one, 1))))
 
 
-def time_calls(fn, n_args, steps, warmup, stream):
+def time_calls(fn, n_args, steps, warmup, stream, prequeue=False):
     """Average ms per call over `steps` calls (after `warmup`), rotating over
-    the argument sets so each call streams its operands from HBM."""
+    the argument sets so each call streams its operands from HBM.  With
+    `prequeue` a GPU sleep is enqueued before the start event, so that the
+    host has queued every call by the time the GPU reaches them: calls of a
+    few µs are then timed on the GPU, not at the host's launch rate."""
     import torch
     for i in range(warmup):
         fn(i % n_args)
     torch.cuda.synchronize()
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
+    if prequeue:
+        torch.cuda._sleep(int(5e7))
     start.record(stream)
     for i in range(steps):
         fn(i % n_args)
@@ -535,9 +540,9 @@ def decode_lines(E, acc, synth, dev, stream, args):
         wsd = torch.empty(max(E.espace_workspace_bytes(E.OP_DENSE, M, K, 1, N, torch.bfloat16), 1),
                           dtype=torch.uint8, device=dev)
         ms = time_calls(lambda i: E.espace_projected_linear(X, Pr[i], Wfr[i], Y, ws), R,
-                        args.steps * 4, args.warmup, stream)
+                        args.steps * 4, args.warmup, stream, prequeue=True)
         msd = time_calls(lambda i: E.espace_dense_linear(X, Wr[i], Y, wsd), Rd,
-                         args.steps * 4, args.warmup, stream)
+                         args.steps * 4, args.warmup, stream, prequeue=True)
         by = acc.projected_bytes(K, M, L, N)
         byd = acc.dense_bytes(K, M, N)
         res[f"N{N}"] = {

@@ -68,8 +68,8 @@ def stats(args):
     # decode at N = 1 (Llama2-7B FFN up+gate, K=4096, M=22016, L=1536): each
     # kernel streams one weight-sized operand once; identified by template and grid
     dec = [("projection: Pt, 1536 x 4096", "gemv_tn_bf16_kernel<1, 8>", "98304 x 1", 1536 * 4096 * 2),
-           ("expansion: Wf, 22016 x 1536", "gemv_rows_bf16_kernel<1, 3, 2>", "235008 x 1", 22016 * 1536 * 2),
-           ("dense: W, 22016 x 4096", "gemv_tn_bf16_kernel<1, 8>", "235008 x 1", 22016 * 4096 * 2)]
+           ("expansion: Wf, 22016 x 1536", "gemv_rows_bf16_kernel<1, 3, 2>", "704512 x 1", 22016 * 1536 * 2),
+           ("dense: W, 22016 x 4096", "gemv_tn_bf16_kernel<1, 8>", "1409024 x 1", 22016 * 4096 * 2)]
     lines += ["", "Decode kernels at N = 1 (Llama2-7B FFN up+gate), bytes of the streamed operand over the "
               "median duration:", "", "| kernel | streamed bytes | median (us) | GB/s | HBM fraction (8 TB/s) |",
               "|---|---|---|---|---|"]
