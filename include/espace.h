@@ -61,7 +61,7 @@
 extern "C" {
 #endif
 
-#define ESPACE_ABI_VERSION 5
+#define ESPACE_ABI_VERSION 6
 
 typedef enum {
     ESPACE_F32 = 0,
@@ -270,6 +270,27 @@ size_t espace_workspace_bytes(espace_op op, int64_t M, int64_t K, int64_t L,
 const char* espace_status_string(espace_status s);
 const char* espace_last_error(void);
 int espace_abi_version(void);
+
+/* Bounded waits.  Some kernels wait for other workgroups of the same launch
+ * (the combine of two depth halves of a tile, and the one-launch projected
+ * linear layer's wait for its projection).  Every such wait gives up after a
+ * limit of polls; the waiting workgroup then writes NaN to the outputs it
+ * could not complete (the call's result shows the failure) and adds one to a
+ * per-device count.  These waits end within microseconds when the launch runs
+ * alone on the device; the limit (about seconds) only matters if workgroups
+ * of a launch are kept from running.
+ *
+ * espace_wait_timeouts: the current device's count of waits that gave up
+ * since the process loaded the library, written to *count.  It reads device
+ * memory synchronously: call it after the streams that ran the kernels have
+ * been synchronised.  ESPACE_ERR_NULL for a NULL count.
+ *
+ * espace_set_wait_limit: the number of polls after which later launches give
+ * up (process-wide; 0 restores the default).  Meant for tests of the failure
+ * path: a limit of 1 makes a workgroup that finds its partner's results not
+ * yet there give up at once. */
+espace_status espace_wait_timeouts(unsigned long long* count);
+espace_status espace_set_wait_limit(unsigned spins);
 
 #ifdef __cplusplus
 }

@@ -50,6 +50,8 @@ _SIGS = {
     "espace_status_string": ([_c_int], ctypes.c_char_p),
     "espace_last_error": ([], ctypes.c_char_p),
     "espace_abi_version": ([], _c_int),
+    "espace_wait_timeouts": ([ctypes.POINTER(ctypes.c_ulonglong)], _c_int),
+    "espace_set_wait_limit": ([ctypes.c_uint], _c_int),
 }
 
 
@@ -88,6 +90,19 @@ def _check(status):
         raise EspaceError(status, msg or lib.espace_status_string(status).decode())
 
 
+def espace_wait_timeouts():
+    """Count of bounded in-kernel waits that gave up on the current device
+    (synchronous read; synchronise the streams first)."""
+    n = ctypes.c_ulonglong(0)
+    _check(lib.espace_wait_timeouts(ctypes.byref(n)))
+    return int(n.value)
+
+
+def espace_set_wait_limit(spins):
+    """Polls after which an in-kernel wait gives up (0: the default)."""
+    _check(lib.espace_set_wait_limit(int(spins)))
+
+
 def _dt(t):
     if t.dtype == torch.bfloat16:
         return BF16
@@ -121,11 +136,25 @@ def padded_empty(rows, cols, dtype, device, align=8):
     return torch.empty((rows, ld), dtype=dtype, device=device)[:, :cols]
 
 
+def _same(first, fname, *others):
+    """Every (tensor, name) in `others` has the dtype and device of `first`: the
+    library reads and writes every operand with one element size, so a mixed
+    call would index outside the smaller buffers."""
+    for t, name in others:
+        if t is None:
+            continue
+        if t.dtype != first.dtype:
+            raise TypeError(f"{name} is {t.dtype}, {fname} is {first.dtype}: operands and outputs must share one dtype")
+        if t.device != first.device:
+            raise ValueError(f"{name} is on {t.device}, {fname} on {first.device}")
+
+
 def _out(out, rows, cols, like, name):
     if out is None:
         return padded_empty(rows, cols, like.dtype, like.device, 8 if like.dtype == torch.bfloat16 else 4)
     if tuple(out.shape) != (rows, cols):
         raise ValueError(f"{name} must be {rows}x{cols}")
+    _same(like, "the input", (out, name))
     return out
 
 
@@ -142,6 +171,10 @@ def _ws(workspace, nbytes, device):
         return None, 0
     if workspace is None:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    if workspace.device != device:
+        raise ValueError(f"workspace is on {workspace.device}, the operands on {device}")
+    if not workspace.is_contiguous():
+        raise ValueError("workspace must be contiguous")
     return workspace, workspace.numel() * workspace.element_size()
 
 
@@ -149,6 +182,7 @@ def espace_fold_weights(W, Pt, Wf=None, workspace=None):
     """Wf = W·P  (W [M][K], Pt [L][K] -> Wf [M][L])."""
     M, K = W.shape
     L = Pt.shape[0]
+    _same(W, "W", (Pt, "Pt"))
     Wf = _out(Wf, M, L, W, "Wf")
     ws, wsb = _ws(workspace, espace_workspace_bytes(OP_FOLD, M, K, L, 0, W.dtype), W.device)
     pw, ldw = _mat(W, "W")
@@ -165,6 +199,7 @@ def espace_project(Pt, X, Z=None, workspace=None):
     """Z = Pᵀ·X  (Pt [L][K], X [N][K] -> Z [N][L])."""
     L, K = Pt.shape
     N = X.shape[0]
+    _same(X, "X", (Pt, "Pt"))
     Z = _out(Z, N, L, X, "Z")
     ws, wsb = _ws(workspace, espace_workspace_bytes(OP_PROJECT, 0, K, L, N, X.dtype), X.device)
     pp, ldp = _mat(Pt, "Pt")
@@ -181,6 +216,7 @@ def espace_expand(Z, Wf, Y=None, workspace=None):
     """Y = Wf·Z  (Z [N][L], Wf [M][L] -> Y [N][M])."""
     N, L = Z.shape
     M = Wf.shape[0]
+    _same(Z, "Z", (Wf, "Wf"))
     Y = _out(Y, N, M, Z, "Y")
     ws, wsb = _ws(workspace, espace_workspace_bytes(OP_EXPAND, M, L, L, N, Z.dtype), Z.device)
     pz, ldz = _mat(Z, "Z")
@@ -198,6 +234,7 @@ def espace_projected_linear(X, Pt, Wf, Y=None, workspace=None):
     N, K = X.shape
     L = Pt.shape[0]
     M = Wf.shape[0]
+    _same(X, "X", (Pt, "Pt"), (Wf, "Wf"))
     Y = _out(Y, N, M, X, "Y")
     ws, wsb = _ws(workspace, espace_workspace_bytes(OP_PROJECTED_LINEAR, M, K, L, N, X.dtype), X.device)
     px, ldx = _mat(X, "X")
@@ -215,6 +252,7 @@ def espace_dense_linear(X, W, Y=None, workspace=None):
     """Y = W·X  (X [N][K], W [M][K] -> Y [N][M])."""
     N, K = X.shape
     M = W.shape[0]
+    _same(X, "X", (W, "W"))
     Y = _out(Y, N, M, X, "Y")
     ws, wsb = _ws(workspace, espace_workspace_bytes(OP_DENSE, M, K, 1, N, X.dtype), X.device)
     px, ldx = _mat(X, "X")
@@ -234,6 +272,8 @@ def espace_autocorrelation_update(X, C, alpha, normalize=False, workspace=None):
     N, K = X.shape
     if C.dtype != torch.float32 or tuple(C.shape) != (K, K):
         raise ValueError(f"C must be a float32 {K}x{K} tensor")
+    if C.device != X.device:
+        raise ValueError(f"C is on {C.device}, X on {X.device}")
     ws, wsb = _ws(workspace, espace_workspace_bytes(OP_AUTOCORR, 0, K, 0, N, X.dtype), X.device)
     px, ldx = _mat(X, "X")
     pc, ldc = _mat(C, "C")
@@ -253,10 +293,13 @@ def espace_symmetrized_product(A, B, C=None, workspace=None, alpha=1.0, beta=0.0
     for t, n in ((A, "A"), (B, "B")):
         if t.dtype != torch.float32 or tuple(t.shape) != (K, K):
             raise ValueError(f"{n} must be a float32 {K}x{K} tensor")
+    _same(A, "A", (B, "B"), (C, "C"))
     if C is None:
         if beta != 0.0:
             raise ValueError("beta != 0 needs C")
         C = padded_empty(K, K, torch.float32, A.device, 4)
+    elif C.dtype != torch.float32 or tuple(C.shape) != (K, K):
+        raise ValueError(f"C must be a float32 {K}x{K} tensor")
     ws, wsb = _ws(workspace, espace_workspace_bytes(OP_SYMPRODUCT, 0, K, 0, 0, torch.float32), A.device)
     pa, lda = _mat(A, "A")
     pb, ldb = _mat(B, "B")
@@ -282,6 +325,11 @@ def espace_principal_components(C, L, dtype=torch.bfloat16, Pt=None, eigenvalues
         Pt = padded_empty(L, K, dtype, C.device, 8 if dtype == torch.bfloat16 else 4)
     if tuple(Pt.shape) != (L, K):
         raise ValueError(f"Pt must be {L}x{K}")
+    if Pt.device != C.device:
+        raise ValueError(f"Pt is on {Pt.device}, C on {C.device}")
+    for t, n, dt, size in ((eigenvalues, "eigenvalues", torch.float32, K), (info, "info", torch.int32, 1)):
+        if t is not None and (t.dtype != dt or t.device != C.device or t.numel() < size or not t.is_contiguous()):
+            raise ValueError(f"{n} must be a contiguous {dt} tensor of {size} elements on {C.device}")
     if eigenvalues is None:
         eigenvalues = torch.empty(K, dtype=torch.float32, device=C.device)
     if info is None:
@@ -314,6 +362,7 @@ def espace_projected_linear_backward(dY, Z, Pt, Wf, dX=None, dW=None, want_dx=Tr
     Returns (dX, dW); either is None when not wanted."""
     N, M = dY.shape
     L, K = Pt.shape
+    _same(dY, "dY", (Z, "Z"), (Pt, "Pt"), (Wf, "Wf"))
     dX, pdx, lddx = _opt_out(dX, N, K, dY, "dX", want_dx)
     dW, pdw, lddw = _opt_out(dW, M, K, dY, "dW", want_dw)
     ws, wsb = _ws(workspace, espace_workspace_bytes(OP_BACKWARD, M, K, L, N, dY.dtype), dY.device)
@@ -334,6 +383,7 @@ def espace_dense_linear_backward(dY, X, W, dX=None, dW=None, want_dx=True, want_
     [M][K].  Returns (dX, dW); either is None when not wanted."""
     N, M = dY.shape
     K = W.shape[1]
+    _same(dY, "dY", (X, "X"), (W, "W"))
     dX, pdx, lddx = _opt_out(dX, N, K, dY, "dX", want_dx)
     dW, pdw, lddw = _opt_out(dW, M, K, dY, "dW", want_dw)
     ws, wsb = _ws(workspace, espace_workspace_bytes(OP_DENSE_BACKWARD, M, K, 1, N, dY.dtype), dY.device)

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kernels.hpp"
+
 namespace espace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -63,6 +65,15 @@ __device__ __forceinline__ u32x4_t load_chunk_clamped(const uint16_t* row, int k
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) {
     return __builtin_bit_cast(bf16x8_t, v);
+}
+
+// Bounded cross-workgroup waits (pair combine, readiness of the projection in
+// the one-launch layer): a wait gives up after `spins` polls; the workgroup
+// then writes NaN to the output it could not complete, so the failure is
+// visible in the result, and counts the event in *timeouts, a device counter
+// the host reads with espace_wait_timeouts().
+__device__ __forceinline__ void note_timeout(const WaitCfg& w) {
+    if (w.timeouts) atomicAdd(w.timeouts, 1ull);
 }
 
 // Workgroups are dispatched to the 8 XCDs of the chip round-robin by linear

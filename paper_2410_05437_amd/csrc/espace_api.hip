@@ -19,9 +19,16 @@
 
 #include "kernels.hpp"
 
+// Count of the bounded cross-workgroup waits that gave up (one per device;
+// the kernels add to it through the address hipGetSymbolAddress gives).
+__device__ unsigned long long g_wait_timeouts;
+
 namespace {
 
 using espace::GemmArgs;
+
+constexpr unsigned kDefaultWaitSpins = 1u << 22;
+std::atomic<unsigned> g_wait_spins{kDefaultWaitSpins};
 
 thread_local std::string g_last_error;
 
@@ -41,13 +48,65 @@ espace_status ok() {
 }
 
 constexpr int64_t kMaxDim = (int64_t)1 << 30;
-constexpr int kNumCUs = 256;          // MI355X; configurations are planned for it
+constexpr int kDefaultCUs = 256;      // MI355X, for queries made without a device
 constexpr size_t kWsAlign = 256;
 
 size_t elem_size(espace_dtype dt) { return dt == ESPACE_BF16 ? 2 : 4; }
 int64_t ld_align(espace_dtype dt) { return dt == ESPACE_BF16 ? 8 : 4; }
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 size_t align_ws(size_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; }
+
+// Compute units of the current device (read once per device); configurations
+// are planned for this count.  Without a usable device (a workspace query on a
+// host with no GPU) the full MI355X count.
+int device_cus() {
+    static std::mutex mu;
+    static int cus[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+        (void)hipGetLastError();
+        return kDefaultCUs;
+    }
+    std::lock_guard<std::mutex> lk(mu);
+    if (cus[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1) {
+            (void)hipGetLastError();
+            n = kDefaultCUs;
+        }
+        cus[dev] = n;
+    }
+    return cus[dev];
+}
+
+// Device address of this device's g_wait_timeouts (looked up once per device;
+// the array's name is a host-side stand-in and must not reach a kernel).
+unsigned long long* timeout_counter() {
+    static std::mutex mu;
+    static unsigned long long* ptr[64] = {nullptr};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lk(mu);
+    if (!ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(g_wait_timeouts)) != hipSuccess) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        ptr[dev] = static_cast<unsigned long long*>(p);
+    }
+    return ptr[dev];
+}
+
+espace::WaitCfg wait_cfg() {
+    espace::WaitCfg w;
+    w.spins = g_wait_spins.load(std::memory_order_relaxed);
+    w.timeouts = timeout_counter();
+    return w;
+}
 
 // ---- planning ---------------------------------------------------------------
 
@@ -63,7 +122,7 @@ struct Plan {
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
-Plan plan_skinny(int R, int Cc, int D) {
+Plan plan_skinny(int R, int Cc, int D, int cus) {
     // Measured on the decode layers (N <= 32): a launch costs a few µs
     // whatever its size, so the depth is split only when the tokens make
     // each workgroup's loads heavy or the depth is very large; 8 waves with
@@ -79,11 +138,11 @@ Plan plan_skinny(int R, int Cc, int D) {
     p.kind = KIND_SKINNY;
     const int nb1 = ceil_div(Cc, 16);
     const int steps = ceil_div(D, 32);
-    const int target = 2 * kNumCUs;
+    const int target = 2 * cus;
     if (nb1 >= target) {
         if (R > 8) p.tile = espace::SKINNY_RG2_W4;
         else p.tile = (steps <= 48) ? espace::SKINNY_RG1_W8_U6 : espace::SKINNY_RG1_W8_U8;
-    } else if (R <= 8 && nb1 < kNumCUs / 2 && steps <= 384) {
+    } else if (R <= 8 && nb1 < cus / 2 && steps <= 384) {
         p.tile = steps <= 128 ? espace::SKINNY_SEG2_W8_U8 : espace::SKINNY_SEG2_W16_U4;
     } else {
         p.tile = espace::SKINNY_RG1_W8_U8;
@@ -125,7 +184,7 @@ void set_partial_bytes(Plan& p, int64_t R, int64_t Cc) {
     }
 }
 
-Plan plan_tiled(int R, int Cc, int D) {
+Plan plan_tiled(int R, int Cc, int D, int cus) {
     // Estimated time of each tile shape (and depth split) from the number of
     // rounds of workgroups the chip needs, the per-tile work and a relative
     // efficiency of the tile shape; the cheapest wins.  Two depth halves can
@@ -140,13 +199,13 @@ Plan plan_tiled(int R, int Cc, int D) {
         {espace::TILE_128x192, 128, 192, 1, 0.70},
     };
     const int ktiles = ceil_div(D, 64);
-    const double byte_cost = 315.0 / (2.0 * 64 * kNumCUs);   // bytes priced against the MFMA rate
+    const double byte_cost = 315.0 / (2.0 * 64 * cus);   // bytes priced against the MFMA rate
     Plan best;
     best.kind = KIND_TILED;
     double best_cost = 1e300;
     for (const TileShape& s : shapes) {
         const int64_t tiles = (int64_t)ceil_div(R, s.bm) * ceil_div(Cc, s.bn);
-        const int64_t slots = (int64_t)kNumCUs * s.per_cu;
+        const int64_t slots = (int64_t)cus * s.per_cu;
         for (int splits = 1; splits <= 4; ++splits) {
             if (splits > 1 && ktiles / splits < 8) break;
             for (int pair = 0; pair <= (splits == 2 ? 1 : 0); ++pair) {
@@ -172,55 +231,6 @@ Plan plan_tiled(int R, int Cc, int D) {
     return best;
 }
 
-// Tuning overrides, read once per process: ESPACE_TILE=<shape name> and
-// ESPACE_SPLITK=<n> force the tiled configuration, ESPACE_PAIR=0|1 turns the
-// in-kernel combine of two depth halves off or on, ESPACE_TUNE_SHAPE=R,Cc,D
-// restricts those three (and ESPACE_SKINNY) to products of that shape;
-// ESPACE_KERNEL=1|2|3
-// selects the register-staged, the eight-wave direct-to-LDS or the ping-pong
-// kernel for every tiled product (default 4: the hand-ordered four-wave
-// kernel for 256 x 256 and 256 x 192 tiles, the direct-to-LDS kernel for the
-// others),
-// ESPACE_VARIANT=<n> a kernel variant, ESPACE_SKINNY=<kind> the small-N kernel,
-// ESPACE_GEMV=0 the MFMA kernel instead of whole-row streaming for 1-2 tokens.
-struct Override {
-    int tile = -1, splits = 0, kernel = 4, variant = 3, skinny = -1, pair = -1, gemv = -1;
-    long long shape[3] = {-1, -1, -1};
-    bool applies(int64_t R, int64_t Cc, int64_t D) const {
-        return shape[0] < 0 || (shape[0] == R && shape[1] == Cc && shape[2] == D);
-    }
-};
-
-const Override& tile_override() {
-    static const Override o = [] {
-        Override r;
-        if (const char* t = std::getenv("ESPACE_TILE")) {
-            if (!std::strcmp(t, "256x256")) r.tile = espace::TILE_256x256;
-            else if (!std::strcmp(t, "256x128")) r.tile = espace::TILE_256x128;
-            else if (!std::strcmp(t, "128x256")) r.tile = espace::TILE_128x256;
-            else if (!std::strcmp(t, "128x128")) r.tile = espace::TILE_128x128;
-            else if (!std::strcmp(t, "256x256w8")) r.tile = espace::TILE_256x256_W8;
-            else if (!std::strcmp(t, "256x256w8t")) r.tile = espace::TILE_256x256_W8T;
-            else if (!std::strcmp(t, "128x192")) r.tile = espace::TILE_128x192;
-            else if (!std::strcmp(t, "256x192w8")) r.tile = espace::TILE_256x192_W8;
-        }
-        if (const char* s = std::getenv("ESPACE_SPLITK")) r.splits = std::atoi(s);
-        if (const char* s = std::getenv("ESPACE_PAIR")) r.pair = std::atoi(s) ? 1 : 0;
-        if (const char* s = std::getenv("ESPACE_TUNE_SHAPE"))
-            if (std::sscanf(s, "%lld,%lld,%lld", &r.shape[0], &r.shape[1], &r.shape[2]) != 3)
-                r.shape[0] = -1;
-        if (const char* s = std::getenv("ESPACE_GEMV")) r.gemv = std::atoi(s) ? 1 : 0;
-        if (const char* s = std::getenv("ESPACE_KERNEL")) r.kernel = std::atoi(s);
-        if (const char* s = std::getenv("ESPACE_VARIANT")) r.variant = std::atoi(s);
-        if (const char* s = std::getenv("ESPACE_SKINNY")) {
-            const int v = std::atoi(s);
-            if (v >= espace::SKINNY_RG1_W4 && v <= espace::SKINNY_SEG2_W16_U4) r.skinny = v;
-        }
-        return r;
-    }();
-    return o;
-}
-
 Plan plan_tn(int64_t R, int64_t Cc, int64_t D, espace_dtype dt) {
     if (dt == ESPACE_F32) return Plan{};
     if (R <= 32) {
@@ -229,42 +239,15 @@ Plan plan_tn(int64_t R, int64_t Cc, int64_t D, espace_dtype dt) {
         // faster than the MFMA kernel, e.g. the Llama2-7B up+gate expansion
         // 15.5 -> 14.2 µs, its dense W 38.1 -> 33.6 µs, the GPT3-22B
         // expansion at L = 2458 31.1 -> 24.4 µs; at N = 2 faster or within
-        // 0.5 µs; slower from 3 tokens on).  ESPACE_GEMV=0 turns it off.
-        const Override& o = tile_override();
-        const bool skinny_forced = o.skinny >= 0 && o.applies(R, Cc, D);
-        if (o.gemv != 0 && !skinny_forced && espace::gemv_supported((int)R, (int)D)) {
+        // 0.5 µs; slower from 3 tokens on).
+        if (espace::gemv_supported((int)R, (int)D)) {
             Plan g;
             g.kind = KIND_GEMV;
             return g;
         }
-        Plan p = plan_skinny((int)R, (int)Cc, (int)D);
-        if (!o.applies(R, Cc, D)) return p;
-        if (o.skinny >= 0) p.tile = o.skinny;
-        if (p.tile >= espace::SKINNY_SEG2_W8_U8) {   // segmented kernels take one depth range
-            p.splits = 1;
-            p.partial_bytes = 0;
-            return p;
-        }
-        if (o.splits > 0) {
-            p.splits = o.splits < ceil_div(D, 32) ? o.splits : (int)ceil_div(D, 32);
-            p.partial_bytes = p.splits > 1 ? (size_t)p.splits * R * espace::splitk_ld(Cc) * sizeof(float) : 0;
-        }
-        return p;
+        return plan_skinny((int)R, (int)Cc, (int)D, device_cus());
     }
-    Plan p = plan_tiled((int)R, (int)Cc, (int)D);
-    const Override& o = tile_override();
-    if ((o.tile >= 0 || o.splits > 0 || o.pair >= 0) && o.applies(R, Cc, D)) {
-        if (o.tile >= 0) p.tile = o.tile;
-        if (o.splits > 0) {
-            p.splits = o.splits;
-            p.pair = 0;
-        }
-        if (p.splits > ceil_div(D, 64)) p.splits = ceil_div(D, 64);
-        if (o.pair >= 0) p.pair = (o.pair == 1 && p.splits == 2) ? 1 : 0;
-        if (p.splits != 2) p.pair = 0;
-        set_partial_bytes(p, R, Cc);
-    }
-    return p;
+    return plan_tiled((int)R, (int)Cc, (int)D, device_cus());
 }
 
 // ESPACE_PLAN_LOG=1 prints each product's plan to stderr (read once per process).
@@ -290,38 +273,6 @@ int64_t z_ld(int64_t L, int64_t N, espace_dtype dt) {
     if (dt != ESPACE_BF16) return round_up(L, 32);
     return round_up(L, 64) + (N <= 32 ? 32 : 0);
 }
-
-// One-launch decode path (bf16, N <= 32).  It is selected per call with
-// ESPACE_DECODE=fused; by default the two-launch path runs, which is faster
-// on this device today (the fused path spends its time on cross-workgroup
-// hand-offs; see decode_fused.hip).
-bool use_fused_decode(int64_t N, int64_t L, espace_dtype dt) {
-    const char* s = std::getenv("ESPACE_DECODE");
-    const bool enabled = s && !std::strcmp(s, "fused");
-    return enabled && dt == ESPACE_BF16 && N >= 1 && N <= 32 && espace::decode_fused_supported((int)N, (int)L);
-}
-
-int64_t part_ld(int64_t L) { return round_up(L, 4); }
-
-struct FusedPlan { int S1 = 1, steps1 = 0, P1 = 0, P2 = 0; };
-
-FusedPlan fused_plan(int64_t N, int64_t K, int64_t L, int64_t M) {
-    FusedPlan p;
-    espace::decode_fused_plan((int)N, (int)K, (int)L, (int)M, kNumCUs, &p.S1, &p.steps1, &p.P1, &p.P2);
-    return p;
-}
-
-size_t fused_partial_bytes(int64_t N, int64_t K, int64_t L, int64_t M, espace_dtype dt) {
-    if (!use_fused_decode(N, L, dt)) return 0;
-    const FusedPlan p = fused_plan(N, K, L, M);
-    return p.S1 > 1 ? (size_t)p.S1 * N * part_ld(L) * sizeof(float) : 0;
-}
-
-// The counter block of the one-launch path sits at the end of the workspace.
-size_t fused_sync_bytes(int64_t N, int64_t L, espace_dtype dt) {
-    return use_fused_decode(N, L, dt) ? espace::decode_fused_sync_bytes((int)L) : 0;
-}
-
 
 size_t z_bytes(int64_t N, int64_t L, espace_dtype dt) {
     return align_ws((size_t)N * z_ld(L, N, dt) * elem_size(dt));
@@ -382,12 +333,9 @@ size_t ws_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int64_t N, espace
         case ESPACE_OP_DENSE_BACKWARD: return (N && M) ? dense_bwd_layout(M, K, N, dt).total : 0;
         case ESPACE_OP_PROJECTED_LINEAR: {
             if (!N || !M) return 0;
-            size_t a = plan_tn(N, L, K, dt).partial_bytes;
-            size_t b = plan_tn(N, M, L, dt).partial_bytes;
-            const size_t c = fused_partial_bytes(N, K, L, M, dt);
-            size_t m = a > b ? a : b;
-            m = m > c ? m : c;
-            return z_bytes(N, L, dt) + align_ws(m) + fused_sync_bytes(N, L, dt);
+            const size_t a = plan_tn(N, L, K, dt).partial_bytes;
+            const size_t b = plan_tn(N, M, L, dt).partial_bytes;
+            return z_bytes(N, L, dt) + align_ws(a > b ? a : b);
         }
     }
     return SIZE_MAX;
@@ -510,22 +458,21 @@ espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, voi
         g.tile = p.tile;
         g.splits = p.splits;
         g.partial = (float*)partial;
-        g.variant = tile_override().variant;
         g.pair = p.pair;
+        g.cus = device_cus();
+        g.wait = wait_cfg();
         if (p.pair) g.epoch = next_epoch();
-        const int kern = tile_override().kernel;
         if (p.kind == KIND_SKINNY) {
             e = espace::launch_skinny_tn_bf16(g, stream);
         } else if (p.kind == KIND_GEMV) {
             e = espace::launch_gemv_tn_bf16(g, stream);
-        } else if (kern == 4 && (p.tile == espace::TILE_256x256_W8T || p.tile == espace::TILE_256x256 ||
-                                 p.tile == espace::TILE_256x192_W8)) {
+        } else if (p.tile == espace::TILE_256x256_W8T || p.tile == espace::TILE_256x192_W8) {
+            // the four-wave kernel; matrices of 2^31 elements or more take the
+            // register-staged kernel with 64-bit offsets
             e = espace::launch_gemm_tn_bf16_v3(g, stream);
-            if (e == hipErrorInvalidValue) e = espace::launch_gemm_tn_bf16_v2(g, stream);
+            if (e == hipErrorInvalidValue) e = espace::launch_gemm_tn_bf16(g, stream);
         } else {
-            e = kern == 1 ? espace::launch_gemm_tn_bf16(g, stream)
-                : kern == 3 ? espace::launch_gemm_tn_bf16_pp(g, stream)
-                            : espace::launch_gemm_tn_bf16_v2(g, stream);
+            e = espace::launch_gemm_tn_bf16_v2(g, stream);
         }
     }
     if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
@@ -537,6 +484,21 @@ espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, voi
 extern "C" {
 
 int espace_abi_version(void) { return ESPACE_ABI_VERSION; }
+
+espace_status espace_set_wait_limit(unsigned spins) {
+    g_wait_spins.store(spins ? spins : kDefaultWaitSpins, std::memory_order_relaxed);
+    return ok();
+}
+
+espace_status espace_wait_timeouts(unsigned long long* count) {
+    if (!count) return fail(ESPACE_ERR_NULL, "count is NULL");
+    ESPACE_TRY(check_device());
+    unsigned long long* p = timeout_counter();
+    if (!p) return fail(ESPACE_ERR_HIP, "device counter not available");
+    const hipError_t e = hipMemcpy(count, p, sizeof *count, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "reading the counter: %s", hipGetErrorString(e));
+    return ok();
+}
 
 const char* espace_last_error(void) { return g_last_error.c_str(); }
 
@@ -667,22 +629,6 @@ espace_status espace_projected_linear(const void* X, int64_t ldx, const void* Pt
     const int64_t ldz = z_ld(L, N, dt);
     void* Z = workspace;
     void* partial = (char*)workspace + z_bytes(N, L, dt);
-    if (use_fused_decode(N, L, dt)) {
-        const FusedPlan p = fused_plan(N, K, L, M);
-        espace::DecodeArgs a;
-        a.X = (const uint16_t*)X; a.ldx = ldx;
-        a.Pt = (const uint16_t*)Pt; a.ldp = ldp;
-        a.Wf = (const uint16_t*)Wf; a.ldwf = ldwf;
-        a.Y = (uint16_t*)Y; a.ldy = ldy;
-        a.Z = (uint16_t*)Z; a.ldz = ldz;
-        a.part = (float*)partial; a.ldpart = part_ld(L);
-        a.sync = (unsigned long long*)((char*)workspace + need - fused_sync_bytes(N, L, dt));
-        a.epoch = next_epoch();
-        a.N = (int)N; a.K = (int)K; a.L = (int)L; a.M = (int)M;
-        a.S1 = p.S1; a.steps1 = p.steps1; a.P1 = p.P1; a.P2 = p.P2;
-        if (espace::launch_decode_fused(a, stream) == hipSuccess) return ok();
-        (void)hipGetLastError();   // not launched: take the two-launch path
-    }
     ESPACE_TRY(run_tn(X, ldx, Pt, ldp, Z, ldz, N, L, K, dt, partial, stream));
     ESPACE_TRY(run_tn(Z, ldz, Wf, ldwf, Y, ldy, N, M, L, dt, partial, stream));
     return ok();

@@ -192,27 +192,31 @@ enum { MODE_BF16 = 0, MODE_F32 = 1, MODE_PAIR = 2 };
 // 4q+2, 4q+3): these writes go through to memory, where partial cache lines
 // cost a read-modify-write.
 // Returns true on the workgroup that writes the output.
+enum { PAIR_FIRST = 0, PAIR_SECOND = 1, PAIR_SECOND_TIMED_OUT = 2 };
+
 template <class T, class Acc>
-__device__ bool pair_combine(Acc (&acc)[T::TM][T::TN], unsigned long long* state, float* part,
-                             unsigned long long epoch, int* role, int wave, int lane) {
+__device__ int pair_combine(Acc (&acc)[T::TM][T::TN], unsigned long long* state, float* part,
+                            unsigned long long epoch, int* role, int wave, int lane, const WaitCfg& wc) {
     const unsigned long long tag = (epoch & 0xFFFFFFFFFFFFull) << 16;
     if (threadIdx.x == 0) {
         unsigned long long old = __hip_atomic_load(state, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        int second = 0;
-        for (int it = 0; it < (1 << 20); ++it) {
+        int r = PAIR_SECOND_TIMED_OUT;
+        for (unsigned it = 0; it < wc.spins; ++it) {
             const unsigned long long st = old & 0xFFFFull;
             if ((old & ~0xFFFFull) == tag && (st == 1 || st == 2)) {
-                second = 1;
+                r = PAIR_SECOND;
                 break;
             }
             if (__hip_atomic_compare_exchange_strong(state, &old, tag | 1ull, __ATOMIC_RELAXED,
-                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                r = PAIR_FIRST;
                 break;
+            }
         }
-        *role = second;
+        *role = r;
     }
     __syncthreads();
-    const bool second = *role != 0;
+    const bool second = *role != PAIR_FIRST;
     // this wave's region: [wave][i][j][q][half][lane] of 8 bytes
     unsigned long long* base =
         reinterpret_cast<unsigned long long*>(part) + (size_t)wave * T::TM * T::TN * T::ACC * 64 / 2;
@@ -236,15 +240,31 @@ __device__ bool pair_combine(Acc (&acc)[T::TM][T::TN], unsigned long long* state
         __builtin_amdgcn_s_waitcnt(0);           // this wave's stores are complete
         __syncthreads();
         if (threadIdx.x == 0) __hip_atomic_store(state, tag | 2ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return false;
+        return PAIR_FIRST;
     }
-    if (threadIdx.x == 0) {
-        for (int it = 0; it < (1 << 24); ++it) {
-            if (__hip_atomic_load(state, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (tag | 2ull)) break;
+    if (threadIdx.x == 0 && *role == PAIR_SECOND) {
+        int r = PAIR_SECOND_TIMED_OUT;
+        for (unsigned it = 0; it < wc.spins; ++it) {
+            if (__hip_atomic_load(state, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (tag | 2ull)) {
+                r = PAIR_SECOND;
+                break;
+            }
             __builtin_amdgcn_s_sleep(2);
         }
+        *role = r;
     }
+    if (threadIdx.x == 0 && *role == PAIR_SECOND_TIMED_OUT) note_timeout(wc);
     __syncthreads();
+    if (*role == PAIR_SECOND_TIMED_OUT) {
+        // the partner's sums never arrived: the tile is written as NaN
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+            for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+                for (int e = 0; e < T::ACC; ++e) acc[i][j][e] = __builtin_nanf("");
+        return PAIR_SECOND_TIMED_OUT;
+    }
 #pragma unroll
     for (int i = 0; i < T::TM; ++i)
 #pragma unroll
@@ -262,7 +282,7 @@ __device__ bool pair_combine(Acc (&acc)[T::TM][T::TN], unsigned long long* state
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (threadIdx.x == 0) __hip_atomic_store(state, tag | 3ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return true;
+    return PAIR_SECOND;
 }
 
 // Matrices handed to this kernel hold fewer than 2^31 elements, so per-lane
@@ -274,7 +294,7 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
                             void* __restrict__ Cout, int64_t ldc,
                             int R, int Cc, int D, int tiles_c, int ktiles_per_split,
                             int64_t split_stride, int map, unsigned long long* tile_state,
-                            float* pair_part, unsigned long long epoch) {
+                            float* pair_part, unsigned long long epoch, WaitCfg wc) {
     using T = Cfg<BM, BN, WM, WN, BK, STAGES, MI>;
     using Acc = typename AccOf<MI>::type;
     __shared__ __attribute__((aligned(1024))) unsigned char smem[T::SMEM];
@@ -377,8 +397,8 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
 
     if constexpr (MODE == MODE_PAIR) {
         const int tile = tile_r * tiles_c + tile_c;
-        if (!pair_combine<T, Acc>(acc, tile_state + tile, pair_part + (size_t)tile * (BM * BN), epoch,
-                             reinterpret_cast<int*>(smem), wave, lane))
+        if (pair_combine<T, Acc>(acc, tile_state + tile, pair_part + (size_t)tile * (BM * BN), epoch,
+                                 reinterpret_cast<int*>(smem), wave, lane, wc) == PAIR_FIRST)
             return;
     }
 
@@ -465,7 +485,7 @@ hipError_t launch_v2(const GemmArgs& g, hipStream_t stream) {
     if (S == 1) {
         hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_BF16, MI>), grid, block,
                            0, stream, g.A, g.lda, g.B, g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c,
-                           ktps, (int64_t)0, g.variant >> 2, nullptr, nullptr, 0ull);
+                           ktps, (int64_t)0, 0, nullptr, nullptr, 0ull, g.wait);
         return hipGetLastError();
     }
     if (S == 2 && g.pair) {
@@ -476,14 +496,14 @@ hipError_t launch_v2(const GemmArgs& g, hipStream_t stream) {
             reinterpret_cast<unsigned long long*>(g.partial + (size_t)ntiles * BM * BN);
         hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_PAIR, MI>), grid, block,
                            0, stream, g.A, g.lda, g.B, g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c,
-                           ktps, (int64_t)0, g.variant >> 2, state, g.partial, g.epoch);
+                           ktps, (int64_t)0, 0, state, g.partial, g.epoch, g.wait);
         return hipGetLastError();
     }
     const int64_t ldp = splitk_ld(g.Cc);
     const int64_t split_stride = (int64_t)g.R * ldp;
     hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_F32, MI>), grid, block, 0,
                        stream, g.A, g.lda, g.B, g.ldb, (void*)g.partial, ldp, g.R, g.Cc, g.D,
-                       tiles_c, ktps, split_stride, g.variant >> 2, nullptr, nullptr, 0ull);
+                       tiles_c, ktps, split_stride, 0, nullptr, nullptr, 0ull, g.wait);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_splitk_reduce(g.partial, S, split_stride, ldp, g.C, g.ldc, g.R, g.Cc,
@@ -503,47 +523,18 @@ void tile_dims(int tile, int* bm, int* bn) {
     }
 }
 
-// variant bit 0 clear: depth step 32 with 4 LDS stages; set: depth step 64
-// with 2.  Bit 1 (with bit 0): 16x16x32 MFMA blocks for the eight-wave
-// tiles.  Bits 2-3: tile order (tile_coords).
+// The four-wave tiles other than the hand-ordered kernel's: depth step 64 in
+// two LDS stages, 32 x 32 x 16 MFMA blocks.  Matrices of 2^31 elements or more
+// take the register-staged kernel (64-bit offsets).
 hipError_t launch_gemm_tn_bf16_v2(const GemmArgs& g, hipStream_t stream) {
     const int64_t lim = (int64_t)1 << 31;
     if ((int64_t)g.R * g.lda >= lim || (int64_t)g.Cc * g.ldb >= lim || g.c_f32)
         return launch_gemm_tn_bf16(g, stream);   // runs a pair plan as one depth range
-    const bool deep = (g.variant & 1) == 0;
-    if (!deep && (g.variant & 2)) {
-        // 16x16x32 blocks: measured faster for the eight-wave tiles (5-6% on
-        // 4096 x 12288 x 1536), slower for the four-wave ones
-        switch (g.tile) {
-            case TILE_256x256_W8T: return launch_v2<256, 256, 4, 2, 64, 2, 16>(g, stream);
-            case TILE_256x192_W8: return launch_v2<256, 192, 4, 2, 64, 2, 16>(g, stream);
-            default: break;
-        }
-    }
     switch (g.tile) {
-        case TILE_256x256:
-            return deep ? launch_v2<256, 256, 2, 2, 32, 4>(g, stream)
-                        : launch_v2<256, 256, 2, 2, 64, 2>(g, stream);
-        case TILE_256x128:
-            return deep ? launch_v2<256, 128, 2, 2, 32, 4>(g, stream)
-                        : launch_v2<256, 128, 2, 2, 64, 2>(g, stream);
-        case TILE_128x256:
-            return deep ? launch_v2<128, 256, 2, 2, 32, 4>(g, stream)
-                        : launch_v2<128, 256, 2, 2, 64, 2>(g, stream);
-        case TILE_256x256_W8:
-            return deep ? launch_v2<256, 256, 2, 4, 32, 4>(g, stream)
-                        : launch_v2<256, 256, 2, 4, 64, 2>(g, stream);
-        case TILE_256x256_W8T:
-            return deep ? launch_v2<256, 256, 4, 2, 32, 4>(g, stream)
-                        : launch_v2<256, 256, 4, 2, 64, 2>(g, stream);
-        case TILE_128x128:
-            return deep ? launch_v2<128, 128, 2, 2, 32, 4>(g, stream)
-                        : launch_v2<128, 128, 2, 2, 64, 2>(g, stream);
-        case TILE_128x192:
-            return deep ? launch_v2<128, 192, 2, 2, 32, 4>(g, stream)
-                        : launch_v2<128, 192, 2, 2, 64, 2>(g, stream);
-        case TILE_256x192_W8:   // depth step 64 only (448 rows of 32 deep do not split over 8 waves)
-            return launch_v2<256, 192, 4, 2, 64, 2>(g, stream);
+        case TILE_256x128: return launch_v2<256, 128, 2, 2, 64, 2>(g, stream);
+        case TILE_128x256: return launch_v2<128, 256, 2, 2, 64, 2>(g, stream);
+        case TILE_128x128: return launch_v2<128, 128, 2, 2, 64, 2>(g, stream);
+        case TILE_128x192: return launch_v2<128, 192, 2, 2, 64, 2>(g, stream);
         default: return hipErrorInvalidValue;
     }
 }

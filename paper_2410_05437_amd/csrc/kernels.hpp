@@ -32,6 +32,13 @@ enum TileKind {
     SKINNY_SEG2_W16_U4 = 23,
 };
 
+// Limit of the bounded cross-workgroup waits and the device counter of the
+// waits that gave up (see note_timeout).
+struct WaitCfg {
+    unsigned spins = 1u << 22;
+    unsigned long long* timeouts = nullptr;
+};
+
 // One "TN" product C[r][c] = sum_k A[r][k] * B[c][k]  (bf16 in, fp32 accumulate).
 struct GemmArgs {
     const uint16_t* A;
@@ -48,7 +55,8 @@ struct GemmArgs {
     int splits;         // depth ranges; > 1 needs `partial`
     float* partial;     // splits * R * splitk_ld(Cc) fp32 (workspace); with `pair`:
                         // tiles * tile area fp32, then one 8-byte state word per tile
-    int variant = 0;    // kernel variant (tuning)
+    int cus = 256;      // compute units of the device (persistent grids)
+    WaitCfg wait;       // bounded waits of the pair combine
     int pair = 0;       // splits == 2 combined inside the kernel (no reduce pass)
     unsigned long long epoch = 0;   // per-call tag of the pair state words
 };
@@ -61,7 +69,6 @@ inline int64_t splitk_ld(int Cc) { return (Cc + 7) / 8 * 8; }
 
 hipError_t launch_gemm_tn_bf16(const GemmArgs& g, hipStream_t stream);
 hipError_t launch_gemm_tn_bf16_v2(const GemmArgs& g, hipStream_t stream);
-hipError_t launch_gemm_tn_bf16_pp(const GemmArgs& g, hipStream_t stream);
 // Four-wave 256 x 256 and 256 x 192 kernel with a hand-ordered main loop;
 // hipErrorInvalidValue for products it does not take (other tiles, fp32
 // output, >= 2^31 elements).
@@ -74,26 +81,6 @@ hipError_t launch_gemv_tn_bf16(const GemmArgs& g, hipStream_t stream);
 hipError_t launch_splitk_reduce(const float* P, int S, int64_t split_stride, int64_t ldp,
                                 void* C, int64_t ldc, int R, int Cc, int out_bf16,
                                 hipStream_t stream);
-// One-launch projected linear layer for N <= 32 tokens (bf16).
-struct DecodeArgs {
-    const uint16_t* X;  int64_t ldx;    // [N][K]
-    const uint16_t* Pt; int64_t ldp;    // [L][K]
-    const uint16_t* Wf; int64_t ldwf;   // [M][L]
-    uint16_t* Y;        int64_t ldy;    // [N][M]
-    uint16_t* Z;        int64_t ldz;    // workspace [N][ldz], ldz >= round_up(L, 16)
-    float* part;        int64_t ldpart; // workspace [S1][N][ldpart] (S1 > 1), ldpart = round_up(L, 4)
-    unsigned long long* sync;           // workspace: counter block (decode_fused_sync_bytes)
-    unsigned long long epoch;           // per-call tag of the counter block
-    int N, K, L, M;
-    int S1, steps1;                     // depth splits of the projection
-    int P1, P2;                         // projection units, phase-2 workgroups
-};
-
-bool decode_fused_supported(int N, int L);
-size_t decode_fused_sync_bytes(int L);
-void decode_fused_plan(int N, int K, int L, int M, int cus, int* S1, int* steps1, int* P1, int* P2);
-hipError_t launch_decode_fused(const DecodeArgs& a, hipStream_t stream);
-
 hipError_t launch_gemm_tn_f32(const float* A, int64_t lda, const float* B, int64_t ldb,
                               float* C, int64_t ldc, int R, int Cc, int D, hipStream_t stream);
 

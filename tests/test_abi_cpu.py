@@ -21,10 +21,10 @@ def test_exports_every_declared_function():
         "espace_dense_linear", "espace_workspace_bytes", "espace_status_string",
         "espace_last_error", "espace_abi_version", "espace_autocorrelation_update",
         "espace_principal_components", "espace_symmetrized_product", "espace_projected_linear_backward",
-        "espace_dense_linear_backward"}
+        "espace_dense_linear_backward", "espace_wait_timeouts", "espace_set_wait_limit"}
     for n in names:
         assert hasattr(L, n)
-    assert E.ABI_VERSION == 5
+    assert E.ABI_VERSION == 6
 
 
 def _fold(W=P16, ldw=64, Pt=P16b, ldp=64, Wf=P16c, ldwf=16, M=32, K=64, Lc=16, dt=1,
@@ -191,3 +191,43 @@ def test_backward_validation():
     assert ws(8, 12288, 4096, 1536, 4096, 1) > 0
     assert ws(8, 12288, 4096, 5000, 4096, 1) == ctypes.c_size_t(-1).value
     assert ws(9, 12288, 4096, 0, 4096, 1) >= 4096 * 12288 * 2
+
+
+def test_binding_rejects_mixed_operand_types():
+    """The binding checks, before any library call, that every operand, output
+    and workspace has the first operand's dtype and device: the library uses
+    one element size for all of them, so a float32 input with a bfloat16
+    output (or the reverse) would read or write past the smaller buffer."""
+    import torch
+    f32, bf = torch.float32, torch.bfloat16
+    X = torch.zeros(8, 64, dtype=f32)
+    Pt = torch.zeros(16, 64, dtype=f32)
+    Wf = torch.zeros(32, 16, dtype=f32)
+    W = torch.zeros(32, 64, dtype=f32)
+    with pytest.raises(TypeError, match="Y"):
+        E.espace_projected_linear(X, Pt, Wf, Y=torch.zeros(8, 32, dtype=bf))
+    with pytest.raises(TypeError, match="Pt"):
+        E.espace_projected_linear(X, Pt.to(bf), Wf)
+    with pytest.raises(TypeError, match="Wf"):
+        E.espace_projected_linear(X, Pt, Wf.to(bf))
+    with pytest.raises(TypeError, match="Pt"):
+        E.espace_fold_weights(W, Pt.to(bf))
+    with pytest.raises(TypeError, match="Wf"):
+        E.espace_fold_weights(W, Pt, Wf=torch.zeros(32, 16, dtype=bf))
+    with pytest.raises(TypeError, match="Pt"):
+        E.espace_project(Pt.to(bf), X)
+    with pytest.raises(TypeError, match="Z"):
+        E.espace_project(Pt, X, Z=torch.zeros(8, 16, dtype=bf))
+    with pytest.raises(TypeError, match="Wf"):
+        E.espace_expand(torch.zeros(8, 16, dtype=f32), Wf.to(bf))
+    with pytest.raises(TypeError, match="W"):
+        E.espace_dense_linear(X, W.to(bf))
+    with pytest.raises(TypeError, match="Y"):
+        E.espace_dense_linear(X, W, Y=torch.zeros(8, 32, dtype=bf))
+    with pytest.raises(TypeError, match="Wf"):
+        E.espace_projected_linear_backward(torch.zeros(8, 32, dtype=f32), torch.zeros(8, 16, dtype=f32), Pt,
+                                           Wf.to(bf))
+    with pytest.raises(TypeError, match="X"):
+        E.espace_dense_linear_backward(torch.zeros(8, 32, dtype=f32), X.to(bf), W)
+    with pytest.raises(ValueError, match="B"):
+        E.espace_symmetrized_product(torch.zeros(4, 4), torch.zeros(4, 4, dtype=bf))
