@@ -271,6 +271,30 @@ const char* espace_status_string(espace_status s);
 const char* espace_last_error(void);
 int espace_abi_version(void);
 
+/* Allocation-free variant of espace_projected_linear, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, computation and results
+ * as espace_projected_linear without the workspace: Z and the partial sums
+ * live in a static device array of ESPACE_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every device it runs on until the process ends.  Calls
+ * neither hipMalloc, hipFree nor any allocating library routine (the first
+ * call on a device looks up that device's copy of the array).
+ *  - Sizes whose workspace (espace_workspace_bytes(ESPACE_OP_PROJECTED_LINEAR,
+ *    ...)) exceeds ESPACE_NOALLOC_SCRATCH_BYTES return ESPACE_ERR_WORKSPACE
+ *    and enqueue nothing.
+ *  - All calls on one device share the array: calls that can overlap on one
+ *    device (other streams, other threads, other processes are not affected)
+ *    race and must be serialised by the caller.  Nothing in it needs to start
+ *    at zero (its state words carry a per-call tag). */
+#define ESPACE_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+espace_status espace_projected_linear_noalloc(const void* X, int64_t ldx,
+                                              const void* Pt, int64_t ldp,
+                                              const void* Wf, int64_t ldwf,
+                                              void* Y, int64_t ldy,
+                                              int64_t M, int64_t K, int64_t L, int64_t N,
+                                              espace_dtype dt, hipStream_t stream);
+
 /* Bounded waits.  Some kernels wait for other workgroups of the same launch
  * (the combine of two depth halves of a tile, and the one-launch projected
  * linear layer's wait for its projection).  Every such wait gives up after a

@@ -29,6 +29,7 @@ from ._lib import (  # noqa: F401
     espace_project,
     espace_projected_linear,
     espace_projected_linear_backward,
+    espace_projected_linear_noalloc,
     espace_set_wait_limit,
     espace_symmetrized_product,
     espace_wait_timeouts,

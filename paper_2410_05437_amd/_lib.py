@@ -36,6 +36,8 @@ _SIGS = {
                        _c_int, _c_p, _c_sz, _c_p], _c_int),
     "espace_projected_linear": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64,
                                  _c_i64, _c_i64, _c_i64, _c_i64, _c_int, _c_p, _c_sz, _c_p], _c_int),
+    "espace_projected_linear_noalloc": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64,
+                                         _c_i64, _c_i64, _c_i64, _c_i64, _c_int, _c_p], _c_int),
     "espace_dense_linear": ([_c_p, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_i64, _c_i64,
                              _c_int, _c_p, _c_sz, _c_p], _c_int),
     "espace_autocorrelation_update": ([_c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_i64, _c_int, ctypes.c_float,
@@ -245,6 +247,24 @@ def espace_projected_linear(X, Pt, Wf, Y=None, workspace=None):
         _check(lib.espace_projected_linear(px, ldx, pp, ldp, pw, ldw, py, ldy, M, K, L, N, _dt(X),
                                            ctypes.c_void_p(ws.data_ptr() if ws is not None else 0),
                                            wsb, _stream(X.device)))
+    return Y
+
+
+def espace_projected_linear_noalloc(X, Pt, Wf, Y):
+    """Y = Wf·(Pᵀ·X) into a caller-provided Y, with the library's static device
+    scratch in place of a workspace (the C call allocates nothing)."""
+    N, K = X.shape
+    L = Pt.shape[0]
+    M = Wf.shape[0]
+    _same(X, "X", (Pt, "Pt"), (Wf, "Wf"))
+    Y = _out(Y, N, M, X, "Y")
+    px, ldx = _mat(X, "X")
+    pp, ldp = _mat(Pt, "Pt")
+    pw, ldw = _mat(Wf, "Wf")
+    py, ldy = _mat(Y, "Y")
+    with torch.cuda.device(X.device):
+        _check(lib.espace_projected_linear_noalloc(px, ldx, pp, ldp, pw, ldw, py, ldy, M, K, L, N, _dt(X),
+                                                   _stream(X.device)))
     return Y
 
 

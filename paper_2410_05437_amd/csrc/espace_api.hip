@@ -19,6 +19,11 @@
 
 #include "kernels.hpp"
 
+// Scratch of espace_projected_linear_noalloc: Z and the partial sums of one
+// call, held by every device the library runs on until the process ends.
+// Calls on one device share it.
+static __device__ __align__(256) unsigned char scratch[ESPACE_NOALLOC_SCRATCH_BYTES];
+
 // Count of the bounded cross-workgroup waits that gave up (one per device;
 // the kernels add to it through the address hipGetSymbolAddress gives).
 __device__ unsigned long long g_wait_timeouts;
@@ -479,6 +484,42 @@ espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, voi
     return ESPACE_OK;
 }
 
+// The layer's launches after validation: Z and the partial sums in
+// `workspace` (ws_bytes(ESPACE_OP_PROJECTED_LINEAR, ...) bytes).
+espace_status projected_linear_launch(const void* X, int64_t ldx, const void* Pt, int64_t ldp, const void* Wf,
+                                      int64_t ldwf, void* Y, int64_t ldy, int64_t M, int64_t K, int64_t L,
+                                      int64_t N, espace_dtype dt, void* workspace, hipStream_t stream) {
+    const int64_t ldz = z_ld(L, N, dt);
+    void* Z = workspace;
+    void* partial = (char*)workspace + z_bytes(N, L, dt);
+    ESPACE_TRY(run_tn(X, ldx, Pt, ldp, Z, ldz, N, L, K, dt, partial, stream));
+    ESPACE_TRY(run_tn(Z, ldz, Wf, ldwf, Y, ldy, N, M, L, dt, partial, stream));
+    return ESPACE_OK;
+}
+
+// Device address of this device's copy of `scratch`, looked up once per
+// device with that device current (the array's name in host code is a
+// host-side stand-in, never passed to a kernel).
+espace_status noalloc_scratch(void** out) {
+    static std::mutex mu;
+    static void* ptr[64] = {nullptr};
+    int dev = 0;
+    const hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= 64) return fail(ESPACE_ERR_DEVICE, "device id %d out of range", dev);
+    std::lock_guard<std::mutex> lk(mu);
+    if (!ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t g = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (g != hipSuccess || !p)
+            return fail(ESPACE_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(g));
+        if ((uintptr_t)p % kWsAlign) return fail(ESPACE_ERR_ALIGN, "scratch not 256-byte aligned");
+        ptr[dev] = p;
+    }
+    *out = ptr[dev];
+    return ESPACE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -626,11 +667,34 @@ espace_status espace_projected_linear(const void* X, int64_t ldx, const void* Pt
     const Range wsr{"workspace", ws.lo, ws.lo + need};
     ESPACE_TRY(check_alias(wsr, ins, 3));
     ESPACE_TRY(check_device());
-    const int64_t ldz = z_ld(L, N, dt);
-    void* Z = workspace;
-    void* partial = (char*)workspace + z_bytes(N, L, dt);
-    ESPACE_TRY(run_tn(X, ldx, Pt, ldp, Z, ldz, N, L, K, dt, partial, stream));
-    ESPACE_TRY(run_tn(Z, ldz, Wf, ldwf, Y, ldy, N, M, L, dt, partial, stream));
+    ESPACE_TRY(projected_linear_launch(X, ldx, Pt, ldp, Wf, ldwf, Y, ldy, M, K, L, N, dt, workspace, stream));
+    return ok();
+}
+
+espace_status espace_projected_linear_noalloc(const void* X, int64_t ldx, const void* Pt, int64_t ldp,
+                                              const void* Wf, int64_t ldwf, void* Y, int64_t ldy,
+                                              int64_t M, int64_t K, int64_t L, int64_t N, espace_dtype dt,
+                                              hipStream_t stream) {
+    ESPACE_TRY(check_dtype(dt));
+    ESPACE_TRY(check_dims(M, K, L, N, true));
+    if (M == 0 || N == 0) return ok();
+    ESPACE_TRY(check_mat("X", X, N, K, ldx, dt));
+    ESPACE_TRY(check_mat("Pt", Pt, L, K, ldp, dt));
+    ESPACE_TRY(check_mat("Wf", Wf, M, L, ldwf, dt));
+    ESPACE_TRY(check_mat("Y", Y, N, M, ldy, dt));
+    const size_t need = ws_bytes(ESPACE_OP_PROJECTED_LINEAR, M, K, L, N, dt);
+    if (need > (size_t)ESPACE_NOALLOC_SCRATCH_BYTES)
+        return fail(ESPACE_ERR_WORKSPACE,
+                    "these sizes need %zu bytes of scratch, above the %zu bytes the allocation-free call holds "
+                    "(use espace_projected_linear with a workspace)",
+                    need, (size_t)ESPACE_NOALLOC_SCRATCH_BYTES);
+    const Range ins[] = {mat_range("X", X, N, ldx, dt), mat_range("Pt", Pt, L, ldp, dt),
+                         mat_range("Wf", Wf, M, ldwf, dt)};
+    ESPACE_TRY(check_alias(mat_range("Y", Y, N, ldy, dt), ins, 3));
+    ESPACE_TRY(check_device());
+    void* ws = nullptr;
+    ESPACE_TRY(noalloc_scratch(&ws));
+    ESPACE_TRY(projected_linear_launch(X, ldx, Pt, ldp, Wf, ldwf, Y, ldy, M, K, L, N, dt, ws, stream));
     return ok();
 }
 

@@ -21,7 +21,8 @@ def test_exports_every_declared_function():
         "espace_dense_linear", "espace_workspace_bytes", "espace_status_string",
         "espace_last_error", "espace_abi_version", "espace_autocorrelation_update",
         "espace_principal_components", "espace_symmetrized_product", "espace_projected_linear_backward",
-        "espace_dense_linear_backward", "espace_wait_timeouts", "espace_set_wait_limit"}
+        "espace_dense_linear_backward", "espace_wait_timeouts", "espace_set_wait_limit",
+        "espace_projected_linear_noalloc"}
     for n in names:
         assert hasattr(L, n)
     assert E.ABI_VERSION == 6
@@ -231,3 +232,25 @@ def test_binding_rejects_mixed_operand_types():
         E.espace_dense_linear_backward(torch.zeros(8, 32, dtype=f32), X.to(bf), W)
     with pytest.raises(ValueError, match="B"):
         E.espace_symmetrized_product(torch.zeros(4, 4), torch.zeros(4, 4, dtype=bf))
+
+
+NOALLOC_MAX = 64 << 20
+
+
+def test_noalloc_rejects_sizes_beyond_its_scratch():
+    """The allocation-free call refuses, before touching any device, sizes
+    whose Z and partial sums exceed its static scratch."""
+    big_n = 1 << 16
+    need = E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, 4096, 4096, 1536, big_n, __import__("torch").bfloat16)
+    assert need > NOALLOC_MAX
+    s = L.espace_projected_linear_noalloc(P16, 4096, ctypes.c_void_p(0x100000000000), 4096,
+                                          ctypes.c_void_p(0x200000000000), 1536, ctypes.c_void_p(0x300000000000),
+                                          4096, 4096, 4096, 1536, big_n, 1, NULL)
+    assert s == 6
+    assert "scratch" in L.espace_last_error().decode()
+    # sizes that fit get past validation and fail only for want of a device
+    s = L.espace_projected_linear_noalloc(P16, 64, P16b, 64, P16c, 16, ctypes.c_void_p(0x60000000), 32,
+                                          32, 64, 16, 8, 1, NULL)
+    assert s in (7, 8)
+    assert L.espace_projected_linear_noalloc(NULL, 64, P16b, 64, P16c, 16, ctypes.c_void_p(0x60000000), 32,
+                                             32, 64, 16, 8, 1, NULL) == 1
