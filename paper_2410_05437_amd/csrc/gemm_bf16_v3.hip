@@ -137,6 +137,9 @@ void gemm_tn_bf16_v3_kernel(const uint16_t* __restrict__ A, int64_t lda,
 #pragma unroll
         for (int x = 0; x < C::NRD; ++x) v3_read_dyn<NBJ>(x, fa0, fb0, aA0, aB0);
         v3_wait_lgkm0();
+        // the first sub-step loads step kt0 + 2 into the half-stage just read:
+        // every wave's reads of it must be complete before any wave issues them
+        __builtin_amdgcn_s_barrier();
 
         int kt = kt0;
         int rel = 0;          // stage of step kt relative to s0
