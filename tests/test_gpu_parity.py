@@ -483,3 +483,50 @@ def test_prefill_layer_under_graph_replay(E):
     B = parity.layer_bound(Y64, Z64, Wf64, parity.row_norms(i0.X), parity.row_norms(i0.Pt), parity.row_norms(i0.W),
                            K, L, parity.U_BF16)
     parity.check(host64(Y), Y64, B, 1e-2, "prefill layer under graph replay")
+
+
+# (K, M, L, N) of prefill layers: a projection whose tiles split their depth
+# in two halves combined in-kernel (the Llama2-7B shape class), ragged token
+# blocks, components and features (a feature count that is not a multiple of
+# 8 takes the scalar stores), a projection of more tiles than CUs
+PREFILL_SHAPES = [(4100, 3000, 1536, 4096), (1003, 517, 131, 301), (700, 1234, 520, 5000),
+                (4500, 1000, 4000, 4096), (2048, 4096, 256, 40)]
+
+
+def _layer_ref(inp):
+    w = inp.w
+    Z64 = oracle.project(inp.Pt, inp.X)
+    Wf64 = oracle.fold(inp.W, inp.Pt)
+    Y64 = oracle.expand(Z64, Wf64)
+    B = parity.layer_bound(Y64, Z64, Wf64, parity.row_norms(inp.X), parity.row_norms(inp.Pt),
+                           parity.row_norms(inp.W), w.K, w.L, parity.U_BF16)
+    return Y64, B
+
+
+@pytest.mark.parametrize("shape", PREFILL_SHAPES, ids=lambda s: "K%d_M%d_L%d_N%d" % s)
+def test_prefill_layer_shapes(E, shape):
+    """The projected linear layer at prefill shapes against the oracle on every
+    output, and bitwise identical whatever its workspace held before (zeros,
+    all ones, random bytes, the previous call's state): the in-kernel pair
+    combine's state words carry a per-call tag."""
+    dev = need_gpu()
+    K, M, L, N = shape
+    inp = _inputs(K, M, L, N, "bf16", seed=80)
+    X, Pt, W = _dev_inputs(inp, dev)
+    Wf = E.espace_fold_weights(W, Pt)
+    Y = E.espace_projected_linear(X, Pt, Wf, out_mat(N, M, "bf16", dev))
+    torch.cuda.synchronize()
+    Y64, B = _layer_ref(inp)
+    parity.check(host64(Y), Y64, B, TOL["bf16"], "prefill layer")
+    assert np.isnan(padding(Y)).all()
+    need = E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, M, K, L, N, torch.bfloat16)
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    gen = torch.Generator(device="cpu").manual_seed(8)
+    for fill in ["zeros", "ones", "random", "keep", "keep"]:
+        if fill == "zeros":
+            ws.zero_()
+        elif fill == "ones":
+            ws.fill_(255)
+        elif fill == "random":
+            ws.copy_(torch.randint(0, 256, (need,), dtype=torch.uint8, generator=gen))
+        assert torch.equal(E.espace_projected_linear(X, Pt, Wf, workspace=ws), Y), fill
