@@ -12,8 +12,9 @@ the method prescribes.  Prints one JSON line.
 Also measured in the same run: the dense layer Y = W·X on the same GPU with
 this library's own kernels (speedup denominator), the fold, the two kernels
 of the path separately (HIP events on the launch stream; the slower one is
-the roofline kernel), decode-sized calls of the Llama2-7B FFN up+gate layer,
-and the CPU oracle on the host cores (cpu_baseline).
+the roofline kernel), the prefill layers of the other workloads, decode token
+counts (N = 1, 8, 16 of the Llama2-7B FFN up+gate layer; N = 1, 16 of the
+GPT3-22B FFN layers), and the CPU oracle on the host cores (cpu_baseline).
 """
 import argparse
 import json
@@ -42,6 +43,11 @@ PAPER_TABLE1 = {"hardware": "NVIDIA A100, BF16, native PyTorch (Table 1, App. B.
                 "headline": "35-45% GEMM latency, up to ~40% TTFT reduction"}
 
 
+def note(msg):
+    """Progress line on stderr (the JSON result goes alone to stdout)."""
+    print(f"bench: {msg}", file=sys.stderr, flush=True)
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -54,8 +60,8 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--kernel-probe", action="store_true",
-                    help="run only a 1 GiB elementwise copy and `steps` launches of the "
-                         "expand GEMM (for hardware-counter runs), then exit")
+                    help="run only the launch sequence of the hardware-counter runs (a 1 GiB "
+                         "elementwise copy, then `steps` launches of each kernel phase), then exit")
     return ap.parse_args()
 
 
@@ -163,6 +169,73 @@ def stored_traffic():
         return None, "summary unreadable"
 
 
+PROBE_DECODE_NS = (1, 8, 16)
+
+
+def kernel_probe(E, dev, stream, args, Xr, Pr, Wfr, Ws, Y, ws, Z, wsz, wse, R):
+    """Launch sequence for the counter runs (rocprofv3 --pmc): the 1 GiB copy
+    the byte counters are scaled by, then `steps` launches of each phase below,
+    consecutive phases separated by one GPU sleep kernel (the marker the
+    summary splits the dispatches at):
+      project, expand, dense   - the Llama2-7B QKV layer's kernels (N=4096)
+      layer_N{n}, dense_N{n}   - the Llama2-7B FFN up+gate layer and its dense
+                                 layer at decode token counts n = 1, 8, 16
+    Every phase rotates its weights over copies larger than the last-level
+    cache.  Prints the phase list as JSON."""
+    import torch
+    bf = torch.bfloat16
+    S = args.steps
+    phases = []
+
+    def phase(name, fn, n_args):
+        torch.cuda._sleep(1000)
+        for i in range(S):
+            fn(i % n_args)
+        torch.cuda._sleep(1000)
+        phases.append(name)
+
+    Rd = copies((Xr[0].numel() + Ws.numel()) * 2)
+    Wr = [Ws] + [clone_padded(Ws) for _ in range(Rd - 1)]
+    wsd = torch.empty(max(E.espace_workspace_bytes(E.OP_DENSE, Ws.shape[0], Ws.shape[1], 1, Xr[0].shape[0], bf),
+                          1), dtype=torch.uint8, device=dev)
+    E.espace_project(Pr[0], Xr[0], Z, wsz)
+    torch.cuda.synchronize()
+    copy_probe(dev)
+    phase("project", lambda i: E.espace_project(Pr[i], Xr[i], Z, wsz), R)
+    phase("expand", lambda i: E.espace_expand(Z, Wfr[i], Y, wse), R)
+    phase("dense", lambda i: E.espace_dense_linear(Xr[i % R], Wr[i], Y, wsd), Rd)
+    torch.cuda.synchronize()
+    del Wr, wsd
+    # decode: Llama2-7B FFN up+gate
+    K, M, L = 4096, 22016, 1536
+    X0 = _rand_mat(E, max(PROBE_DECODE_NS), K, 1.0, dev)
+    Pt0 = _rand_mat(E, L, K, K ** -0.5, dev)
+    W0 = _rand_mat(E, M, K, K ** -0.5, dev)
+    Wf0 = E.espace_fold_weights(W0, Pt0)
+    Rl = copies((Pt0.numel() + Wf0.numel()) * 2)
+    Pl = [Pt0] + [clone_padded(Pt0) for _ in range(Rl - 1)]
+    Wfl = [Wf0] + [clone_padded(Wf0) for _ in range(Rl - 1)]
+    Rw = copies(W0.numel() * 2)
+    Wl = [W0] + [clone_padded(W0) for _ in range(Rw - 1)]
+    bufs = {}
+    for N in PROBE_DECODE_NS:
+        bufs[N] = (E.padded_empty(N, M, bf, dev),
+                   torch.empty(max(E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, M, K, L, N, bf), 1),
+                               dtype=torch.uint8, device=dev),
+                   torch.empty(max(E.espace_workspace_bytes(E.OP_DENSE, M, K, 1, N, bf), 1),
+                               dtype=torch.uint8, device=dev))
+    torch.cuda.synchronize()
+    for N in PROBE_DECODE_NS:
+        Yn, wsn, wsdn = bufs[N]
+        X = X0[:N]
+        phase(f"layer_N{N}", lambda i: E.espace_projected_linear(X, Pl[i], Wfl[i], Yn, wsn), Rl)
+        phase(f"dense_N{N}", lambda i: E.espace_dense_linear(X, Wl[i], Yn, wsdn), Rw)
+    torch.cuda.synchronize()
+    print(json.dumps({"kernel_probe": phases, "launches_per_phase": S, "copy_probe_bytes": COPY_PROBE_BYTES,
+                      "qkv": {"K": 4096, "M": 12288, "L": 1536, "N": 4096},
+                      "decode": {"K": K, "M": M, "L": L, "N": list(PROBE_DECODE_NS)}}), flush=True)
+
+
 def cpu_baseline(inp, seconds):
     """The float64 oracle of the same layer on the host cores (fold excluded,
     as on the GPU); repeated full calls for about `seconds` seconds."""
@@ -234,13 +307,7 @@ def main():
         E.espace_projected_linear(Xr[i], Pr[i], Wfr[i], Y, ws)
 
     if args.kernel_probe:
-        copy_probe(dev)
-        E.espace_project(Pts, Xs, Z, wsz)
-        for i in range(args.steps):
-            E.espace_expand(Z, Wfr[i % R], Y, wse)
-        torch.cuda.synchronize()
-        print(json.dumps({"kernel_probe": "expand", "launches": args.steps, "R": N, "Cc": M, "D": L,
-                          "copy_probe_bytes": COPY_PROBE_BYTES}), flush=True)
+        kernel_probe(E, dev, stream, args, Xr, Pr, Wfr, Ws, Y, ws, Z, wsz, wse, R)
         return
 
     # the timed region: exactly `steps` calls, synchronised on both sides
@@ -258,6 +325,7 @@ def main():
 
     flops = acc.projected_flops(K, M, L, N)
     tflops = flops / (ms * 1e-3) / 1e12
+    note(f"timed region: {ms * 1e3:.1f} us per layer")
 
     # the two kernels of the path, each as `steps` back-to-back launches between
     # two events on the launch stream (average launch duration)
@@ -315,18 +383,24 @@ def main():
     detail["expand_algorithmic_bytes"] = acc.gemm_bytes(N, M, L)
     detail["traffic_note"] = traffic_note
 
+    note("kernels, dense baseline and fold timed")
     if not args.no_decode:
-        detail["decode"] = decode_lines(E, acc, synth, dev, stream, args)
+        detail["decode"] = decode_lines(E, acc, dev, stream, args)
+        note("decode lines done")
     if not args.no_calibration:
         detail["calibration"] = calibration_lines(E, Xs, dev, stream, args)
+        note("calibration lines done")
     if not args.no_training:
         detail["training"] = training_lines(E, Xs, Pts, Ws, dev, stream, args)
+        note("training lines done")
     if not args.no_workloads:
         detail["workloads"] = workload_lines(E, acc, dev, stream, args)
+        note("workload lines done")
 
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(inp, args.cpu_seconds)
+        note("cpu baseline done")
 
     out = {
         "metric": "projected-linear TFLOP/s + µs/layer and speedup vs dense GEMM at 50% compression",
@@ -346,7 +420,9 @@ def main():
         "roofline": {"bound": "mfma", "kernel": dom,
                      "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": traffic if dom == "expand" else None},
+                     "traffic": traffic if dom == "expand" else None,
+                     "layer_achieved": round(tflops, 1),
+                     "layer_frac": round(tflops / PEAK_BF16_TFLOPS, 4)},
         "cpu_baseline": cpu,
         "detail": detail,
     }
@@ -357,59 +433,88 @@ def main():
 OTHER_LAYERS = [
     ("llama2_7b_ffn_upgate", 4096, 22016, 1536, 4096),
     ("llama2_7b_ffn_down", 11008, 4096, 1536, 4096),
-    ("gpt3_22b_ffn_up_L2458", 6144, 24576, 2458, 8192),
-    ("gpt3_22b_ffn_down_L2458", 24576, 6144, 2458, 8192),
-    ("gpt3_22b_ffn_up_L3686", 6144, 24576, 3686, 8192),
-    ("gpt3_22b_ffn_up_L1966", 6144, 24576, 1966, 8192),
-]
+] + [(f"gpt3_22b_ffn_{layer}_L{L}", K, M, L, 8192)
+     for layer, K, M in (("up", 6144, 24576), ("down", 24576, 6144))
+     for L in (3686, 2458, 1966)]
+
+# decode layers: (name, K, M, L, token counts)
+DECODE_LAYERS = [("llama2_7b_ffn_upgate", 4096, 22016, 1536, (1, 8, 16))] + [
+    (f"gpt3_22b_ffn_{layer}_L{L}", K, M, L, (1, 16))
+    for layer, K, M in (("up", 6144, 24576), ("down", 24576, 6144))
+    for L in (3686, 2458, 1966)]
 
 
-def workload_lines(E, acc, dev, stream, args):
-    """The prefill layers of the other workloads (Llama2-7B FFN, GPT3-22B FFN
-    at 25/50/60% compression): µs per layer, TFLOP/s and MFMA fraction, and
-    the dense layer on the same kernels.  Random bf16 operands of the layer's
-    shape (the parity tests cover these shapes against the oracle), rotated
-    over copies larger than the last-level cache."""
+def _rand_mat(E, r, c, scale, dev):
+    import torch
+    t = E.padded_empty(r, c, torch.bfloat16, dev)
+    t.copy_(torch.randn(r, c, device=dev) * scale)
+    return t
+
+
+def layer_case(E, acc, dev, stream, K, M, L, Ns, steps, warmup, prequeue):
+    """The projected linear layer and the dense layer of one shape at the token
+    counts Ns, on random bf16 operands of that shape (the parity tests cover
+    these shapes against the oracle).  The weights (Pt and Wf, or W for the
+    dense layer) and, for prefill, the activations rotate over copies larger
+    than the last-level cache, so every call streams its operands from HBM.
+    Returns {N: timings}."""
     import torch
     bf = torch.bfloat16
+    Nmax = max(Ns)
+    X0 = _rand_mat(E, Nmax, K, 1.0, dev)
+    Pt0 = _rand_mat(E, L, K, K ** -0.5, dev)
+    W0 = _rand_mat(E, M, K, K ** -0.5, dev)
+    Wf0 = E.espace_fold_weights(W0, Pt0)
     out = {}
-    n = max(3, args.steps // 10)
-    for name, K, M, L, N in OTHER_LAYERS:
-        def mk(r, c, scale):
-            t = E.padded_empty(r, c, bf, dev)
-            t.copy_(torch.randn(r, c, device=dev) * scale)
-            return t
-        X0, Pt0, W0 = mk(N, K, 1.0), mk(L, K, K ** -0.5), mk(M, K, K ** -0.5)
-        Wf0 = E.espace_fold_weights(W0, Pt0)
-        R = copies((X0.numel() + Pt0.numel() + Wf0.numel()) * 2)
-        Xr = [X0] + [clone_padded(X0) for _ in range(R - 1)]
+    for N in Ns:
+        rot_x = N > 32
+        one = (Pt0.numel() + Wf0.numel() + (N * K if rot_x else 0)) * 2
+        R = copies(one)
+        Xr = [X0[:N]] + [clone_padded(X0[:N]) for _ in range(R - 1)] if rot_x else [X0[:N]] * R
         Pr = [Pt0] + [clone_padded(Pt0) for _ in range(R - 1)]
         Wfr = [Wf0] + [clone_padded(Wf0) for _ in range(R - 1)]
         Y = E.padded_empty(N, M, bf, dev)
-        ws = torch.empty(max(E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, M, K, L, N, bf), 1), dtype=torch.uint8,
-                         device=dev)
-        ms = time_calls(lambda i: E.espace_projected_linear(Xr[i], Pr[i], Wfr[i], Y, ws), R, n, 2, stream)
+        ws = torch.empty(max(E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, M, K, L, N, bf), 1),
+                         dtype=torch.uint8, device=dev)
+        ms = time_calls(lambda i: E.espace_projected_linear(Xr[i], Pr[i], Wfr[i], Y, ws), R, steps, warmup,
+                        stream, prequeue=prequeue)
         del Pr, Wfr
-        Rd = copies((X0.numel() + W0.numel()) * 2)
+        Rd = copies((W0.numel() + (N * K if rot_x else 0)) * 2)
         Wr = [W0] + [clone_padded(W0) for _ in range(Rd - 1)]
         wsd = torch.empty(max(E.espace_workspace_bytes(E.OP_DENSE, M, K, 1, N, bf), 1), dtype=torch.uint8,
                           device=dev)
-        ms_d = time_calls(lambda i: E.espace_dense_linear(Xr[i % R], Wr[i], Y, wsd), Rd, n, 2, stream)
-        tf = acc.projected_flops(K, M, L, N) / (ms * 1e-3) / 1e12
-        tfd = acc.dense_flops(K, M, N) / (ms_d * 1e-3) / 1e12
+        ms_d = time_calls(lambda i: E.espace_dense_linear(Xr[i % R], Wr[i], Y, wsd), Rd, steps, warmup, stream,
+                          prequeue=prequeue)
+        out[N] = {"ms": ms, "ms_dense": ms_d, "copies": R}
+        del Xr, Wr, Y, ws, wsd
+        torch.cuda.empty_cache()
+    del X0, Pt0, W0, Wf0
+    torch.cuda.empty_cache()
+    return out
+
+
+def workload_lines(E, acc, dev, stream, args):
+    """The prefill layers of the other workloads (Llama2-7B FFN up+gate and
+    down, GPT3-22B FFN up and down at L = 3686, 2458, 1966): µs per layer,
+    TFLOP/s and MFMA fraction, and the dense layer on the same kernels."""
+    out = {}
+    n = max(3, args.steps // 10)
+    for name, K, M, L, N in OTHER_LAYERS:
+        t = layer_case(E, acc, dev, stream, K, M, L, (N,), n, 2, False)[N]
+        tf = acc.projected_flops(K, M, L, N) / (t["ms"] * 1e-3) / 1e12
+        tfd = acc.dense_flops(K, M, N) / (t["ms_dense"] * 1e-3) / 1e12
         out[name] = {
             "K": K, "M": M, "L": L, "N": N,
             "compression": round(acc.compression(K, M, L), 4),
-            "us_per_layer": round(ms * 1e3, 1),
+            "us_per_layer": round(t["ms"] * 1e3, 1),
             "tflops": round(tf, 1),
             "mfma_frac": round(tf / PEAK_BF16_TFLOPS, 4),
-            "dense_us": round(ms_d * 1e3, 1),
+            "dense_us": round(t["ms_dense"] * 1e3, 1),
             "dense_mfma_frac": round(tfd / PEAK_BF16_TFLOPS, 4),
-            "speedup_vs_dense": round(ms_d / ms, 3),
+            "speedup_vs_dense": round(t["ms_dense"] / t["ms"], 3),
             "ideal_speedup": round(acc.ideal_speedup(K, M, L), 3),
+            "rotating_copies": t["copies"],
         }
-        del Xr, Wr, Y, ws, wsd, X0, Pt0, W0, Wf0
-        torch.cuda.empty_cache()
     return out
 
 
@@ -514,45 +619,27 @@ def calibration_lines(E, Xs, dev, stream, args):
     }
 
 
-def decode_lines(E, acc, synth, dev, stream, args):
-    """Llama2-7B FFN up+gate (K=4096, M=22016, L=1536) at N = 1 and 16 tokens:
-    HBM-bound, rotating over copies larger than the last-level cache."""
-    import torch
+def decode_lines(E, acc, dev, stream, args):
+    """Decode token counts: the Llama2-7B FFN up+gate layer at N = 1, 8, 16
+    and the GPT3-22B FFN up and down layers at N = 1, 16 for L = 3686, 2458,
+    1966.  HBM-bound: µs per layer, algorithmic bytes over time against the
+    HBM peak, and the dense layer on the same kernels."""
     res = {}
-    base = synth.workload(2, N=16)
-    inp = synth.make_inputs(base)
-    K, M, L = base.K, base.M, base.L
-    Ps = to_dev(inp.Pt_s, dev)
-    Ws = to_dev(inp.W_s, dev)
-    Wf = E.espace_fold_weights(Ws, Ps)
-    Xall = to_dev(inp.X_s, dev)
-    R = copies((Ps.numel() + Wf.numel()) * 2)
-    Pr = [Ps] + [clone_padded(Ps) for _ in range(R - 1)]
-    Wfr = [Wf] + [clone_padded(Wf) for _ in range(R - 1)]
-    Rd = copies(Ws.numel() * 2)
-    Wr = [Ws] + [clone_padded(Ws) for _ in range(Rd - 1)]
-    for N in (1, 16):
-        X = Xall[:N]
-        Y = E.padded_empty(N, M, torch.bfloat16, dev)
-        ws = torch.empty(max(E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, M, K, L, N,
-                                                      torch.bfloat16), 1),
-                         dtype=torch.uint8, device=dev)
-        wsd = torch.empty(max(E.espace_workspace_bytes(E.OP_DENSE, M, K, 1, N, torch.bfloat16), 1),
-                          dtype=torch.uint8, device=dev)
-        ms = time_calls(lambda i: E.espace_projected_linear(X, Pr[i], Wfr[i], Y, ws), R,
-                        args.steps * 4, args.warmup, stream, prequeue=True)
-        msd = time_calls(lambda i: E.espace_dense_linear(X, Wr[i], Y, wsd), Rd,
-                         args.steps * 4, args.warmup, stream, prequeue=True)
-        by = acc.projected_bytes(K, M, L, N)
-        byd = acc.dense_bytes(K, M, N)
-        res[f"N{N}"] = {
-            "us_per_layer": round(ms * 1e3, 2),
-            "GB_s": round(by / (ms * 1e-3) / 1e9, 1),
-            "hbm_frac": round(by / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-            "dense_us": round(msd * 1e3, 2),
-            "dense_GB_s": round(byd / (msd * 1e-3) / 1e9, 1),
-            "speedup_vs_dense": round(msd / ms, 3),
-        }
+    for name, K, M, L, Ns in DECODE_LAYERS:
+        ts = layer_case(E, acc, dev, stream, K, M, L, Ns, args.steps * 4, args.warmup, True)
+        for N, t in ts.items():
+            by = acc.projected_bytes(K, M, L, N)
+            byd = acc.dense_bytes(K, M, N)
+            res[f"{name}_N{N}"] = {
+                "K": K, "M": M, "L": L, "N": N,
+                "us_per_layer": round(t["ms"] * 1e3, 2),
+                "GB_s": round(by / (t["ms"] * 1e-3) / 1e9, 1),
+                "hbm_frac": round(by / (t["ms"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                "dense_us": round(t["ms_dense"] * 1e3, 2),
+                "dense_GB_s": round(byd / (t["ms_dense"] * 1e-3) / 1e9, 1),
+                "speedup_vs_dense": round(t["ms_dense"] / t["ms"], 3),
+                "rotating_copies": t["copies"],
+            }
     return res
 
 

@@ -1,7 +1,8 @@
 """Text summaries of rocprofv3 outputs of bench.py (written to profiles/).
 
-    python -m paper_2410_05437_amd.prof_summary stats TRACE_CSV OUT_MD CMD [--steps S --warmup W]
-    python -m paper_2410_05437_amd.prof_summary traffic FETCH_CSV WRITE_CSV OUT_MD CMD_FETCH CMD_WRITE
+    python profile_summary.py stats TRACE_CSV OUT_MD CMD [--steps S --warmup W]
+    python profile_summary.py traffic FETCH_CSV WRITE_CSV OUT_MD CMD_FETCH CMD_WRITE
+    python profile_summary.py counters OUT_MD --run CSV CMD [--run CSV CMD ...]
 
 `stats` reads a `--kernel-trace --output-format csv` trace and tabulates
 launches per kernel and grid; the 256x256 GEMM launches that serve both the
@@ -9,6 +10,11 @@ expand GEMM and the dense baseline are split by their place in bench.py's
 launch order.  `traffic` reads two `--pmc FETCH_SIZE` / `--pmc WRITE_SIZE`
 runs of `bench.py --kernel-probe` and scales the expand GEMM's counters by
 what the same counters read for the 1 GiB elementwise copy of that run.
+`counters` reads any number of `--pmc` runs of `bench.py --kernel-probe`,
+splits each run's dispatches into the probe's phases at its marker kernels
+and tabulates every counter per phase and kernel, with the MFMA busy ratio,
+the MFMA flops against the algorithmic flops, and the byte counters scaled
+by the copy calibration.
 """
 import argparse
 import collections
@@ -16,7 +22,7 @@ import csv
 import os
 import sys
 
-ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+ROOT = os.path.dirname(os.path.abspath(__file__))
 EXPAND_KERNEL = "gemm_tn_bf16_v3_kernel<0, 256>"   # the four-wave 256x256 kernel, bf16 output
 EXPAND_GRID = 256 * 256                        # one workgroup of 256 threads per CU
 COPY_KERNELS = ("AUnaryFunctor<c10::BFloat16", "MulFunctor")   # torch.mul(bf16, 1.0)
@@ -83,18 +89,28 @@ def stats(args):
     print("\n".join(lines))
 
 
-def _counter(path, counter):
-    """{(kernel name, dispatch id): value} for one counter of a pmc run."""
-    vals = {}
+MARKER = "spin_kernel"           # torch.cuda._sleep, around each of the probe's phases
+# the phases of bench.py --kernel-probe, in launch order
+PROBE_PHASES = ["project", "expand", "dense", "layer_N1", "dense_N1", "layer_N8", "dense_N8",
+                "layer_N16", "dense_N16"]
+OWN = ("gemm_tn", "skinny_tn", "gemv_", "splitk_reduce", "espace::")
+
+
+def _dispatches(path):
+    """Dispatches of one pmc run in launch order: name, grid, {counter: value}."""
+    by = {}
     for r in csv.DictReader(open(path)):
-        if r["Counter_Name"] != counter:
-            continue
-        vals[(r["Kernel_Name"], r["Dispatch_Id"], int(r["Grid_Size"]))] = float(r["Counter_Value"])
-    return vals
+        d = by.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"], "grid": int(r["Grid_Size"]), "c": {}})
+        d["c"][r["Counter_Name"]] = d["c"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return [by[k] for k in sorted(by)]
 
 
-def _select(vals, pred):
-    return [v for (name, _, grid), v in vals.items() if pred(name, grid)]
+def _phases(ds, names):
+    """{phase: [dispatch]}: phase i lies between markers 2i and 2i + 1."""
+    marks = [i for i, d in enumerate(ds) if MARKER in d["name"]]
+    if len(marks) < 2 * len(names):
+        raise SystemExit(f"{len(marks)} markers for {len(names)} phases")
+    return {n: ds[marks[2 * i] + 1:marks[2 * i + 1]] for i, n in enumerate(names)}
 
 
 def traffic(args):
@@ -103,9 +119,10 @@ def traffic(args):
     from paper_2410_05437_amd import accounting as acc
     res = {}
     for counter, path in (("FETCH_SIZE", args.fetch), ("WRITE_SIZE", args.write)):
-        vals = _counter(path, counter)
-        exp = _select(vals, lambda n, g: EXPAND_KERNEL in n and g == EXPAND_GRID)
-        cpy = _select(vals, lambda n, g: all(k in n for k in COPY_KERNELS))
+        ds = _dispatches(path)
+        ph = _phases(ds, PROBE_PHASES)["expand"]
+        exp = [d["c"][counter] for d in ph if EXPAND_KERNEL in d["name"] and d["grid"] == EXPAND_GRID]
+        cpy = [d["c"][counter] for d in ds if all(k in d["name"] for k in COPY_KERNELS)]
         if not exp or len(cpy) != 1:
             raise SystemExit(f"{counter}: expected expand launches and one copy, found {len(exp)} / {len(cpy)}")
         scale = (COPY_BYTES / 1024.0) / cpy[0]     # counters are in KiB
@@ -138,6 +155,84 @@ def traffic(args):
     print("\n".join(lines))
 
 
+def _alg(phase, probe):
+    """(algorithmic flops, algorithmic bytes) of one launch of a probe phase."""
+    from paper_2410_05437_amd import accounting as acc
+    q, d = probe["qkv"], probe["decode"]
+    if phase == "project":
+        return acc.gemm_flops(q["N"], q["L"], q["K"]), acc.gemm_bytes(q["N"], q["L"], q["K"])
+    if phase == "expand":
+        return acc.gemm_flops(q["N"], q["M"], q["L"]), acc.gemm_bytes(q["N"], q["M"], q["L"])
+    if phase == "dense":
+        return acc.gemm_flops(q["N"], q["M"], q["K"]), acc.gemm_bytes(q["N"], q["M"], q["K"])
+    n = int(phase.split("_N")[1])
+    if phase.startswith("layer"):
+        return acc.projected_flops(d["K"], d["M"], d["L"], n), acc.projected_bytes(d["K"], d["M"], d["L"], n)
+    return acc.dense_flops(d["K"], d["M"], n), acc.dense_bytes(d["K"], d["M"], n)
+
+
+def counters(args):
+    sys.path.insert(0, ROOT)
+    probe = {"qkv": {"K": 4096, "M": 12288, "L": 1536, "N": 4096},
+             "decode": {"K": 4096, "M": 22016, "L": 1536, "N": [1, 8, 16]}, "phases": PROBE_PHASES}
+    table = collections.OrderedDict()      # (phase, kernel, grid) -> {counter: [values]}
+    scale = {}
+    for path, _ in args.run:
+        ds = _dispatches(path)
+        cpy = [d for d in ds if all(k in d["name"] for k in COPY_KERNELS)]
+        for c in ("FETCH_SIZE", "WRITE_SIZE"):
+            if cpy and c in cpy[0]["c"]:
+                scale[c] = (COPY_BYTES / 1024.0) / cpy[0]["c"][c]
+        for ph, rows in _phases(ds, probe["phases"]).items():
+            for d in rows:
+                if not any(k in d["name"] for k in OWN):
+                    continue
+                key = (ph, _short(d["name"]), d["grid"])
+                ent = table.setdefault(key, collections.defaultdict(list))
+                for c, v in d["c"].items():
+                    ent[c].append(v)
+    lines = ["# Hardware counters: the projected linear layer's kernels and the dense layer's", "",
+             "Llama2-7B fused QKV (K=4096, M=12288, L=1536, N=4096): project, expand and dense GEMMs; "
+             "Llama2-7B FFN up+gate (K=4096, M=22016, L=1536) at decode token counts N = 1, 8, 16: "
+             "every kernel of the layer and of the dense layer.  bf16, weights rotated over copies "
+             "larger than the last-level cache.", "",
+             "Counter runs (from the repository root, on one MI355X), one run per counter set:", "", "```"]
+    lines += [cmd for _, cmd in args.run] + ["```", ""]
+    lines += ["Columns are means per launch.  MFMA busy: the derived `MfmaUtil` (SQ_VALU_MFMA_BUSY_CYCLES "
+              "over GRBM_GUI_ACTIVE times the SIMD count).  MFMA flops: SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512, "
+              "against the product's 2·R·C·D.  Bytes: FETCH_SIZE and WRITE_SIZE (KiB) scaled by the "
+              "1 GiB copy of the same run "
+              + ", ".join(f"({c} x {v:.4f})" for c, v in sorted(scale.items())) + ".", "",
+              "| phase | kernel | grid | launches | MFMA busy % | MFMA flops / algorithmic | "
+              "fetch MB | write MB | bytes / algorithmic |", "|---|---|---|---|---|---|---|---|---|"]
+    phase_bytes = collections.defaultdict(float)
+    for (ph, k, grid), ent in table.items():
+        mean = {c: sum(v) / len(v) for c, v in ent.items()}
+        n = max(len(v) for v in ent.values())
+        fl, by = _alg(ph, probe)
+        busy = f"{mean['MfmaUtil']:.1f}" if "MfmaUtil" in mean else ""
+        mops = f"{mean['SQ_INSTS_VALU_MFMA_MOPS_BF16'] * 512 / fl:.3f}" if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in mean else ""
+        fb = mean.get("FETCH_SIZE", 0.0) * 1024 * scale.get("FETCH_SIZE", 0.0)
+        wb = mean.get("WRITE_SIZE", 0.0) * 1024 * scale.get("WRITE_SIZE", 0.0)
+        phase_bytes[ph] += fb + wb
+        fm = f"{fb / 1e6:.1f}" if "FETCH_SIZE" in mean else ""
+        wm = f"{wb / 1e6:.1f}" if "WRITE_SIZE" in mean else ""
+        lines.append(f"| {ph} | `{k}` | {grid} | {n} | {busy} | {mops} | {fm} | {wm} | "
+                     f"{(fb + wb) / by:.3f} |" if fm and wm else
+                     f"| {ph} | `{k}` | {grid} | {n} | {busy} | {mops} | {fm} | {wm} | |")
+    if scale:
+        lines += ["", "Per phase, all kernels of one call (counter bytes over the call's algorithmic bytes: "
+                  "each operand read once, the output written once):", "",
+                  "| phase | counter MB per call | algorithmic MB | ratio |", "|---|---|---|---|"]
+        for ph in probe["phases"]:
+            if ph in phase_bytes:
+                _, by = _alg(ph, probe)
+                lines.append(f"| {ph} | {phase_bytes[ph] / 1e6:.1f} | {by / 1e6:.1f} | "
+                             f"{phase_bytes[ph] / by:.3f} |")
+    open(args.out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="mode", required=True)
@@ -153,8 +248,11 @@ def main():
     b.add_argument("out")
     b.add_argument("cmd_fetch")
     b.add_argument("cmd_write")
+    c = sub.add_parser("counters")
+    c.add_argument("out")
+    c.add_argument("--run", nargs=2, action="append", metavar=("CSV", "CMD"), required=True)
     args = ap.parse_args()
-    stats(args) if args.mode == "stats" else traffic(args)
+    {"stats": stats, "traffic": traffic, "counters": counters}[args.mode](args)
 
 
 if __name__ == "__main__":
