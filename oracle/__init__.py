@@ -25,6 +25,17 @@ from .espace_ref import (  # noqa: F401
     train_backward,
     dense_backward,
 )
+from .mxfp8_ref import (  # noqa: F401
+    e4m3_round,
+    e4m3_decode,
+    e4m3_encode,
+    mx_quantize,
+    mx_scale,
+    mx_dequantize,
+    mx_project,
+    mx_expand,
+    mx_projected_linear,
+)
 from .brute import (  # noqa: F401
     bf_fold,
     bf_project,

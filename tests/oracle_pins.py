@@ -9,6 +9,7 @@ permutation matrices, and with the identities of Theorem 1, Proposition 1
 and Theorem 2.
 """
 import itertools
+import math
 
 import numpy as np
 
@@ -408,6 +409,145 @@ def pin_training_gradients(o):
         assert abs((loss(X, Wp) - loss(X, Wm)) / (2 * h) - dW[m, k]) < 1e-7, ("dW", m, k)
 
 
+# -- MX-FP8 (the low-precision reading of Section 1.1 / Section 5) ------------
+
+def _torch_e4m3_table():
+    """float64 values of the 256 E4M3 bit patterns by torch's float8_e4m3fn
+    (a library the oracle does not use)."""
+    import torch
+    return torch.arange(256, dtype=torch.int32).to(torch.uint8).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+
+
+def pin_e4m3_decode_table(o):
+    """Every E4M3 bit pattern decodes to torch's value (NaN patterns
+    included), and encode inverts decode on all 254 finite patterns."""
+    ref = _torch_e4m3_table()
+    got = o.e4m3_decode(np.arange(256))
+    assert np.array_equal(np.isnan(got), np.isnan(ref)), "e4m3 NaN patterns"
+    fin = ~np.isnan(ref)
+    assert np.array_equal(got[fin], ref[fin]), "e4m3 decode"
+    codes = np.arange(256)[fin]
+    back = o.e4m3_encode(ref[fin])
+    assert np.array_equal(back.astype(np.int64), codes), "e4m3 encode"
+    # closed form: 448 is the largest finite value, 2^-9 the smallest positive one
+    assert np.nanmax(ref) == 448.0 and np.min(ref[fin & (ref > 0)]) == 2.0 ** -9
+
+
+def pin_e4m3_round(o):
+    """Rounding to E4M3 agrees with torch's float32 -> float8_e4m3fn cast on
+    every in-range value of a random sweep, and takes the ties, the
+    saturation and the subnormal steps a reader can check by hand."""
+    import torch
+    rng = _rng(40)
+    v = np.concatenate([rng.standard_normal(20000) * 30, rng.standard_normal(20000) * 1e-2,
+                        rng.uniform(-448, 448, 20000)]).astype(np.float32).astype(np.float64)
+    ref = torch.from_numpy(v.astype(np.float32)).to(torch.float8_e4m3fn).to(torch.float64).numpy()
+    assert np.array_equal(o.e4m3_round(v), ref), "e4m3 rounding vs torch"
+    cases = {1.0625: 1.0, 1.1875: 1.25, 17.0: 16.0, 19.0: 20.0, 2.0 ** -10: 0.0, 3 * 2.0 ** -10: 2.0 ** -8,
+             5 * 2.0 ** -10: 2.0 ** -8, 448.0: 448.0, 460.0: 448.0, 500.0: 448.0, 1e30: 448.0, -1e30: -448.0,
+             0.3: 0.3125, -0.3: -0.3125}
+    for x, want in cases.items():
+        got = float(o.e4m3_round(np.array([x]))[0])
+        assert got == want, f"e4m3_round({x}) = {got}, expected {want}"
+
+
+def _mx_blocks_case(seed):
+    rng = _rng(seed)
+    A = rng.standard_normal((6, 75)) * np.exp(rng.uniform(-12, 12, (6, 1)))
+    A[1, 32:64] = 0.0                         # an all-zero block
+    A[2, :32] *= 1e-30                        # tiny magnitudes
+    A[3, 5] = 2.0 ** 20                       # one large entry dominating its block
+    A[4, 64:] = [2.0 ** k for k in range(-5, 6)]    # powers of two in the ragged tail block
+    return A
+
+
+def pin_mx_quantize(o):
+    """MX-FP8 blocks (32 along the row, ragged tail): the scale byte is the
+    brute-force smallest S with max|v| < 2^(S + 9) (zero blocks: byte 0), every
+    nonzero block's largest element lies in [256, 448], every element is
+    within half an E4M3 step of v / 2^S, and values already on the MX grid
+    come back unchanged."""
+    for seed in (41, 42, 43):
+        A = _mx_blocks_case(seed)
+        q, sb = o.mx_quantize(A)
+        rows, cols = A.shape
+        nb = -(-cols // 32)
+        assert q.shape == A.shape and sb.shape == (rows, nb)
+        for r in range(rows):
+            for b in range(nb):
+                blk = A[r, 32 * b:32 * b + 32]
+                amax = float(np.abs(blk).max())
+                if amax == 0.0:
+                    assert sb[r, b] == 0, "zero block scale"
+                    assert np.all(q[r, 32 * b:32 * b + 32] == 0)
+                    continue
+                S = next(S for S in range(-400, 400) if amax < 2.0 ** (S + 9))
+                assert int(sb[r, b]) == min(max(S + 127, 0), 254), (r, b, int(sb[r, b]), S)
+                Se = int(sb[r, b]) - 127
+                qb = q[r, 32 * b:32 * b + 32]
+                if S + 127 >= 0:
+                    assert 256.0 <= np.abs(qb).max() <= 448.0, (r, b, np.abs(qb).max())
+                for x, y in zip(blk / 2.0 ** Se, qb):
+                    a = abs(x)
+                    step = 2.0 ** -9 if a < 2.0 ** -6 else 2.0 ** (math.floor(math.log2(a)) - 3)
+                    assert abs(min(a, 448.0) - abs(y)) <= step / 2 * (1 + 1e-12), (x, y)
+        deq = o.mx_dequantize(q, sb)
+        q2, sb2 = o.mx_quantize(deq)
+        assert np.array_equal(q2, q) and np.array_equal(sb2, sb), "MX round trip"
+
+
+def _mx_inputs(seed, N, K, L, M):
+    rng = _rng(seed)
+    X = rng.standard_normal((N, K)) * np.exp(rng.uniform(-2, 2, (N, 1)))
+    Pt = _orthonormal(K, L, rng).T.copy()
+    Wf = rng.standard_normal((M, L)) / np.sqrt(L)
+    return o_q(X), o_q(Pt), o_q(Wf)
+
+
+def o_q(A):
+    from oracle import mxfp8_ref
+    return mxfp8_ref.mx_quantize(A)
+
+
+def pin_mx_layer_brute_force(o):
+    """The MX-FP8 layer on tiny shapes: Z and Y equal entry-by-entry exactly
+    rounded loop sums (math.fsum) over the decoded operands, with Z
+    re-quantised in between (Section 2.2, Eq. 3)."""
+    for seed, (N, K, L, M) in enumerate([(3, 40, 33, 5), (2, 64, 7, 3), (4, 70, 64, 9)]):
+        (Xq, Xs), (Pq, Ps), (Wq, Ws) = _mx_inputs(50 + seed, N, K, L, M)
+        Xd, Pd, Wd = o.mx_dequantize(Xq, Xs), o.mx_dequantize(Pq, Ps), o.mx_dequantize(Wq, Ws)
+        Z = o.mx_project(Xq, Xs, Pq, Ps)
+        _close(Z, brute.bf_project(Pd.tolist(), Xd.tolist()), what="mx project")
+        Y, Zq, Zs = o.mx_projected_linear(Xq, Xs, Pq, Ps, Wq, Ws)
+        Zq2, Zs2 = o.mx_quantize(Z)
+        assert np.array_equal(Zq, Zq2) and np.array_equal(Zs, Zs2), "layer re-quantises Z"
+        Zd = o.mx_dequantize(Zq, Zs)
+        _close(Y, brute.bf_expand(Zd.tolist(), Wd.tolist()), what="mx layer")
+        _close(o.mx_expand(Zq, Zs, Wq, Ws), Y, what="mx expand")
+
+
+def pin_mx_block_selection(o):
+    """With P selecting whole 32-blocks of coordinates, Z is exactly the
+    selected decoded columns of X, its re-quantisation returns X's codes and
+    scales for those blocks, and Y is the plain product of those columns with
+    the decoded folded weight."""
+    rng = _rng(60)
+    N, K, M = 5, 128, 7
+    X = rng.standard_normal((N, K)) * np.exp(rng.uniform(-3, 3, (N, K // 32))).repeat(32, axis=1)
+    Xq, Xs = o.mx_quantize(X)
+    sel_blocks = [2, 0]
+    sel = np.concatenate([np.arange(32 * b, 32 * b + 32) for b in sel_blocks])
+    Pt = np.zeros((len(sel), K))
+    Pt[np.arange(len(sel)), sel] = 1.0
+    Pq, Ps = o.mx_quantize(Pt)
+    Wq, Ws = o.mx_quantize(rng.standard_normal((M, len(sel))))
+    Y, Zq, Zs = o.mx_projected_linear(Xq, Xs, Pq, Ps, Wq, Ws)
+    assert np.array_equal(Zq, Xq[:, sel]), "selected codes"
+    assert np.array_equal(Zs, Xs[:, sel_blocks]), "selected scales"
+    ref = o.mx_dequantize(Xq, Xs)[:, sel] @ o.mx_dequantize(Wq, Ws).T
+    assert np.array_equal(Y, ref), "selected product"
+
+
 ALL_PINS = [
     pin_brute_force,
     pin_associativity,
@@ -427,4 +567,9 @@ ALL_PINS = [
     pin_gomse_bound_identity,
     pin_magnitude_order,
     pin_training_gradients,
+    pin_e4m3_decode_table,
+    pin_e4m3_round,
+    pin_mx_quantize,
+    pin_mx_layer_brute_force,
+    pin_mx_block_selection,
 ]

@@ -137,6 +137,72 @@ MUTANTS = {
 }
 
 
+from oracle import mxfp8_ref as MX
+
+
+def _e4m3_ties_away(v):
+    v = np.asarray(v, dtype=np.float64)
+    a = np.minimum(np.abs(v), 448.0)
+    _, e = np.frexp(a)
+    e = np.maximum(e - 1, -6)
+    step = np.ldexp(1.0, e - 3)
+    return np.copysign(np.minimum(np.floor(a / step + 0.5) * step, 448.0), v)
+
+
+def _e4m3_no_clamp(v):
+    v = np.asarray(v, dtype=np.float64)
+    a = np.abs(v)
+    _, e = np.frexp(a)
+    e = np.maximum(e - 1, -6)
+    step = np.ldexp(1.0, e - 3)
+    return np.copysign(np.rint(a / step) * step, v)
+
+
+def _mx_quantize_emax7(A):
+    # S = floor(log2 amax) - 7: elements land in [128, 256), one bit lost
+    q, sb = MX.mx_quantize(np.asarray(A, dtype=np.float64) / 2.0)
+    sb = np.where(sb > 0, sb.astype(np.int64) + 1, 0).clip(0, 254).astype(np.uint8)
+    return MX.e4m3_round(q / 2.0), sb
+
+
+def _mx_quantize_block16(A):
+    A = np.asarray(A, dtype=np.float64)
+    rows, cols = A.shape
+    q = np.zeros_like(A)
+    sb = np.zeros((rows, -(-cols // 32)), np.uint8)
+    for c0 in range(0, cols, 16):
+        qq, ss = MX.mx_quantize(A[:, c0:c0 + 16])
+        q[:, c0:c0 + 16] = qq
+        if c0 % 32 == 0:
+            sb[:, c0 // 32] = ss[:, 0]
+    return q, sb
+
+
+def _mx_layer_no_requant(Xq, Xs, Ptq, Pts, Wfq, Wfs):
+    Z = MX.mx_project(Xq, Xs, Ptq, Pts)
+    Zq, Zs = MX.mx_quantize(Z)
+    return Z @ MX.mx_dequantize(Wfq, Wfs).T, Zq, Zs
+
+
+def _mx_dequantize_no_scale(values, scale_bytes):
+    return np.asarray(values, dtype=np.float64)
+
+
+def _mx_expand_transposed_scales(Zq, Zs, Wfq, Wfs):
+    return MX.mx_dequantize(Zq, Zs) @ (np.asarray(Wfq, float) * MX.mx_scale(Wfs[::-1], Wfq.shape[1])).T
+
+
+MUTANTS.update({
+    "e4m3 ties away from zero": {"e4m3_round": _e4m3_ties_away},
+    "e4m3 without saturation": {"e4m3_round": _e4m3_no_clamp},
+    "MX scale exponent off by one": {"mx_quantize": _mx_quantize_emax7},
+    "MX blocks of 16": {"mx_quantize": _mx_quantize_block16},
+    "MX layer skips re-quantising Z": {"mx_projected_linear": _mx_layer_no_requant},
+    "MX dequantisation ignores scales": {"mx_dequantize": _mx_dequantize_no_scale},
+    "MX expand uses another row's scales": {"mx_expand": _mx_expand_transposed_scales},
+})
+
+
 def _caught(ns):
     for pin in oracle_pins.ALL_PINS:
         try:
