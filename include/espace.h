@@ -61,7 +61,7 @@
 extern "C" {
 #endif
 
-#define ESPACE_ABI_VERSION 6
+#define ESPACE_ABI_VERSION 7
 
 typedef enum {
     ESPACE_F32 = 0,
@@ -90,7 +90,8 @@ typedef enum {
     ESPACE_OP_PCA = 6,         /* espace_principal_components: uses K, L */
     ESPACE_OP_SYMPRODUCT = 7,  /* espace_symmetrized_product: uses K */
     ESPACE_OP_BACKWARD = 8,    /* espace_projected_linear_backward: uses M, K, L, N */
-    ESPACE_OP_DENSE_BACKWARD = 9   /* espace_dense_linear_backward: uses M, K, N */
+    ESPACE_OP_DENSE_BACKWARD = 9,  /* espace_dense_linear_backward: uses M, K, N */
+    ESPACE_OP_PROJECTED_LINEAR_MXFP8 = 10  /* espace_projected_linear_mxfp8: uses L, N */
 } espace_op;
 
 /* Folded weight Wf = W·P (Section 2.2: the paper's PᵀW, "pre-computed before
@@ -261,6 +262,71 @@ espace_status espace_principal_components(const float* C, int64_t ldc,
                                           void* workspace, size_t workspace_bytes,
                                           hipStream_t stream);
 
+/* ---- MX-FP8 layer -------------------------------------------------------------
+ * The paper notes that the activation projection can be carried out in low
+ * precision (Section 1.1) and leaves combining ESPACE with quantisation to
+ * future work (Section 5), without fixing a number format.  This path uses
+ * the OCP Microscaling format MX-FP8, which gfx950's block-scaled MFMA
+ * consumes directly:
+ *  - elements: FP8 E4M3 (exponent bias 7, 3 mantissa bits, subnormals below
+ *    2^-6, largest magnitude 448, no infinities), one byte each;
+ *  - blocks: 32 consecutive elements of a row (the reduction dimension of both
+ *    products) share the scale 2^S, stored as the byte S + 127 (E8M0), with
+ *    S = floor(log2(max |v|)) - 8, the byte clamped to [0, 254] and 0 for a
+ *    block of zeros; an element is v / 2^S rounded to the nearest E4M3 value
+ *    (ties to even), magnitudes above 448 clamped to 448.
+ * An MX-FP8 matrix of R rows and C columns is stored as
+ *     codes  Q [R][ldq]  uint8, ldq >= round_up(C, 128) and a multiple of 16,
+ *                        16-byte aligned; the columns [C, round_up(C, 128))
+ *                        must hold zeros (espace_quantize_mxfp8 and
+ *                        espace_project_mxfp8 write them);
+ *     scales S [R][lds]  uint8, lds >= round_up(C, 128) / 32 and a multiple of
+ *                        4, 4-byte aligned; byte b scales columns [32b, 32b + 32)
+ *                        (the bytes up to round_up(C, 128) / 32 are written).
+ * Both products accumulate in fp32 through the MFMA.
+ * Shapes as for the bf16 layer (1 <= L <= K; M, N >= 0); every code matrix
+ * must span less than 2^31 bytes.  Other conventions (device pointers,
+ * stream order, statuses, no overlap of outputs and inputs) as above. */
+
+/* Quantise a bfloat16 matrix A [R][C] (lda, a multiple of 8) to MX-FP8 along
+ * its rows: the activations X (per token, along K) at run time, the
+ * projection Pt (along K) and the folded weight Wf (along L) once, like the
+ * fold.  Out: Q [R][ldq], S [R][lds]. */
+espace_status espace_quantize_mxfp8(const void* A, int64_t lda, int64_t R, int64_t C,
+                                    void* Q, int64_t ldq, void* S, int64_t lds,
+                                    hipStream_t stream);
+
+/* Projection Z = Pᵀ·X from MX-FP8 operands (Section 2.2, Eq. 3, right
+ * factor), accumulated in fp32 and written in MX-FP8 along L (per token).
+ * In: Pt codes/scales [L][K] (ldpq, ldps), X codes/scales [N][K] (ldxq,
+ * ldxs).  Out: Z codes/scales [N][L] (ldzq, ldzs). */
+espace_status espace_project_mxfp8(const void* Ptq, int64_t ldpq, const void* Pts, int64_t ldps,
+                                   const void* Xq, int64_t ldxq, const void* Xs, int64_t ldxs,
+                                   void* Zq, int64_t ldzq, void* Zs, int64_t ldzs,
+                                   int64_t K, int64_t L, int64_t N, hipStream_t stream);
+
+/* Expansion Y = Wf·Z from MX-FP8 operands (Section 2.2, Eq. 3), fp32
+ * accumulation, Y bfloat16 (round to nearest even).
+ * In: Z codes/scales [N][L] (ldzq, ldzs), Wf codes/scales [M][L] (ldwq,
+ * ldws).  Out: Y [N][M] (ldy, a multiple of 8). */
+espace_status espace_expand_mxfp8(const void* Zq, int64_t ldzq, const void* Zs, int64_t ldzs,
+                                  const void* Wfq, int64_t ldwq, const void* Wfs, int64_t ldws,
+                                  void* Y, int64_t ldy,
+                                  int64_t M, int64_t L, int64_t N, hipStream_t stream);
+
+/* The MX-FP8 layer: espace_project_mxfp8 then espace_expand_mxfp8 with Z in
+ * the workspace (espace_workspace_bytes(ESPACE_OP_PROJECTED_LINEAR_MXFP8, M,
+ * K, L, N, ESPACE_BF16) bytes, 256-byte aligned); computes exactly what the
+ * two calls compute.
+ * In: X, Pt, Wf codes/scales.  Out: Y [N][M] bfloat16 (ldy). */
+espace_status espace_projected_linear_mxfp8(const void* Xq, int64_t ldxq, const void* Xs, int64_t ldxs,
+                                            const void* Ptq, int64_t ldpq, const void* Pts, int64_t ldps,
+                                            const void* Wfq, int64_t ldwq, const void* Wfs, int64_t ldws,
+                                            void* Y, int64_t ldy,
+                                            int64_t M, int64_t K, int64_t L, int64_t N,
+                                            void* workspace, size_t workspace_bytes,
+                                            hipStream_t stream);
+
 /* Workspace bytes needed by `op` for these sizes (0 when none is needed).
  * Arguments an op does not use are ignored (e.g. L for ESPACE_OP_DENSE).
  * Returns SIZE_MAX for invalid sizes. */
@@ -296,8 +362,7 @@ espace_status espace_projected_linear_noalloc(const void* X, int64_t ldx,
                                               espace_dtype dt, hipStream_t stream);
 
 /* Bounded waits.  Some kernels wait for other workgroups of the same launch
- * (the combine of two depth halves of a tile, and the one-launch projected
- * linear layer's wait for its projection).  Every such wait gives up after a
+ * (the combine of two depth halves of a tile).  Every such wait gives up after a
  * limit of polls; the waiting workgroup then writes NaN to the outputs it
  * could not complete (the call's result shows the failure) and adds one to a
  * per-device count.  These waits end within microseconds when the launch runs

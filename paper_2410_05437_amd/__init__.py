@@ -19,6 +19,13 @@ from ._lib import (  # noqa: F401
     OP_PCA,
     OP_SYMPRODUCT,
     OP_PROJECTED_LINEAR,
+    OP_PROJECTED_LINEAR_MXFP8,
+    MXTensor,
+    mx_empty,
+    espace_quantize_mxfp8,
+    espace_project_mxfp8,
+    espace_expand_mxfp8,
+    espace_projected_linear_mxfp8,
     EspaceError,
     espace_autocorrelation_update,
     espace_dense_linear,

@@ -19,7 +19,7 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "espace.h")
 F32 = 0
 BF16 = 1
 (OP_FOLD, OP_PROJECT, OP_EXPAND, OP_PROJECTED_LINEAR, OP_DENSE, OP_AUTOCORR, OP_PCA, OP_SYMPRODUCT, OP_BACKWARD,
- OP_DENSE_BACKWARD) = range(10)
+ OP_DENSE_BACKWARD, OP_PROJECTED_LINEAR_MXFP8) = range(11)
 
 _c_i64 = ctypes.c_int64
 _c_p = ctypes.c_void_p
@@ -49,6 +49,10 @@ _SIGS = {
     "espace_projected_linear_backward": ([_c_p, _c_i64] * 6 + [_c_i64] * 4 + [_c_int, _c_p, _c_sz, _c_p], _c_int),
     "espace_dense_linear_backward": ([_c_p, _c_i64] * 5 + [_c_i64] * 3 + [_c_int, _c_p, _c_sz, _c_p], _c_int),
     "espace_workspace_bytes": ([_c_int, _c_i64, _c_i64, _c_i64, _c_i64, _c_int], _c_sz),
+    "espace_quantize_mxfp8": ([_c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_i64, _c_p, _c_i64, _c_p], _c_int),
+    "espace_project_mxfp8": ([_c_p, _c_i64] * 6 + [_c_i64] * 3 + [_c_p], _c_int),
+    "espace_expand_mxfp8": ([_c_p, _c_i64] * 5 + [_c_i64] * 3 + [_c_p], _c_int),
+    "espace_projected_linear_mxfp8": ([_c_p, _c_i64] * 7 + [_c_i64] * 4 + [_c_p, _c_sz, _c_p], _c_int),
     "espace_status_string": ([_c_int], ctypes.c_char_p),
     "espace_last_error": ([], ctypes.c_char_p),
     "espace_abi_version": ([], _c_int),
@@ -415,3 +419,118 @@ def espace_dense_linear_backward(dY, X, W, dX=None, dW=None, want_dx=True, want_
                                                 _dt(dY), ctypes.c_void_p(ws.data_ptr() if ws is not None else 0),
                                                 wsb, _stream(dY.device)))
     return dX, dW
+
+
+# ---- MX-FP8 ------------------------------------------------------------------
+
+class MXTensor:
+    """An MX-FP8 matrix of `rows` x `cols`: E4M3 codes [rows][ldq] (uint8,
+    ldq >= round_up(cols, 128); the columns past `cols` hold zeros) and E8M0
+    scale bytes [rows][lds] (byte b scales columns 32b .. 32b + 31)."""
+
+    def __init__(self, codes, scales, cols):
+        self.codes = codes
+        self.scales = scales
+        self.cols = int(cols)
+
+    @property
+    def rows(self):
+        return self.codes.shape[0]
+
+    @property
+    def device(self):
+        return self.codes.device
+
+
+def mx_empty(rows, cols, device):
+    """Uninitialised MX-FP8 matrix with the smallest leading dimensions."""
+    cp = (cols + 127) // 128 * 128
+    return MXTensor(torch.empty((rows, cp), dtype=torch.uint8, device=device),
+                    torch.empty((rows, cp // 32), dtype=torch.uint8, device=device), cols)
+
+
+def _mx(m, name, rows=None, cols=None):
+    """(codes pointer, ldq, scales pointer, lds) of an MXTensor."""
+    if not isinstance(m, MXTensor):
+        raise TypeError(f"{name} must be an MXTensor")
+    for t, what in ((m.codes, "codes"), (m.scales, "scales")):
+        if t.dtype != torch.uint8 or t.dim() != 2 or (t.stride(1) != 1 and t.shape[1] > 1):
+            raise ValueError(f"{name} {what}: a 2-D uint8 tensor with unit column stride")
+    if m.scales.shape[0] != m.rows or m.scales.device != m.device:
+        raise ValueError(f"{name}: codes and scales must share rows and device")
+    if rows is not None and m.rows != rows:
+        raise ValueError(f"{name} has {m.rows} rows, expected {rows}")
+    if cols is not None and m.cols != cols:
+        raise ValueError(f"{name} has {m.cols} columns, expected {cols}")
+    pq, ldq = _mat(m.codes, name + " codes")
+    ps, lds = _mat(m.scales, name + " scales")
+    return pq, ldq, ps, lds
+
+
+def espace_quantize_mxfp8(A, out=None):
+    """MX-FP8 of a bfloat16 matrix A [R][C] along its rows -> MXTensor."""
+    if A.dtype != torch.bfloat16:
+        raise TypeError("A must be bfloat16")
+    R, C = A.shape
+    out = mx_empty(R, C, A.device) if out is None else out
+    pq, ldq, ps, lds = _mx(out, "out", R, C)
+    if out.device != A.device:
+        raise ValueError("out and A must share a device")
+    pa, lda = _mat(A, "A")
+    with torch.cuda.device(A.device):
+        _check(lib.espace_quantize_mxfp8(pa, lda, R, C, pq, ldq, ps, lds, _stream(A.device)))
+    return out
+
+
+def espace_project_mxfp8(Pt, X, Z=None):
+    """Z = Pᵀ·X from MX-FP8 Pt [L][K] and X [N][K] -> MX-FP8 Z [N][L]."""
+    L, K, N = Pt.rows, Pt.cols, X.rows
+    Z = mx_empty(N, L, X.device) if Z is None else Z
+    a = _mx(Pt, "Pt")
+    b = _mx(X, "X", cols=K)
+    c = _mx(Z, "Z", N, L)
+    if len({Pt.device, X.device, Z.device}) != 1:
+        raise ValueError("operands must share a device")
+    with torch.cuda.device(X.device):
+        _check(lib.espace_project_mxfp8(*a, *b, *c, K, L, N, _stream(X.device)))
+    return Z
+
+
+def espace_expand_mxfp8(Z, Wf, Y=None):
+    """Y = Wf·Z from MX-FP8 Z [N][L] and Wf [M][L] -> bfloat16 Y [N][M]."""
+    N, L, M = Z.rows, Z.cols, Wf.rows
+    a = _mx(Z, "Z")
+    b = _mx(Wf, "Wf", cols=L)
+    if Y is None:
+        Y = padded_empty(N, M, torch.bfloat16, Z.device)
+    if tuple(Y.shape) != (N, M) or Y.dtype != torch.bfloat16 or Y.device != Z.device:
+        raise ValueError(f"Y must be a bfloat16 {N}x{M} tensor on {Z.device}")
+    if Wf.device != Z.device:
+        raise ValueError("operands must share a device")
+    py, ldy = _mat(Y, "Y")
+    with torch.cuda.device(Z.device):
+        _check(lib.espace_expand_mxfp8(*a, *b, py, ldy, M, L, N, _stream(Z.device)))
+    return Y
+
+
+def espace_projected_linear_mxfp8(X, Pt, Wf, Y=None, workspace=None):
+    """Y = Wf·(Pᵀ·X) from MX-FP8 X [N][K], Pt [L][K], Wf [M][L] -> bfloat16
+    Y [N][M], Z in MX-FP8 in the workspace."""
+    N, K, L, M = X.rows, X.cols, Pt.rows, Wf.rows
+    a = _mx(X, "X")
+    b = _mx(Pt, "Pt", cols=K)
+    c = _mx(Wf, "Wf", cols=L)
+    if len({X.device, Pt.device, Wf.device}) != 1:
+        raise ValueError("operands must share a device")
+    if Y is None:
+        Y = padded_empty(N, M, torch.bfloat16, X.device)
+    if tuple(Y.shape) != (N, M) or Y.dtype != torch.bfloat16 or Y.device != X.device:
+        raise ValueError(f"Y must be a bfloat16 {N}x{M} tensor on {X.device}")
+    ws, wsb = _ws(workspace, espace_workspace_bytes(OP_PROJECTED_LINEAR_MXFP8, M, K, L, N, torch.bfloat16),
+                  X.device)
+    py, ldy = _mat(Y, "Y")
+    with torch.cuda.device(X.device):
+        _check(lib.espace_projected_linear_mxfp8(*a, *b, *c, py, ldy, M, K, L, N,
+                                                 ctypes.c_void_p(ws.data_ptr() if ws is not None else 0), wsb,
+                                                 _stream(X.device)))
+    return Y

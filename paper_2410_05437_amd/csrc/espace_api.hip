@@ -346,6 +346,19 @@ size_t ws_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int64_t N, espace
     return SIZE_MAX;
 }
 
+// ---- MX-FP8 sizes -------------------------------------------------------------
+
+// Columns of an MX-FP8 matrix as stored: whole 128-column steps of the MFMA.
+int64_t mx_cols(int64_t cols) { return (cols + 127) / 128 * 128; }
+
+// Workspace of the MX-FP8 layer: Z's codes [N][mx_cols(L)] and scale bytes
+// [N][mx_cols(L) / 32].
+size_t mx_ws_bytes(int64_t M, int64_t L, int64_t N) {
+    if (!N || !M) return 0;
+    return align_ws((size_t)N * mx_cols(L)) + align_ws((size_t)N * mx_cols(L) / 32);
+}
+
+
 // ---- validation -------------------------------------------------------------
 
 struct Range { const char* name; uintptr_t lo, hi; };
@@ -401,6 +414,28 @@ espace_status check_workspace(void* ws, size_t have, size_t need) {
     if (have < need) return fail(ESPACE_ERR_WORKSPACE, "workspace of %zu bytes needed, got %zu", need, have);
     if ((uintptr_t)ws % kWsAlign) return fail(ESPACE_ERR_ALIGN, "workspace not 256-byte aligned");
     return ESPACE_OK;
+}
+
+// An MX-FP8 operand: codes [rows][ldq] and scale bytes [rows][lds] covering
+// mx_cols(cols) columns, each spanning less than 2^31 bytes.
+espace_status check_mx(const char* name, const void* Q, int64_t ldq, const void* S, int64_t lds, int64_t rows,
+                       int64_t cols) {
+    if (!Q || !S) return fail(ESPACE_ERR_NULL, "%s: codes or scales NULL", name);
+    const int64_t cp = mx_cols(cols);
+    if (ldq < cp || lds < cp / 32)
+        return fail(ESPACE_ERR_SHAPE, "%s: leading dimensions %lld (codes) / %lld (scales) below %lld / %lld", name,
+                    (long long)ldq, (long long)lds, (long long)cp, (long long)(cp / 32));
+    if (ldq % 16 || lds % 4)
+        return fail(ESPACE_ERR_ALIGN, "%s: leading dimensions must be multiples of 16 (codes) and 4 (scales)", name);
+    if ((uintptr_t)Q % 16 || (uintptr_t)S % 4)
+        return fail(ESPACE_ERR_ALIGN, "%s: codes not 16-byte or scales not 4-byte aligned", name);
+    if (rows * ldq >= ((int64_t)1 << 31) || rows * lds >= ((int64_t)1 << 31))
+        return fail(ESPACE_ERR_SHAPE, "%s spans 2^31 bytes or more", name);
+    return ESPACE_OK;
+}
+
+Range byte_range(const char* name, const void* p, int64_t rows, int64_t ld) {
+    return Range{name, (uintptr_t)p, (uintptr_t)p + (uintptr_t)(rows * ld)};
 }
 
 std::mutex g_dev_mu;
@@ -522,6 +557,34 @@ espace_status noalloc_scratch(void** out) {
 
 }  // namespace
 
+// The MX-FP8 products after validation.
+espace_status mx_project_launch(const void* Ptq, int64_t ldpq, const void* Pts, int64_t ldps, const void* Xq,
+                                int64_t ldxq, const void* Xs, int64_t ldxs, void* Zq, int64_t ldzq, void* Zs,
+                                int64_t ldzs, int64_t K, int64_t L, int64_t N, hipStream_t stream) {
+    espace::MxGemmArgs a{};
+    a.T = (const uint8_t*)Xq; a.ldt = ldxq; a.Ts = (const uint8_t*)Xs; a.ldts = ldxs;
+    a.W = (const uint8_t*)Ptq; a.ldw = ldpq; a.Ws = (const uint8_t*)Pts; a.ldws = ldps;
+    a.out = Zq; a.ldo = ldzq; a.outs = (uint8_t*)Zs; a.ldos = ldzs;
+    a.R = (int)N; a.C = (int)L; a.D = (int)K; a.cpad = (int)mx_cols(L);
+    const hipError_t e = espace::launch_gemm_mx(a, 1, device_cus(), stream);
+    if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "MX-FP8 projection launch: %s", hipGetErrorString(e));
+    return ESPACE_OK;
+}
+
+espace_status mx_expand_launch(const void* Zq, int64_t ldzq, const void* Zs, int64_t ldzs, const void* Wfq,
+                               int64_t ldwq, const void* Wfs, int64_t ldws, void* Y, int64_t ldy, int64_t M,
+                               int64_t L, int64_t N, hipStream_t stream) {
+    espace::MxGemmArgs a{};
+    a.T = (const uint8_t*)Zq; a.ldt = ldzq; a.Ts = (const uint8_t*)Zs; a.ldts = ldzs;
+    a.W = (const uint8_t*)Wfq; a.ldw = ldwq; a.Ws = (const uint8_t*)Wfs; a.ldws = ldws;
+    a.out = Y; a.ldo = ldy;
+    a.R = (int)N; a.C = (int)M; a.D = (int)L; a.cpad = (int)mx_cols(M);
+    const hipError_t e = espace::launch_gemm_mx(a, 0, device_cus(), stream);
+    if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "MX-FP8 expansion launch: %s", hipGetErrorString(e));
+    return ESPACE_OK;
+}
+
+
 extern "C" {
 
 int espace_abi_version(void) { return ESPACE_ABI_VERSION; }
@@ -578,6 +641,11 @@ size_t espace_workspace_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int
         if (M < 0 || N < 0 || K < 1 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return SIZE_MAX;
         if (hl && (L < 1 || L > K)) return SIZE_MAX;
         return ws_bytes(op, M, K, hl ? L : 0, N, dt);
+    }
+    if (op == ESPACE_OP_PROJECTED_LINEAR_MXFP8) {
+        if (M < 0 || N < 0 || K < 1 || M > kMaxDim || N > kMaxDim || K > kMaxDim || L < 1 || L > K)
+            return SIZE_MAX;
+        return mx_ws_bytes(M, L, N);
     }
     const bool has_L = op != ESPACE_OP_DENSE;
     int64_t Kc = K;
@@ -903,6 +971,87 @@ espace_status espace_principal_components(const float* C, int64_t ldc, void* Pt,
     const hipError_t e = espace::launch_principal_components(C, ldc, (int)K, (int)L, by_magnitude != 0, Pt, ldp,
                                                              dt == ESPACE_F32, eigenvalues, info, workspace, stream);
     if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "principal components: %s", hipGetErrorString(e));
+    return ok();
+}
+
+espace_status espace_quantize_mxfp8(const void* A, int64_t lda, int64_t R, int64_t C, void* Q, int64_t ldq, void* S,
+                                    int64_t lds, hipStream_t stream) {
+    if (R < 0 || C < 1 || R > kMaxDim || C > kMaxDim)
+        return fail(ESPACE_ERR_SHAPE, "need R >= 0 and C >= 1 (R=%lld, C=%lld)", (long long)R, (long long)C);
+    if (R == 0) return ok();
+    ESPACE_TRY(check_mat("A", A, R, C, lda, ESPACE_BF16));
+    ESPACE_TRY(check_mx("Q/S", Q, ldq, S, lds, R, C));
+    const Range ar = mat_range("A", A, R, lda, ESPACE_BF16);
+    const Range qr = byte_range("Q", Q, R, ldq), sr = byte_range("S", S, R, lds);
+    const Range for_q[] = {ar, sr};
+    ESPACE_TRY(check_alias(qr, for_q, 2));
+    ESPACE_TRY(check_alias(sr, &ar, 1));
+    ESPACE_TRY(check_device());
+    const hipError_t e = espace::launch_mx_quantize((const uint16_t*)A, lda, (int)R, (int)C, (uint8_t*)Q, ldq,
+                                                    (uint8_t*)S, lds, stream);
+    if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "MX-FP8 quantisation launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
+espace_status espace_project_mxfp8(const void* Ptq, int64_t ldpq, const void* Pts, int64_t ldps, const void* Xq,
+                                   int64_t ldxq, const void* Xs, int64_t ldxs, void* Zq, int64_t ldzq, void* Zs,
+                                   int64_t ldzs, int64_t K, int64_t L, int64_t N, hipStream_t stream) {
+    ESPACE_TRY(check_dims(0, K, L, N, true));
+    if (N == 0) return ok();
+    ESPACE_TRY(check_mx("Pt", Ptq, ldpq, Pts, ldps, L, K));
+    ESPACE_TRY(check_mx("X", Xq, ldxq, Xs, ldxs, N, K));
+    ESPACE_TRY(check_mx("Z", Zq, ldzq, Zs, ldzs, N, L));
+    const Range ins[] = {byte_range("Pt codes", Ptq, L, ldpq), byte_range("Pt scales", Pts, L, ldps),
+                         byte_range("X codes", Xq, N, ldxq), byte_range("X scales", Xs, N, ldxs),
+                         byte_range("Z scales", Zs, N, ldzs)};
+    ESPACE_TRY(check_alias(byte_range("Z codes", Zq, N, ldzq), ins, 5));
+    ESPACE_TRY(check_alias(byte_range("Z scales", Zs, N, ldzs), ins, 4));
+    ESPACE_TRY(check_device());
+    ESPACE_TRY(mx_project_launch(Ptq, ldpq, Pts, ldps, Xq, ldxq, Xs, ldxs, Zq, ldzq, Zs, ldzs, K, L, N, stream));
+    return ok();
+}
+
+espace_status espace_expand_mxfp8(const void* Zq, int64_t ldzq, const void* Zs, int64_t ldzs, const void* Wfq,
+                                  int64_t ldwq, const void* Wfs, int64_t ldws, void* Y, int64_t ldy, int64_t M,
+                                  int64_t L, int64_t N, hipStream_t stream) {
+    ESPACE_TRY(check_dims(M, L, L, N, true));
+    if (M == 0 || N == 0) return ok();
+    ESPACE_TRY(check_mx("Z", Zq, ldzq, Zs, ldzs, N, L));
+    ESPACE_TRY(check_mx("Wf", Wfq, ldwq, Wfs, ldws, M, L));
+    ESPACE_TRY(check_mat("Y", Y, N, M, ldy, ESPACE_BF16));
+    const Range ins[] = {byte_range("Z codes", Zq, N, ldzq), byte_range("Z scales", Zs, N, ldzs),
+                         byte_range("Wf codes", Wfq, M, ldwq), byte_range("Wf scales", Wfs, M, ldws)};
+    ESPACE_TRY(check_alias(mat_range("Y", Y, N, ldy, ESPACE_BF16), ins, 4));
+    ESPACE_TRY(check_device());
+    ESPACE_TRY(mx_expand_launch(Zq, ldzq, Zs, ldzs, Wfq, ldwq, Wfs, ldws, Y, ldy, M, L, N, stream));
+    return ok();
+}
+
+espace_status espace_projected_linear_mxfp8(const void* Xq, int64_t ldxq, const void* Xs, int64_t ldxs,
+                                            const void* Ptq, int64_t ldpq, const void* Pts, int64_t ldps,
+                                            const void* Wfq, int64_t ldwq, const void* Wfs, int64_t ldws, void* Y,
+                                            int64_t ldy, int64_t M, int64_t K, int64_t L, int64_t N, void* workspace,
+                                            size_t workspace_bytes, hipStream_t stream) {
+    ESPACE_TRY(check_dims(M, K, L, N, true));
+    if (M == 0 || N == 0) return ok();
+    ESPACE_TRY(check_mx("X", Xq, ldxq, Xs, ldxs, N, K));
+    ESPACE_TRY(check_mx("Pt", Ptq, ldpq, Pts, ldps, L, K));
+    ESPACE_TRY(check_mx("Wf", Wfq, ldwq, Wfs, ldws, M, L));
+    ESPACE_TRY(check_mat("Y", Y, N, M, ldy, ESPACE_BF16));
+    const size_t need = mx_ws_bytes(M, L, N);
+    ESPACE_TRY(check_workspace(workspace, workspace_bytes, need));
+    const Range ins[] = {byte_range("X codes", Xq, N, ldxq), byte_range("X scales", Xs, N, ldxs),
+                         byte_range("Pt codes", Ptq, L, ldpq), byte_range("Pt scales", Pts, L, ldps),
+                         byte_range("Wf codes", Wfq, M, ldwq), byte_range("Wf scales", Wfs, M, ldws),
+                         Range{"workspace", (uintptr_t)workspace, (uintptr_t)workspace + workspace_bytes}};
+    ESPACE_TRY(check_alias(mat_range("Y", Y, N, ldy, ESPACE_BF16), ins, 7));
+    ESPACE_TRY(check_alias(ins[6], ins, 6));
+    ESPACE_TRY(check_device());
+    const int64_t ldzq = mx_cols(L), ldzs = mx_cols(L) / 32;
+    unsigned char* Zq = static_cast<unsigned char*>(workspace);
+    unsigned char* Zs = Zq + align_ws((size_t)N * ldzq);
+    ESPACE_TRY(mx_project_launch(Ptq, ldpq, Pts, ldps, Xq, ldxq, Xs, ldxs, Zq, ldzq, Zs, ldzs, K, L, N, stream));
+    ESPACE_TRY(mx_expand_launch(Zq, ldzq, Zs, ldzs, Wfq, ldwq, Wfs, ldws, Y, ldy, M, L, N, stream));
     return ok();
 }
 

@@ -110,4 +110,25 @@ hipError_t launch_symmetrized_product(const float* A, int64_t lda, const float* 
                                       int64_t ldc, int K, float alpha, float beta, void* workspace,
                                       hipStream_t stream);
 
+// ---- MX-FP8 products (gemm_mxfp8.hip) ----------------------------------------
+// out[r][c] = sum_d T[r][d]·W[c][d] over MX-FP8 operands (codes with zero
+// padding up to round_up(D, 128), one E8M0 scale byte per 32 along d).
+struct MxGemmArgs {
+    const uint8_t* T;  int64_t ldt;     // token-side codes [R][ldt]
+    const uint8_t* Ts; int64_t ldts;    // its scale bytes [R][ldts]
+    const uint8_t* W;  int64_t ldw;     // weight-side codes [C][ldw]
+    const uint8_t* Ws; int64_t ldws;    // its scale bytes [C][ldws]
+    void* out;         int64_t ldo;     // bf16 Y [R][ldo], or MX-FP8 codes [R][ldo]
+    uint8_t* outs;     int64_t ldos;    // MX-FP8 output: scale bytes [R][ldos]
+    int R, C, D;
+    int cpad;                           // MX-FP8 output: columns written, round_up(C, 128)
+};
+// Tile of the MX GEMM for R x C outputs (0: 256 x 256, 1: 256 x 128, 2: 128 x 128).
+int mx_gemm_tile(int R, int C, int cus);
+// out_mx: write MX-FP8 (codes and scales along the columns) instead of bf16.
+// hipErrorInvalidValue when an operand spans 2^31 bytes or more.
+hipError_t launch_gemm_mx(const MxGemmArgs& a, int out_mx, int cus, hipStream_t stream);
+hipError_t launch_mx_quantize(const uint16_t* A, int64_t lda, int R, int C, uint8_t* Q, int64_t ldq, uint8_t* S,
+                              int64_t lds, hipStream_t stream);
+
 }  // namespace espace

@@ -22,10 +22,11 @@ def test_exports_every_declared_function():
         "espace_last_error", "espace_abi_version", "espace_autocorrelation_update",
         "espace_principal_components", "espace_symmetrized_product", "espace_projected_linear_backward",
         "espace_dense_linear_backward", "espace_wait_timeouts", "espace_set_wait_limit",
-        "espace_projected_linear_noalloc"}
+        "espace_projected_linear_noalloc", "espace_quantize_mxfp8", "espace_project_mxfp8",
+        "espace_expand_mxfp8", "espace_projected_linear_mxfp8"}
     for n in names:
         assert hasattr(L, n)
-    assert E.ABI_VERSION == 6
+    assert E.ABI_VERSION == 7
 
 
 def _fold(W=P16, ldw=64, Pt=P16b, ldp=64, Wf=P16c, ldwf=16, M=32, K=64, Lc=16, dt=1,
@@ -254,3 +255,52 @@ def test_noalloc_rejects_sizes_beyond_its_scratch():
     assert s in (7, 8)
     assert L.espace_projected_linear_noalloc(NULL, 64, P16b, 64, P16c, 16, ctypes.c_void_p(0x60000000), 32,
                                              32, 64, 16, 8, 1, NULL) == 1
+
+
+# MX-FP8 operands: codes [rows][ldq] (ldq >= round_up(cols, 128), % 16), scales
+# [rows][lds] (lds >= round_up(cols, 128) / 32, % 4)
+Q1, S1 = ctypes.c_void_p(0x1000000), ctypes.c_void_p(0x2000000)
+Q2, S2 = ctypes.c_void_p(0x3000000), ctypes.c_void_p(0x4000000)
+Q3, S3 = ctypes.c_void_p(0x5000000), ctypes.c_void_p(0x6000000)
+YM = ctypes.c_void_p(0x7000000)
+WSM = ctypes.c_void_p(0x8000000)
+
+
+def _mxl(Xq=Q1, ldxq=256, Xs=S1, ldxs=8, Pq=Q2, ldpq=256, Ps=S2, ldps=8, Wq=Q3, ldwq=128, Ws=S3, ldws=4,
+         Y=YM, ldy=32, M=32, K=200, Lc=100, N=8, ws=WSM, wsb=1 << 20):
+    return L.espace_projected_linear_mxfp8(Xq, ldxq, Xs, ldxs, Pq, ldpq, Ps, ldps, Wq, ldwq, Ws, ldws, Y, ldy,
+                                           M, K, Lc, N, ws, wsb, NULL)
+
+
+def _mxq(A=P16, lda=208, R=8, C=200, Q=Q1, ldq=256, S=S1, lds=8):
+    return L.espace_quantize_mxfp8(A, lda, R, C, Q, ldq, S, lds, NULL)
+
+
+def test_mxfp8_validation_errors():
+    assert _mxq(A=NULL) == 1
+    assert _mxq(S=NULL) == 1
+    assert _mxq(C=0) == 2
+    assert _mxq(ldq=240) == 2                           # codes below round_up(200, 128)
+    assert _mxq(lds=4) == 2                             # scales below 256 / 32
+    assert _mxq(ldq=264) == 3                           # codes ld % 16
+    assert _mxq(lds=10) == 3                            # scales ld % 4
+    assert _mxq(Q=ctypes.c_void_p(0x1000008)) == 3      # codes alignment
+    assert _mxq(S=ctypes.c_void_p(0x2000002)) == 3      # scales alignment
+    assert _mxq(Q=ctypes.c_void_p(0x10000 + 256)) == 5  # codes over A
+    assert _mxq(R=1 << 24, ldq=256) == 2                # codes span 2^32 bytes
+    assert _mxl(Lc=201) == 2                            # L > K
+    assert _mxl(ldwq=112) == 2                          # Wf codes below round_up(100, 128)
+    assert _mxl(ldy=36) == 3                            # Y ld % 8
+    assert _mxl(ws=NULL, wsb=0) == 6                    # workspace missing
+    assert _mxl(wsb=64) == 6                            # workspace too small
+    assert _mxl(Y=ctypes.c_void_p(0x1000000 + 512)) == 5   # Y over X's codes
+    assert _mxl(ws=Q2) == 5                             # workspace over Pt's codes
+    assert L.espace_workspace_bytes(10, 32, 200, 100, 8, 1) == 1024 + 256   # Z codes 8 x 128, scales 8 x 4
+    assert L.espace_workspace_bytes(10, 32, 200, 201, 8, 1) == ctypes.c_size_t(-1).value
+
+
+def test_mxfp8_empty_and_device():
+    assert _mxl(N=0, Xq=NULL, Xs=NULL, Y=NULL, ws=NULL, wsb=0) == 0
+    assert _mxq(R=0, A=NULL, Q=NULL, S=NULL) == 0
+    assert _mxq() in (7, 8), L.espace_last_error()
+    assert _mxl() in (7, 8), L.espace_last_error()
