@@ -29,6 +29,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 ROTATE_BYTES = 600 << 20    # > 2x the 256 MB last-level cache
 COPY_PROBE_BYTES = 1 << 30  # calibration copy for the traffic counters
@@ -57,6 +58,7 @@ def parse():
     ap.add_argument("--no-calibration", action="store_true")
     ap.add_argument("--no-training", action="store_true")
     ap.add_argument("--no-workloads", action="store_true")
+    ap.add_argument("--no-mxfp8", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--kernel-probe", action="store_true",
@@ -396,6 +398,9 @@ def main():
     if not args.no_workloads:
         detail["workloads"] = workload_lines(E, acc, dev, stream, args)
         note("workload lines done")
+    if not args.no_mxfp8:
+        detail["mxfp8"] = mxfp8_lines(E, acc, dev, stream, args, ms)
+        note("MX-FP8 lines done")
 
     cpu = None
     if not args.no_cpu:
@@ -515,6 +520,64 @@ def workload_lines(E, acc, dev, stream, args):
             "ideal_speedup": round(acc.ideal_speedup(K, M, L), 3),
             "rotating_copies": t["copies"],
         }
+    return out
+
+
+# layers of the MX-FP8 lines: (name, K, M, L, N)
+MXFP8_LAYERS = [
+    ("llama2_7b_qkv", 4096, 12288, 1536, 4096),
+    ("llama2_7b_ffn_upgate", 4096, 22016, 1536, 4096),
+    ("llama2_7b_ffn_down", 11008, 4096, 1536, 4096),
+]
+
+
+def mxfp8_lines(E, acc, dev, stream, args, bf16_ms_qkv):
+    """The MX-FP8 layer (E4M3 elements, E8M0 scale per 32 along the reduction
+    dimension, both products on the block-scaled MFMA) on the Llama2-7B
+    prefill layers: µs per layer with the weights quantised once, the
+    run-time quantisation of X timed apart and together, TFLOP/s against the
+    dense fp8 peak, and the ratio to the bf16 layer.  Random bf16 operands of
+    the layer's shape (the parity tests cover these shapes against the
+    oracle), rotated over copies larger than the last-level cache."""
+    import torch
+    bf = torch.bfloat16
+    out = {}
+    n = max(3, args.steps // 5)
+    for name, K, M, L, N in MXFP8_LAYERS:
+        X0 = _rand_mat(E, N, K, 1.0, dev)
+        Pt0 = _rand_mat(E, L, K, K ** -0.5, dev)
+        Wf0 = _rand_mat(E, M, L, K ** -0.5, dev)
+        R = copies(N * K + L * K + M * L)
+        Xr = [X0] + [clone_padded(X0) for _ in range(R - 1)]
+        Xq = [E.espace_quantize_mxfp8(x) for x in Xr]
+        Pq = [E.espace_quantize_mxfp8(Pt0) for _ in range(R)]
+        Wq = [E.espace_quantize_mxfp8(Wf0) for _ in range(R)]
+        Y = E.padded_empty(N, M, bf, dev)
+        ws = torch.empty(E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR_MXFP8, M, K, L, N, bf),
+                         dtype=torch.uint8, device=dev)
+        Xo = E.mx_empty(N, K, dev)
+        ms = time_calls(lambda i: E.espace_projected_linear_mxfp8(Xq[i], Pq[i], Wq[i], Y, ws), R, n, 2, stream)
+        ms_q = time_calls(lambda i: E.espace_quantize_mxfp8(Xr[i], Xo), R, n, 2, stream)
+
+        def with_quant(i):
+            E.espace_quantize_mxfp8(Xr[i], Xo)
+            E.espace_projected_linear_mxfp8(Xo, Pq[i], Wq[i], Y, ws)
+
+        ms_t = time_calls(with_quant, R, n, 2, stream)
+        tf = acc.projected_flops(K, M, L, N) / (ms * 1e-3) / 1e12
+        out[name] = {
+            "K": K, "M": M, "L": L, "N": N,
+            "us_per_layer": round(ms * 1e3, 1),
+            "tflops": round(tf, 1),
+            "fp8_mfma_frac": round(tf / PEAK_FP8_TFLOPS, 4),
+            "quantize_x_us": round(ms_q * 1e3, 1),
+            "us_with_quantize_x": round(ms_t * 1e3, 1),
+            "rotating_copies": R,
+        }
+        if name == "llama2_7b_qkv":
+            out[name]["speedup_vs_bf16_layer"] = round(bf16_ms_qkv / ms, 3)
+        del Xr, Xq, Pq, Wq, Y, ws, Xo, X0, Pt0, Wf0
+        torch.cuda.empty_cache()
     return out
 
 
