@@ -20,8 +20,6 @@
 // eight passes (kept there from five passes on: at eight passes the register
 // form needs twice the registers and was slower, e.g. 34.7 against 33.6 µs
 // on a 22016 x 4096 weight at one token).
-#include <cstdlib>
-
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -273,13 +271,7 @@ bool gemv_supported(int R, int D) {
 
 hipError_t launch_gemv_tn_bf16(const GemmArgs& g, hipStream_t stream) {
     if (!gemv_supported(g.R, g.D) || g.Cc < 1) return hipErrorInvalidValue;
-    // ESPACE_GEMV_WAVES=<n> overrides the number of waves the rows are spread over (tuning)
-    static const int forced = [] {
-        const char* e = std::getenv("ESPACE_GEMV_WAVES");
-        return e ? std::atoi(e) : 0;
-    }();
-    const int target = forced > 0 ? forced
-                       : (gv_passes(g.D) > 4 && g.R == 1) ? GV_TARGET_WAVES_LONG1 : GV_TARGET_WAVES;
+    const int target = (gv_passes(g.D) > 4 && g.R == 1) ? GV_TARGET_WAVES_LONG1 : GV_TARGET_WAVES;
     int rows_per_wave = (g.Cc + target - 1) / target;
     if (rows_per_wave < 1) rows_per_wave = 1;
     return gv_tokens(g.R) == 1 ? launch_nt<1>(g, rows_per_wave, stream) : launch_nt<2>(g, rows_per_wave, stream);

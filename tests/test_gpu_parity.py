@@ -530,3 +530,69 @@ def test_prefill_layer_shapes(E, shape):
         elif fill == "random":
             ws.copy_(torch.randint(0, 256, (need,), dtype=torch.uint8, generator=gen))
         assert torch.equal(E.espace_projected_linear(X, Pt, Wf, workspace=ws), Y), fill
+
+
+# (K, M, L, N) of decode layers on the whole-row kernels: one and two tokens,
+# Wf rows of one to eight 512-element passes, projection depths with a
+# partial block of passes
+DECODE_LAYER_SHAPES = [(4096, 22016, 1536, 1), (4096, 12288, 1536, 2), (11008, 4096, 1536, 1),
+                       (6144, 24576, 3686, 1), (4500, 3001, 2458, 2), (700, 1234, 520, 2), (64, 17, 8, 1)]
+
+
+@pytest.mark.parametrize("shape", DECODE_LAYER_SHAPES, ids=lambda s: "K%d_M%d_L%d_N%d" % s)
+def test_decode_layer_shapes(E, shape):
+    """The decode layer against the oracle on every output, equal bitwise to
+    the projection followed by the expansion, and bitwise the same whatever
+    its workspace held before (zeros, all ones, random bytes, the previous
+    call's Z)."""
+    dev = need_gpu()
+    K, M, L, N = shape
+    inp = _inputs(K, M, L, N, "bf16", seed=90)
+    X, Pt, W = _dev_inputs(inp, dev)
+    Wf = E.espace_fold_weights(W, Pt)
+    Y = E.espace_projected_linear(X, Pt, Wf, out_mat(N, M, "bf16", dev))
+    Ye = E.espace_expand(E.espace_project(Pt, X), Wf)
+    torch.cuda.synchronize()
+    assert torch.equal(Y, Ye), "layer != project then expand"
+    Y64, B = _layer_ref(inp)
+    parity.check(host64(Y), Y64, B, TOL["bf16"], "decode layer")
+    assert np.isnan(padding(Y)).all()
+    need = E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, M, K, L, N, torch.bfloat16)
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    gen = torch.Generator(device="cpu").manual_seed(9)
+    for fill in ["zeros", "ones", "random", "keep", "keep"]:
+        if fill == "zeros":
+            ws.zero_()
+        elif fill == "ones":
+            ws.fill_(255)
+        elif fill == "random":
+            ws.copy_(torch.randint(0, 256, (need,), dtype=torch.uint8, generator=gen))
+        assert torch.equal(E.espace_projected_linear(X, Pt, Wf, workspace=ws), Y), fill
+
+
+def test_decode_layer_under_graph_replay(E):
+    """The decode layer captured in a HIP graph and replayed with new tokens
+    copied in between: every replay equals the eager call bitwise."""
+    dev = need_gpu()
+    K, M, L, N = 4096, 12288, 1536, 1
+    inps = [_inputs(K, M, L, N, "bf16", seed=95 + i) for i in range(2)]
+    X, Pt, W = _dev_inputs(inps[0], dev)
+    Wf = E.espace_fold_weights(W, Pt)
+    Y = out_mat(N, M, "bf16", dev)
+    ws = torch.empty(E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, M, K, L, N, torch.bfloat16),
+                     dtype=torch.uint8, device=dev)
+    E.espace_projected_linear(X, Pt, Wf, Y, ws)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        E.espace_projected_linear(X, Pt, Wf, Y, ws)
+    torch.cuda.synchronize()
+    for rep in range(6):
+        X.copy_(dev_mat(inps[rep % 2].X_s, "bf16", dev))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = Y.clone()
+        ref = E.espace_projected_linear(X, Pt, Wf)
+        torch.cuda.synchronize()
+        assert torch.equal(got, ref), rep
