@@ -7,7 +7,10 @@ projection GEMM followed by the folded-weight GEMM, Section 2.2, Eq. 3) on the
 Llama2-7B fused-QKV layer at 50% compression: K=4096, M=12288, L=1536,
 N=4096 tokens, bfloat16 storage with fp32 accumulation, synthetic seeded
 inputs resident in HBM.  The folded weight is computed once before timing, as
-the method prescribes.  Prints one JSON line.
+the method prescribes.  The timed region runs twice: straight after set-up
+(reported as detail `cold_us_per_layer`), and after `--clock-warmup` seconds
+of untimed layer calls, once the device's clocks have left their idle state
+(the headline).  Prints one JSON line.
 
 Also measured in the same run: the dense layer Y = W·X on the same GPU with
 this library's own kernels (speedup denominator), the fold, the two kernels
@@ -61,6 +64,9 @@ def parse():
     ap.add_argument("--no-mxfp8", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--clock-warmup", type=float, default=0.25,
+                    help="seconds of untimed layer calls between the cold timed region and the "
+                         "headline one (0: the headline is the cold region)")
     ap.add_argument("--kernel-probe", action="store_true",
                     help="run only the launch sequence of the hardware-counter runs (a 1 GiB "
                          "elementwise copy, then `steps` launches of each kernel phase), then exit")
@@ -312,18 +318,36 @@ def main():
         kernel_probe(E, dev, stream, args, Xr, Pr, Wfr, Ws, Y, ws, Z, wsz, wse, R)
         return
 
-    # the timed region: exactly `steps` calls, synchronised on both sides
-    for i in range(args.warmup):
-        step(i % R)
-    torch.cuda.synchronize()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    t_start.record(stream)
-    for i in range(args.steps):
-        step(i % R)
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    ms = t_start.elapsed_time(t_end) / args.steps
+    def timed_region():
+        # `warmup` calls, then exactly `steps` calls between two events,
+        # synchronised on both sides
+        for i in range(args.warmup):
+            step(i % R)
+        torch.cuda.synchronize()
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_end = torch.cuda.Event(enable_timing=True)
+        t_start.record(stream)
+        for i in range(args.steps):
+            step(i % R)
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        return t_start.elapsed_time(t_end) / args.steps
+
+    # The device's clocks rise over the first ~100 layers after an idle
+    # period (measured after 1 s idle: 331 us per layer over the first 20
+    # calls, 214 over calls 40-60, 186-199 from call 200 on through 6000
+    # calls).  The timed region as set up first (`cold`) is reported as
+    # detail; the headline is the same region after the layer has run for
+    # `clock_warmup` seconds, i.e. the throughput of a device under load.
+    ms_cold = timed_region()
+    t0 = time.time()
+    i = 0
+    while time.time() - t0 < args.clock_warmup:
+        for _ in range(50):
+            step(i % R)
+            i += 1
+        torch.cuda.synchronize()
+    ms = timed_region()
 
     flops = acc.projected_flops(K, M, L, N)
     tflops = flops / (ms * 1e-3) / 1e12
@@ -366,6 +390,8 @@ def main():
     # the parity tests cover this launch configuration against the oracle)
     detail = {
         "us_per_layer": round(ms * 1e3, 2),
+        "cold_us_per_layer": round(ms_cold * 1e3, 2),
+        "clock_warmup_s": args.clock_warmup,
         "dense_us": round(ms_dense * 1e3, 2),
         "dense_tflops": round(dense_tflops, 1),
         "dense_mfma_frac": round(dense_tflops / PEAK_BF16_TFLOPS, 4),

@@ -523,9 +523,15 @@ void tile_dims(int tile, int* bm, int* bn) {
     }
 }
 
-// The four-wave tiles other than the hand-ordered kernel's: depth step 64 in
-// two LDS stages, 32 x 32 x 16 MFMA blocks.  Matrices of 2^31 elements or more
-// take the register-staged kernel (64-bit offsets).
+// The tiles other than the hand-ordered kernel's: depth step 64.  256 x 128,
+// 128 x 256 and 128 x 128: four waves, 32 x 32 x 16 MFMA blocks, two LDS
+// stages.  128 x 192 (the Llama2-7B projection, 4096 x 1536 x 4096, one round
+// of 256 tiles): eight waves as 4 x 2 (32 x 96 each, 16 x 16 x 32 blocks) and
+// three stages — with operands streamed from HBM 67-69 us with four waves and
+// two stages, 58-60 with three stages, 57-58 with eight waves; four stages
+// were no faster, four waves with 16 x 16 x 32 blocks slower (75-80 us).
+// Matrices of 2^31 elements or more take the register-staged kernel (64-bit
+// offsets).
 hipError_t launch_gemm_tn_bf16_v2(const GemmArgs& g, hipStream_t stream) {
     const int64_t lim = (int64_t)1 << 31;
     if ((int64_t)g.R * g.lda >= lim || (int64_t)g.Cc * g.ldb >= lim || g.c_f32)
@@ -534,7 +540,7 @@ hipError_t launch_gemm_tn_bf16_v2(const GemmArgs& g, hipStream_t stream) {
         case TILE_256x128: return launch_v2<256, 128, 2, 2, 64, 2>(g, stream);
         case TILE_128x256: return launch_v2<128, 256, 2, 2, 64, 2>(g, stream);
         case TILE_128x128: return launch_v2<128, 128, 2, 2, 64, 2>(g, stream);
-        case TILE_128x192: return launch_v2<128, 192, 2, 2, 64, 2>(g, stream);
+        case TILE_128x192: return launch_v2<128, 192, 4, 2, 64, 3, 16>(g, stream);
         default: return hipErrorInvalidValue;
     }
 }

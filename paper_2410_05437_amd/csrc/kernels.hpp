@@ -14,7 +14,7 @@ enum TileKind {
     TILE_128x128 = 3,
     TILE_256x256_W8 = 4,     // 8 waves as 2 x 4 (128 x 64 each)
     TILE_256x256_W8T = 5,    // 8 waves as 4 x 2 (64 x 128 each)
-    TILE_128x192 = 6,        // 4 waves as 2 x 2 (64 x 96 each)
+    TILE_128x192 = 6,        // 8 waves as 4 x 2 (32 x 96 each)
     TILE_256x192_W8 = 7,     // 8 waves as 4 x 2 (64 x 96 each)
     SKINNY_RG1_W4 = 10,
     SKINNY_RG2_W4 = 11,
