@@ -24,9 +24,11 @@ import sys
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 EXPAND_KERNEL = "gemm_tn_bf16_v3_kernel<0, 256>"   # the four-wave 256x256 kernel, bf16 output
+PROJECT_KERNEL = "gemm_tn_bf16_v2_kernel<128, 192"   # the projection's 128x192 tile
 EXPAND_GRID = 256 * 256                        # one workgroup of 256 threads per CU
 COPY_KERNELS = ("AUnaryFunctor<c10::BFloat16", "MulFunctor")   # torch.mul(bf16, 1.0)
 COPY_BYTES = 1 << 30
+OWN = ("gemm_tn", "skinny_tn", "gemv_", "splitk_reduce", "espace::")
 
 
 def _short(name):
@@ -58,15 +60,29 @@ def stats(args):
         lines.append(f"| `{k}` | {grid} | {len(v)} | {sum(v) / len(v):.1f} | {v[len(v) // 2]:.1f} |")
     lines.append(f"| other kernels (input generation, torch copies) | | {other[0]} | "
                  f"{other[1] / max(other[0], 1):.1f} | |")
-    big = [r for r in rows if EXPAND_KERNEL in r["Kernel_Name"] and int(r["Grid_Size_X"]) == EXPAND_GRID]
+    # bench.py's launch order: the layer (project, expand) for the cold timed
+    # region, the clock warm-up and the headline timed region (W + S calls
+    # each, the warm-up a variable number), then the projection alone and the
+    # expansion alone (2 + S launches each), then the dense baseline (W + S)
+    own = [r for r in rows if any(k in r["Kernel_Name"] for k in OWN)]
+    is_p = [PROJECT_KERNEL in r["Kernel_Name"] for r in own]
     W, S = args.warmup, args.steps
-    seg = [("expand, inside the timed projected-linear steps", big[:W + S]),
-           ("expand, back-to-back loop (the roofline kernel; 2 warm-up launches)", big[W + S + 2:W + 2 * S + 2]),
-           ("dense baseline", big[W + 2 * S + 2:2 * W + 3 * S + 2])]
-    lines += ["", "The 256x256 kernel (one workgroup per CU, 768 tiles) serves both the expand GEMM "
-              "(depth L=1536) and the dense baseline (depth K=4096); split by position in bench.py's "
-              "launch order:", "", "| launches | count | average (us) | median (us) |",
-              "|---|---|---|---|"]
+    pb = next(i for i in range(len(own)) if all(is_p[i:i + 2 + S]))      # the projection's own loop
+    pe = pb + 2 + S
+    layer = own[pb - 2 * S:pb]                                           # headline: S (project, expand) pairs
+    p0 = is_p.index(True)                                                # the first layer call (after the fold)
+    cold = own[p0 + 2 * W:p0 + 2 * (W + S)]
+    seg = [("projection, inside the cold timed region (straight after set-up)", cold[0::2]),
+           ("projection, inside the headline timed region (after the clock warm-up)", layer[0::2]),
+           ("projection, back-to-back loop", own[pb + 2:pe]),
+           ("expand, inside the cold timed region", cold[1::2]),
+           ("expand, inside the headline timed region", layer[1::2]),
+           ("expand, back-to-back loop (the roofline kernel)", own[pe + 2:pe + 2 + S]),
+           ("dense baseline", own[pe + 2 + S + W:pe + 2 + 2 * S + W])]
+    lines += ["", "The projection (128x192 tiles) and the 256x256 kernel (one workgroup per CU, 768 "
+              "tiles; it serves both the expand GEMM, depth L=1536, and the dense baseline, depth "
+              "K=4096), split by position in bench.py's launch order (timed launches only):", "",
+              "| launches | count | average (us) | median (us) |", "|---|---|---|---|"]
     for name, rs in seg:
         d = sorted(_dur_us(r) for r in rs)
         if d:
@@ -93,7 +109,6 @@ MARKER = "spin_kernel"           # torch.cuda._sleep, around each of the probe's
 # the phases of bench.py --kernel-probe, in launch order
 PROBE_PHASES = ["project", "expand", "dense", "layer_N1", "dense_N1", "layer_N8", "dense_N8",
                 "layer_N16", "dense_N16"]
-OWN = ("gemm_tn", "skinny_tn", "gemv_", "splitk_reduce", "espace::")
 
 
 def _dispatches(path):
