@@ -3,10 +3,37 @@
 // elements along the reduction dimension), the two products of Section 2.2,
 // Eq. 3 with fp32 accumulation.  The projection's epilogue writes Z back in
 // MX-FP8 along L, so the expansion consumes it as it consumes the folded
-// weight.
+// weight.  Two GEMM kernels:
 //
-// v_mfma_scale_f32_16x16x128_f8f6f4 (operands "A" then "B", scale bytes in
-// byte 0 of a VGPR per lane):
+// * The expansion (bf16 output) runs the four-wave bfloat16 kernel's
+//   pipeline (gemm_bf16_v3.hip) on fp8 operands: a depth step of 128 codes is
+//   two sub-steps of 64, each with its own LDS half-stage of 64-byte rows laid
+//   out exactly as the bf16 kernel's (same loads, same chunk swizzle), plus
+//   one scale dword per row (the four 32-blocks of the step).  Per sub-step a
+//   wave issues NI x NJ v_mfma_scale_f32_32x32x64_f8f6f4 (16 for the
+//   256 x 256 tile, as long on the matrix pipe as the bf16 kernel's 64
+//   16x16x32 MFMAs) with the fragment reads of the next sub-step and the
+//   loads of step + 2 between them; persistent tiles, the next tile's first
+//   two steps loaded during the last two of the current one.
+// * The projection (MX-FP8 output, a few hundred tiles at most) runs a
+//   two-stage kernel on v_mfma_scale_f32_16x16x128_f8f6f4 with tiles small
+//   enough to give every CU work (128 x 128 tiles, two workgroups per CU, for
+//   the 4096 x 1536 projections: 43 us against 54-60 us with the pipelined
+//   kernel's 256 x 128 or 256 x 256 tiles on 192 or 96 CUs).
+//
+// v_mfma_scale_f32_32x32x64_f8f6f4 (operands "A" then "B"), as measured on
+// the device:
+//   - lane l of an operand holds row l % 32 of its 32 x 64 slice: bytes
+//     0..15 are depth 16 (l / 32) .. +15 and bytes 16..31 are depth
+//     32 + 16 (l / 32) .. +15, i.e. 16-byte chunks l / 32 and 2 + l / 32 of
+//     the 64-byte row;
+//   - the scale byte of lane l applies to row l % 32 over depth block
+//     32 (l / 32) .. +31; the instruction's op_sel picks the byte of the
+//     scale register (byte 0 for the first sub-step of a step, byte 2 for
+//     the second, each lane's dword shifted right by 8 (l / 32) beforehand);
+//   - register i of lane l of the result holds row 8 (i / 4) + 4 (l / 32) +
+//     i % 4 (from A) of column l % 32 (from B).
+// v_mfma_scale_f32_16x16x128_f8f6f4:
 //   - lane l of an operand holds row l % 16 of its 16 x 128 slice: bytes
 //     0..15 are depth 16 (l / 16) .. +15 and bytes 16..31 are depth
 //     64 + 16 (l / 16) .. +15;
@@ -14,15 +41,19 @@
 //     32 (l / 16) .. +31;
 //   - lane l of the result holds rows 4 (l / 16) + {0..3} (from A) of column
 //     l % 16 (from B).
-// The weight-side slice is passed as A and the token-side slice as B, so a
-// lane's four results are four consecutive output features of one token.
+// In both the weight-side slice is passed as A and the token-side slice as
+// B, so a lane's results are runs of consecutive output features of one
+// token.
 //
-// The scaled MFMA adds the running sum C with limited precision (on gfx950
+// The scaled MFMAs add the running sum C with limited precision (on gfx950
 // the result differs from the exact C + sum of products by up to about
-// 2^-12 (|C| + sum |a·b|)); the accumulators stay in the MFMA chain, and the
-// parity tests bound the error accordingly.
+// 2^-11.5 (|C| + sum |a·b|), either form); the accumulators stay in the MFMA
+// chain, and the parity tests bound the error accordingly.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
+#include "v3_core.hpp"
 
 namespace espace {
 
@@ -30,6 +61,56 @@ namespace {
 
 typedef int i32x8_t __attribute__((ext_vector_type(8)));
 typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+// Tile 256 tokens x BW output columns (BW = 256 or 128), four waves as 2 x 2,
+// each owning 128 tokens x BW/2 columns as NI x NJ blocks of 32 x 32.  The
+// code half-stages are the bf16 kernel's (V3Cfg<BW>: token rows first, 64
+// bytes each); after the four of them, four scale areas of one dword per
+// row.
+template <int BW>
+struct MxCfg {
+    using V = V3Cfg<BW>;
+    static constexpr int NI = 4, NJ = BW / 64;
+    static constexpr int ROWS = V::ROWS;
+    static constexpr int SCB = ROWS * 4;              // scale bytes of a half-stage
+    static constexpr int NSC = ROWS / 64;             // 256-byte scale loads per half-stage
+    static constexpr int LSC = (NSC + 3) / 4;         // per wave (uniform: extra ones repeat a load)
+    static constexpr int LPH = V::LPH + LSC;          // loads per wave and half-stage
+    static constexpr int NMF = NI * NJ;               // MFMAs per sub-step
+    static constexpr int NRD = 2 * (NI + NJ);         // code fragment reads per sub-step
+    static constexpr int NSR = NI + NJ;               // scale dword reads per step
+    static constexpr int NST = 2 * NI * NJ;           // 16-byte stores per wave (bf16 output)
+    static constexpr int SMEM = 4 * V::HS + 4 * SCB;
+    static_assert(BW == 256 || BW == 128, "tile");
+    static_assert(2 * LPH + NST < 64 && 3 * LPH + NST < 64, "vmcnt");
+    // MFMA after which load y of a sub-step is issued
+    static constexpr int load_slot(int y) { return y * NMF / LPH + NMF / (2 * LPH); }
+    // MFMA after which read x of a sub-step is issued (n reads in all)
+    static constexpr int read_slot(int x, int n) { return x * NMF / n; }
+};
+
+// MX-FP8 code byte of x (already divided by its block scale): clamp to the
+// largest E4M3 magnitude, then the hardware's round-to-nearest-even
+// conversion (which turns magnitudes past 464 into NaN, hence the clamp).
+__device__ __forceinline__ uint32_t mx_pack4(float x0, float x1, float x2, float x3) {
+    x0 = fminf(fmaxf(x0, -448.f), 448.f);
+    x1 = fminf(fmaxf(x1, -448.f), 448.f);
+    x2 = fminf(fmaxf(x2, -448.f), 448.f);
+    x3 = fminf(fmaxf(x3, -448.f), 448.f);
+    uint32_t r = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(x0, x1, 0, false);
+    return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(x2, x3, (int)r, true);
+}
+
+// Scale exponent S of a block with largest magnitude amax: floor(log2 amax)
+// - 8 with the byte S + 127 clamped to [0, 254]; byte 0 for a zero block.
+__device__ __forceinline__ int mx_scale_byte(float amax) {
+    if (!(amax > 0.f)) return 0;
+    const int e = __builtin_amdgcn_frexp_expf(amax) - 1;   // floor(log2 amax)
+    const int b = e - 8 + 127;
+    return b < 0 ? 0 : (b > 254 ? 254 : b);
+}
+
+// ---- the projection's kernel ------------------------------------------------
 
 constexpr int MX_BK = 128;   // depth of one step: one block-scaled MFMA
 
@@ -41,7 +122,7 @@ __device__ __forceinline__ int mx_swz(int r) { return (r >> 1) & 7; }
 // A stage holds the tile's BT + BW rows of 128 code bytes (token rows first),
 // then one scale dword (the 4 blocks of the step) per row.
 template <int BT, int BW>
-struct MxCfg {
+struct MxZCfg {
     static constexpr int ROWS = BT + BW;
     static constexpr int DATA = ROWS * MX_BK;
     static constexpr int STAGE = DATA + ROWS * 4;
@@ -59,7 +140,7 @@ struct MxCfg {
 template <int BT, int BW>
 __device__ __forceinline__ void mx_issue(unsigned char* stage, const MxGemmArgs& a, int row0, int col0, int t,
                                          int wave, int lane) {
-    using C = MxCfg<BT, BW>;
+    using C = MxZCfg<BT, BW>;
     const auto tr = __builtin_amdgcn_make_buffer_rsrc((void*)a.T, (short)0, (int)(a.R * a.ldt), 0x00020000);
     const auto wr = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, (short)0, (int)(a.C * a.ldw), 0x00020000);
     const auto ts = __builtin_amdgcn_make_buffer_rsrc((void*)a.Ts, (short)0, (int)(a.R * a.ldts), 0x00020000);
@@ -104,31 +185,12 @@ __device__ __forceinline__ i32x8_t mx_frag(const unsigned char* stage, int rr, i
 
 __device__ __forceinline__ void mx_wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-// MX-FP8 code byte of x (already divided by its block scale): clamp to the
-// largest E4M3 magnitude, then the hardware's round-to-nearest-even
-// conversion (which turns magnitudes past 464 into NaN, hence the clamp).
-__device__ __forceinline__ uint32_t mx_pack4(float x0, float x1, float x2, float x3) {
-    x0 = fminf(fmaxf(x0, -448.f), 448.f);
-    x1 = fminf(fmaxf(x1, -448.f), 448.f);
-    x2 = fminf(fmaxf(x2, -448.f), 448.f);
-    x3 = fminf(fmaxf(x3, -448.f), 448.f);
-    uint32_t r = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(x0, x1, 0, false);
-    return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(x2, x3, (int)r, true);
-}
-
-// Scale exponent S of a block with largest magnitude amax: floor(log2 amax)
-// - 8 with the byte S + 127 clamped to [0, 254]; byte 0 for a zero block.
-__device__ __forceinline__ int mx_scale_byte(float amax) {
-    if (!(amax > 0.f)) return 0;
-    const int e = __builtin_amdgcn_frexp_expf(amax) - 1;   // floor(log2 amax)
-    const int b = e - 8 + 127;
-    return b < 0 ? 0 : (b > 254 ? 254 : b);
-}
-
-template <int BT, int BW, int OUT>
+// Tile BT tokens x BW columns, MX-FP8 output along the columns (codes and
+// one scale byte per 32 columns, up to cpad columns); one workgroup per tile.
+template <int BT, int BW>
 __global__ __launch_bounds__(256, (BT + BW) <= 256 ? 2 : 1)
-void gemm_mx_kernel(MxGemmArgs a) {
-    using C = MxCfg<BT, BW>;
+void gemm_mx_z_kernel(MxGemmArgs a) {
+    using C = MxZCfg<BT, BW>;
     __shared__ __attribute__((aligned(1024))) unsigned char smem[C::SMEM];
 
     const int tiles_c = (a.C + BW - 1) / BW;
@@ -183,27 +245,7 @@ void gemm_mx_kernel(MxGemmArgs a) {
 
     // ---- epilogue: lane holds token row wt0 + 16 i + lr, output columns
     // ww0 + 16 j + 4 q + {0..3}
-    if constexpr (OUT == 0) {
-        uint16_t* Y = static_cast<uint16_t*>(a.out);
-#pragma unroll
-        for (int i = 0; i < C::NI; ++i) {
-            const int n = row0 + wt0 + 16 * i + lr;
-            if (n >= a.R) continue;
-#pragma unroll
-            for (int j = 0; j < C::NJ; ++j) {
-                const int m = col0 + ww0 + 16 * j + 4 * q;
-                const f32x4_t v = acc[i][j];
-                uint16_t* p = Y + (int64_t)n * a.ldo + m;
-                if (m + 4 <= a.C) {
-                    *reinterpret_cast<u32x2_t*>(p) = u32x2_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (m + e < a.C) p[e] = (uint16_t)bf16_rne(v[e]);
-                }
-            }
-        }
-    } else {
+    {
         // MX-FP8 along the columns: block pair (j, j + 1) is one 32-column
         // block; its largest magnitude over the 4 lanes of the token row
         uint8_t* Zq = static_cast<uint8_t*>(a.out);
@@ -238,6 +280,463 @@ void gemm_mx_kernel(MxGemmArgs a) {
                 }
             }
         }
+    }
+}
+
+// ---- the expansion's kernel -------------------------------------------------
+
+// v_mfma_scale_f32_32x32x64_f8f6f4 by inline assembly, so that the
+// accumulators stay in the AGPRs and the order is the one written; SEL is
+// the op_sel_hi bit of both scale operands (0: byte 0, 1: byte 2).
+#define MX_MFMA(acc, w, t, ws, ts, SEL)                                                                \
+    asm volatile("v_mfma_scale_f32_32x32x64_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[" SEL "," SEL ",0]" \
+                 : "+a"(acc) : "v"(w), "v"(t), "v"(ws), "v"(ts))
+#define MX_MFMA0(acc, w, t, ws, ts, SEL)                                                              \
+    asm volatile("v_mfma_scale_f32_32x32x64_f8f6f4 %0, %1, %2, 0, %3, %4 op_sel_hi:[" SEL "," SEL ",0]" \
+                 : "=a"(acc) : "v"(w), "v"(t), "v"(ws), "v"(ts))
+#define MX_READ(dst, addr, off) \
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(dst) : "v"(addr), "i"(off))
+#define MX_READ32(dst, addr, off) \
+    asm volatile("ds_read_b32 %0, %1 offset:%2" : "=v"(dst) : "v"(addr), "i"(off))
+
+// Code fragments of one sub-step: 32 bytes per lane and block, read as the
+// two 16-byte chunks of the 64-byte row.
+template <int NJ>
+struct MxFrag {
+    i32x4_t tl[4], th[4], wl[NJ], wh[NJ];
+};
+
+// LDS addresses of one half-stage for this lane: its token and weight rows'
+// two chunks, and its token and weight scale dwords.
+struct MxAddr {
+    unsigned tl, th, wl, wh, ts, ws;
+};
+
+// Code read x of a sub-step, in the order the MFMAs use them: token block 0,
+// weight blocks 0 .. NJ-1, token blocks 1 .. 3 (two reads per block; blocks
+// are 32 rows, 2048 bytes, apart).
+template <int NJ>
+__device__ __forceinline__ void mx_read(int x, MxFrag<NJ>& f, const MxAddr& a) {
+#define MX_R(n)                                                                                     \
+    if constexpr (n < 2 * (4 + NJ)) {                                                               \
+        if (x == n) {                                                                               \
+            constexpr int b = n / 2;                                                                \
+            if constexpr (b == 0) {                                                                 \
+                if constexpr (n % 2) MX_READ(f.th[0], a.th, 0); else MX_READ(f.tl[0], a.tl, 0);     \
+            } else if constexpr (b <= NJ) {                                                         \
+                if constexpr (n % 2) MX_READ(f.wh[b - 1], a.wh, (b - 1) * 2048);                    \
+                else MX_READ(f.wl[b - 1], a.wl, (b - 1) * 2048);                                    \
+            } else {                                                                                \
+                if constexpr (n % 2) MX_READ(f.th[b - NJ], a.th, (b - NJ) * 2048);                  \
+                else MX_READ(f.tl[b - NJ], a.tl, (b - NJ) * 2048);                                  \
+            }                                                                                       \
+        }                                                                                           \
+    }
+    MX_R(0) MX_R(1) MX_R(2) MX_R(3) MX_R(4) MX_R(5) MX_R(6) MX_R(7)
+    MX_R(8) MX_R(9) MX_R(10) MX_R(11) MX_R(12) MX_R(13) MX_R(14) MX_R(15)
+#undef MX_R
+}
+
+// Scale read x of a step (token blocks 0 .. 3, then weight blocks; 32 rows,
+// 128 bytes, apart) into the raw dwords.
+template <int NJ>
+__device__ __forceinline__ void mx_read_scale(int x, int* tsr, int* wsr, const MxAddr& a) {
+#define MX_S(n)                                                                           \
+    if constexpr (n < 4 + NJ) {                                                           \
+        if (x == n) {                                                                     \
+            if constexpr (n < 4) MX_READ32(tsr[n], a.ts, n * 128);                        \
+            else MX_READ32(wsr[n - 4], a.ws, (n - 4) * 128);                              \
+        }                                                                                 \
+    }
+    MX_S(0) MX_S(1) MX_S(2) MX_S(3) MX_S(4) MX_S(5) MX_S(6) MX_S(7)
+#undef MX_S
+}
+
+// What a sub-step's loads need: the code operands as 16-bit arrays (the
+// bf16 kernel's load helpers; one step of 128 codes is 64 of their
+// elements), the scale arrays, and this lane's per-load row offsets.
+template <int BW>
+struct MxLoad {
+    using C = MxCfg<BW>;
+    const uint16_t* T;
+    const uint16_t* W;
+    unsigned tbytes, wbytes;
+    const uint8_t* Ts;
+    const uint8_t* Ws;
+    unsigned tsbytes, wsbytes;
+    int voff[C::V::LPH];
+    int soff[C::LSC];
+    int wave;
+
+    // scale load j covers rows 64 s .. 64 s + 63 of the tile, s = (wave + 4 j) % NSC
+    __device__ __forceinline__ void scale_offsets(const MxGemmArgs& a, int row0, int col0, int lane) {
+#pragma unroll
+        for (int j = 0; j < C::LSC; ++j) {
+            const int s = (wave + 4 * j) % C::NSC;
+            const int rr = 64 * s + lane;
+            soff[j] = rr < 256 ? min(row0 + rr, a.R - 1) * (int)a.ldts
+                               : min(col0 + rr - 256, a.C - 1) * (int)a.ldws;
+        }
+    }
+
+    // load y of half h of step kt into half-stage u
+    __device__ __forceinline__ void load(unsigned char* smem, int kt, int h, int u, int y) const {
+        if (y < C::V::LPH) {
+            v3_load<typename C::V>(smem, T, W, tbytes, wbytes, voff, wave, kt, h, u, y);
+        } else {
+            const int j = y - C::V::LPH;
+            const int s = (wave + 4 * j) % C::NSC;
+            const bool tok = s < 4;
+            const auto rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(tok ? Ts : Ws), (short)0,
+                                                                (int)(tok ? tsbytes : wsbytes), 0x00020000);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rsrc, (__attribute__((address_space(3))) void*)(smem + 4 * C::V::HS + u * C::SCB + 256 * s), 4,
+                soff[j], 4 * kt, 0, 0);
+        }
+    }
+};
+
+// One sub-step: NMF MFMAs on (cur, the shifted scales tsc / wsc) with
+// op_sel_hi SEL; between them the NRD code reads of the next sub-step into
+// nxt from rd, with SREADS also the NSR scale dwords of the next step from
+// sd into tsr / wsr, and with do_load the LPH loads of half h of step lkt
+// into half-stage u.  FIRST: the accumulators start from zero.
+template <int BW, bool FIRST, bool SEL1, bool SREADS>
+__device__ __forceinline__ void mx_substep(f32x16_t (&acc)[4][BW / 64], const MxFrag<BW / 64>& cur,
+                                           const int* tsc, const int* wsc, MxFrag<BW / 64>& nxt,
+                                           const MxAddr& rd, const MxAddr& sd, int* tsr, int* wsr,
+                                           unsigned char* smem, const MxLoad<BW>& ld, int lkt, int h, int u,
+                                           bool do_load) {
+    using C = MxCfg<BW>;
+    constexpr int NJ = C::NJ;
+    constexpr int NR = C::NRD + (SREADS ? C::NSR : 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const i32x8_t w = __builtin_shufflevector(cur.wl[j], cur.wh[j], 0, 1, 2, 3, 4, 5, 6, 7);
+            const i32x8_t t = __builtin_shufflevector(cur.tl[i], cur.th[i], 0, 1, 2, 3, 4, 5, 6, 7);
+            if constexpr (FIRST) {
+                if constexpr (SEL1) MX_MFMA0(acc[i][j], w, t, wsc[j], tsc[i], "1");
+                else MX_MFMA0(acc[i][j], w, t, wsc[j], tsc[i], "0");
+            } else {
+                if constexpr (SEL1) MX_MFMA(acc[i][j], w, t, wsc[j], tsc[i], "1");
+                else MX_MFMA(acc[i][j], w, t, wsc[j], tsc[i], "0");
+            }
+            const int m = i * NJ + j;
+#pragma unroll
+            for (int x = 0; x < NR; ++x)
+                if (C::read_slot(x, NR) == m) {
+                    if (x < C::NRD) mx_read<NJ>(x, nxt, rd);
+                    else mx_read_scale<NJ>(x - C::NRD, tsr, wsr, sd);
+                }
+#pragma unroll
+            for (int y = 0; y < C::LPH; ++y)
+                if (C::load_slot(y) == m && do_load) ld.load(smem, lkt, h, u, y);
+        }
+}
+
+// vmcnt(n) for the counts the steps need (k sub-steps of LPH loads, plus the
+// previous tile's NST stores); any other n waits for everything
+template <class C>
+__device__ __forceinline__ void mx_wait_vm_n(int n) {
+    constexpr int L = C::LPH, S = C::NST;
+    if (n == 0) v3_wait_vm<0>();
+    else if (n == L) v3_wait_vm<L>();
+    else if (n == 2 * L) v3_wait_vm<2 * L>();
+    else if (n == 3 * L) v3_wait_vm<3 * L>();
+    else if (n == S) v3_wait_vm<S>();
+    else if (n == L + S) v3_wait_vm<L + S>();
+    else if (n == 2 * L + S) v3_wait_vm<2 * L + S>();
+    else if (n == 3 * L + S) v3_wait_vm<3 * L + S>();
+    else v3_wait_vm<0>();
+}
+
+// Copy of an accumulator block in VGPRs (the accumulators are named only by
+// inline assembly with AGPR operands).
+__device__ __forceinline__ f32x16_t mx_acc_read(const f32x16_t& a) {
+    f32x16_t v;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        float x;
+        asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(x) : "a"(a[r]));
+        v[r] = x;
+    }
+    return v;
+}
+
+// The MX GEMM: out[n][c] = sum_k T[n][k] W[c][k] over MX-FP8 codes and
+// scales, n < R tokens, c < C columns, depth D (the codes are zero-padded to
+// whole steps of 128).  Persistent: min(tiles, CUs) workgroups,
+// each taking tiles blockIdx.x, blockIdx.x + gridDim.x, ...  As in the bf16
+// kernel, when the output is bf16 with C a multiple of 8, the last two steps
+// of a tile load the next tile's first two, and the tile's results leave with
+// exactly NST stores per wave.  Output: bf16 Y [R][ldo].
+template <int BW>
+__global__ __launch_bounds__(256, 1)
+void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
+    using C = MxCfg<BW>;
+    using V = typename C::V;
+    constexpr int NJ = C::NJ;
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[C::SMEM];
+
+    const int ktiles = (a.D + 127) / 128;           // the codes are zero-padded to whole steps
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wrow0 = (wave >> 1) * 128;              // the wave's tokens in the tile
+    const int wcol0 = (wave & 1) * (BW / 2);          // its output columns
+    const bool ahead_ok = (a.C & 7) == 0 && ktiles >= 2;
+
+    MxLoad<BW> ld;
+    ld.T = reinterpret_cast<const uint16_t*>(a.T);
+    ld.W = reinterpret_cast<const uint16_t*>(a.W);
+    ld.tbytes = (unsigned)((uint64_t)a.R * a.ldt);
+    ld.wbytes = (unsigned)((uint64_t)a.C * a.ldw);
+    ld.Ts = a.Ts;
+    ld.Ws = a.Ws;
+    ld.tsbytes = (unsigned)((uint64_t)a.R * a.ldts);
+    ld.wsbytes = (unsigned)((uint64_t)a.C * a.ldws);
+    ld.wave = wave;
+
+    // fragment addresses: a lane reads row lane % 32 of each 32-row block,
+    // chunks lh and 2 + lh; the swizzle depends on the row only through
+    // lane % 32 (blocks start at multiples of 32 rows)
+    const int lr = lane & 31;
+    const int lh = lane >> 5;
+    const int sw = v3_swz(lr);
+    const unsigned sbase = (unsigned)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
+    const unsigned c_lo = (unsigned)((lh ^ sw) * 16), c_hi = (unsigned)(((2 + lh) ^ sw) * 16);
+    const unsigned trow = sbase + (unsigned)((wrow0 + lr) * V3_ROWB);
+    const unsigned wrow = sbase + (unsigned)((V3_BM + wcol0 + lr) * V3_ROWB);
+    const unsigned tsca = sbase + (unsigned)(4 * V::HS + 4 * (wrow0 + lr));
+    const unsigned wsca = sbase + (unsigned)(4 * V::HS + 4 * (V3_BM + wcol0 + lr));
+    auto addr = [&](int u) {
+        MxAddr m;
+        m.tl = trow + c_lo + (unsigned)(u * V::HS);
+        m.th = trow + c_hi + (unsigned)(u * V::HS);
+        m.wl = wrow + c_lo + (unsigned)(u * V::HS);
+        m.wh = wrow + c_hi + (unsigned)(u * V::HS);
+        m.ts = tsca + (unsigned)(u * C::SCB);
+        m.ws = wsca + (unsigned)(u * C::SCB);
+        return m;
+    };
+    const int shift = 8 * lh;                         // block lh of a sub-step at byte 0 (or 2)
+
+    f32x16_t acc[4][NJ];
+    MxFrag<NJ> f0, f1;
+    int tsr[4], wsr[NJ], tsc[4], wsc[NJ];
+
+    int item = blockIdx.x;
+    int tile_r, tile_c;
+    tile_coords<4>(item, ntiles, tiles_c, 0, tile_r, tile_c);
+    bool ahead = false;     // this tile's first two steps were loaded by the previous one
+    int s0 = 0;             // stage of this tile's first step (half-stages 2 s0, 2 s0 + 1)
+    while (true) {
+        const int row0 = tile_r * V3_BM;
+        const int col0 = tile_c * BW;
+        const int next = item + (int)gridDim.x;
+        const bool ahead_next = ahead_ok && next < ntiles;
+        int ntr = 0, ntc = 0;
+        if (next < ntiles) tile_coords<4>(next, ntiles, tiles_c, 0, ntr, ntc);
+
+        // half-stage of (stage relative to s0, half)
+        auto hs = [&](int rel, int h) { return ((rel ^ s0) << 1) | h; };
+        const MxAddr A0 = addr(hs(0, 0)), A1 = addr(hs(0, 1)), A2 = addr(hs(1, 0)), A3 = addr(hs(1, 1));
+
+        if (ahead) {
+            // the first step's loads, then the second's and the previous
+            // tile's stores were issued
+            v3_wait_vm<2 * C::LPH + C::NST>();
+        } else {
+            // the half-stages may still be read by a wave finishing the previous tile
+            if (item != (int)blockIdx.x) __syncthreads();
+            v3_offsets<V>(ld.voff, row0, col0, a.R, a.C, a.ldt / 2, a.ldw / 2, wave, lane);
+            ld.scale_offsets(a, row0, col0, lane);
+#pragma unroll
+            for (int y = 0; y < C::LPH; ++y) ld.load(smem, 0, 0, hs(0, 0), y);
+#pragma unroll
+            for (int y = 0; y < C::LPH; ++y) ld.load(smem, 0, 1, hs(0, 1), y);
+            if (ktiles > 1) {
+#pragma unroll
+                for (int y = 0; y < C::LPH; ++y) ld.load(smem, 1, 0, hs(1, 0), y);
+#pragma unroll
+                for (int y = 0; y < C::LPH; ++y) ld.load(smem, 1, 1, hs(1, 1), y);
+                v3_wait_vm<2 * C::LPH>();
+            } else {
+                v3_wait_vm<0>();
+            }
+        }
+        __builtin_amdgcn_s_barrier();
+#pragma unroll
+        for (int x = 0; x < C::NRD; ++x) mx_read<NJ>(x, f0, A0);
+#pragma unroll
+        for (int x = 0; x < C::NSR; ++x) mx_read_scale<NJ>(x, tsr, wsr, A0);
+        v3_wait_lgkm0();
+        // the first sub-step loads step 2 into the half-stage just read:
+        // every wave's reads of it must be complete before any wave issues them
+        __builtin_amdgcn_s_barrier();
+
+        int kt = 0;
+        int rel = 0;          // stage of step kt relative to s0
+        // the loads of sub-step h of step kt: half h of step kt + 2 of this
+        // tile, or of the next tile's first steps once this one has none left
+        // (step lkt of that tile); false: none
+        auto load_kind = [&](int h, int& lkt) -> bool {
+            if (kt + 2 < ktiles) {
+                lkt = kt + 2;
+                return true;
+            }
+            lkt = kt + 2 - ktiles;
+            if (!ahead_next) return false;
+            if (kt + 2 == ktiles && h == 0) {
+                v3_offsets<V>(ld.voff, ntr * V3_BM, ntc * BW, a.R, a.C, a.ldt / 2, a.ldw / 2, wave, lane);
+                ld.scale_offsets(a, ntr * V3_BM, ntc * BW, lane);
+            }
+            return true;
+        };
+        // the step's scale dwords, each lane's shifted right by 8 lh: inline
+        // assembly, so that the shifts stay after the lgkmcnt wait that
+        // completes the reads (the compiler does not know them as LDS reads)
+        auto shift_scales = [&]() {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) asm volatile("v_lshrrev_b32 %0, %1, %2" : "=v"(tsc[i]) : "v"(shift), "v"(tsr[i]));
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) asm volatile("v_lshrrev_b32 %0, %1, %2" : "=v"(wsc[j]) : "v"(shift), "v"(wsr[j]));
+        };
+        // one step with the stage chosen at run time (the first one and the
+        // last ones); FIRST: the accumulators start at zero
+        auto generic_step = [&](auto first) {
+            constexpr bool F = decltype(first)::value;
+            // after a tile loaded ahead, its first step has the previous
+            // tile's stores in flight behind the loads of its second step
+            const int stores = (F && ahead) ? C::NST : 0;
+            shift_scales();
+            int lkt;
+            const bool k0 = load_kind(0, lkt);
+            mx_substep<BW, F, false, false>(acc, f0, tsc, wsc, f1, rel ? A3 : A1, A0, tsr, wsr, smem, ld, lkt, 0,
+                                            hs(rel, 0), k0);
+            const int n0 = k0 ? C::LPH : 0;
+            v3_wait_lgkm0();
+            if (kt + 1 < ktiles || ahead_next) {
+                // the next step's first half has landed (the loads just issued may stay in flight)
+                if (kt + 1 < ktiles) mx_wait_vm_n<C>(C::LPH + stores + n0);
+                __builtin_amdgcn_s_barrier();
+            }
+            // sub-step 1: fragments and scales of the next step's sub-step 0
+            // (after the last step the reads are of no use but harmless)
+            const bool k1 = load_kind(1, lkt);
+            mx_substep<BW, false, true, true>(acc, f1, tsc, wsc, f0, rel ? A0 : A2, rel ? A0 : A2, tsr, wsr, smem,
+                                              ld, lkt, 1, hs(rel, 1), k1);
+            const int n1 = k1 ? C::LPH : 0;
+            v3_wait_lgkm0();
+            if (kt + 1 < ktiles) {
+                // the next step's second half has landed
+                mx_wait_vm_n<C>(stores + n0 + n1);
+                __builtin_amdgcn_s_barrier();
+            }
+            rel ^= 1;
+            ++kt;
+        };
+        generic_step(std::true_type{});
+        // steady state, two steps per iteration (relative stages 1 and 0):
+        // the loads issued in them are this tile's; each barrier waits for the
+        // half-stage the next sub-step reads, with the two newer half-steps of
+        // loads in flight
+        while (kt + 3 < ktiles) {
+            shift_scales();
+            mx_substep<BW, false, false, false>(acc, f0, tsc, wsc, f1, A3, A3, tsr, wsr, smem, ld, kt + 2, 0,
+                                                hs(1, 0), true);
+            v3_wait_lgkm0();
+            v3_wait_vm<2 * C::LPH>();
+            __builtin_amdgcn_s_barrier();
+            mx_substep<BW, false, true, true>(acc, f1, tsc, wsc, f0, A0, A0, tsr, wsr, smem, ld, kt + 2, 1,
+                                              hs(1, 1), true);
+            v3_wait_lgkm0();
+            v3_wait_vm<2 * C::LPH>();
+            __builtin_amdgcn_s_barrier();
+            shift_scales();
+            mx_substep<BW, false, false, false>(acc, f0, tsc, wsc, f1, A1, A1, tsr, wsr, smem, ld, kt + 3, 0,
+                                                hs(0, 0), true);
+            v3_wait_lgkm0();
+            v3_wait_vm<2 * C::LPH>();
+            __builtin_amdgcn_s_barrier();
+            mx_substep<BW, false, true, true>(acc, f1, tsc, wsc, f0, A2, A2, tsr, wsr, smem, ld, kt + 3, 1,
+                                              hs(0, 1), true);
+            v3_wait_lgkm0();
+            v3_wait_vm<2 * C::LPH>();
+            __builtin_amdgcn_s_barrier();
+            kt += 2;
+        }
+        while (kt < ktiles) generic_step(std::false_type{});
+
+        // the accumulators are written by inline assembly the compiler does
+        // not know as MFMAs: wait out the MFMA-to-VALU read hazard
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+
+        // ---- epilogue: register r of block (i, j) holds token row
+        // wrow0 + 32 i + lr and output column wcol0 + 32 j + 8 (r / 4) + 4 lh + r % 4
+        uint16_t* Y = static_cast<uint16_t*>(a.out);
+        if (ahead_ok) {
+            // two 16-byte stores per block: after the swap with the lane
+            // 32 away, lane lh holds columns 16 g + 8 lh .. + 7 (g = 0, 1)
+            // of its row; lanes outside the matrix get an offset past
+            // the buffer, which its range check drops
+            const unsigned ybytes = (unsigned)((uint64_t)a.R * a.ldo * 2u);
+            const auto yr = __builtin_amdgcn_make_buffer_rsrc((void*)Y, (short)0, (int)ybytes, 0x00020000);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int n = row0 + wrow0 + 32 * i + lr;
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    const f32x16_t v = mx_acc_read(acc[i][j]);
+#pragma unroll
+                    for (int g = 0; g < 2; ++g) {
+                        const auto s0v = __builtin_amdgcn_permlane32_swap(
+                            pack_bf16x2(v[8 * g], v[8 * g + 1]), pack_bf16x2(v[8 * g + 4], v[8 * g + 5]), false,
+                            false);
+                        const auto s1v = __builtin_amdgcn_permlane32_swap(
+                            pack_bf16x2(v[8 * g + 2], v[8 * g + 3]), pack_bf16x2(v[8 * g + 6], v[8 * g + 7]),
+                            false, false);
+                        const u32x4_t out = u32x4_t{s0v[0], s1v[0], s0v[1], s1v[1]};
+                        const int c = col0 + wcol0 + 32 * j + 16 * g + 8 * lh;
+                        const unsigned off =
+                            (n < a.R && c < a.C) ? ((unsigned)n * (unsigned)a.ldo + (unsigned)c) * 2u : 0xFFFFFFF0u;
+                        __builtin_amdgcn_raw_buffer_store_b128(out, yr, (int)off, 0, 0);
+                    }
+                }
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int n = row0 + wrow0 + 32 * i + lr;
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    const f32x16_t v = mx_acc_read(acc[i][j]);
+                    if (n >= a.R) continue;
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int c = col0 + wcol0 + 32 * j + 8 * g + 4 * lh;
+                        uint16_t* p = Y + (int64_t)n * a.ldo + c;
+                        if (c + 4 <= a.C) {
+                            *reinterpret_cast<u32x2_t*>(p) =
+                                u32x2_t{pack_bf16x2(v[4 * g], v[4 * g + 1]), pack_bf16x2(v[4 * g + 2], v[4 * g + 3])};
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                if (c + e < a.C) p[e] = (uint16_t)bf16_rne(v[4 * g + e]);
+                        }
+                    }
+                }
+            }
+        }
+        if (next >= ntiles) break;
+        item = next;
+        tile_r = ntr;
+        tile_c = ntc;
+        s0 = (s0 + ktiles) & 1;
+        ahead = ahead_next;
     }
 }
 
@@ -286,37 +785,54 @@ void mx_quantize_kernel(const uint16_t* A, int64_t lda, int R, int C, uint8_t* Q
     S[(int64_t)r * lds + b] = (uint8_t)sb;
 }
 
-template <int BT, int BW, int OUT>
-hipError_t launch_tile(const MxGemmArgs& a, hipStream_t stream) {
+template <int BW>
+hipError_t launch_pipelined(const MxGemmArgs& a, int cus, hipStream_t stream) {
+    const int tiles_c = (a.C + BW - 1) / BW;
+    const int ntiles = tiles_c * ((a.R + 255) / 256);
+    const int grid = ntiles < cus ? ntiles : cus;
+    hipLaunchKernelGGL((gemm_mx_kernel<BW>), dim3(grid), dim3(256), 0, stream, a, tiles_c, ntiles);
+    return hipGetLastError();
+}
+
+template <int BT, int BW>
+hipError_t launch_z(const MxGemmArgs& a, hipStream_t stream) {
     const int tiles = ((a.R + BT - 1) / BT) * ((a.C + BW - 1) / BW);
-    hipLaunchKernelGGL((gemm_mx_kernel<BT, BW, OUT>), dim3(tiles), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL((gemm_mx_z_kernel<BT, BW>), dim3(tiles), dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 
 }  // namespace
 
-int mx_gemm_tile(int R, int C, int cus) {
-    // the largest tile that still gives every CU a tile, else the smallest
+int mx_gemm_tile(int R, int C, int cus, int out_mx) {
     const long long t256 = (long long)((R + 255) / 256) * ((C + 255) / 256);
     const long long t128 = (long long)((R + 255) / 256) * ((C + 127) / 128);
-    if (t256 >= cus) return 0;
-    if (t128 >= cus) return 1;
-    return 2;
+    if (out_mx) {
+        // the largest tile that still gives every CU a tile, else the smallest
+        if (t256 >= cus) return 0;
+        if (t128 >= cus) return 1;
+        return 2;
+    }
+    // 256 x 256 tiles when they give every CU a tile or when 256 x 128 tiles
+    // (half the work each) need twice the rounds or more
+    const long long r256 = (t256 + cus - 1) / cus, r128 = (t128 + cus - 1) / cus;
+    return (t256 >= cus || 2 * r256 <= r128) ? 0 : 1;
 }
 
 hipError_t launch_gemm_mx(const MxGemmArgs& a, int out_mx, int cus, hipStream_t stream) {
     const int64_t lim = (int64_t)1 << 31;
     if (a.R < 1 || a.C < 1 || a.D < 1 || a.R * a.ldt >= lim || a.C * a.ldw >= lim || a.R * a.ldts >= lim ||
-        a.C * a.ldws >= lim)
+        a.C * a.ldws >= lim || a.ldt % 16 || a.ldw % 16 || a.ldts % 4 || a.ldws % 4 ||
+        (!out_mx && (int64_t)a.R * a.ldo * 2 >= lim))
         return hipErrorInvalidValue;
-    switch (mx_gemm_tile(a.R, a.C, cus) * 2 + (out_mx ? 1 : 0)) {
-        case 0: return launch_tile<256, 256, 0>(a, stream);
-        case 1: return launch_tile<256, 256, 1>(a, stream);
-        case 2: return launch_tile<256, 128, 0>(a, stream);
-        case 3: return launch_tile<256, 128, 1>(a, stream);
-        case 4: return launch_tile<128, 128, 0>(a, stream);
-        default: return launch_tile<128, 128, 1>(a, stream);
+    const int tile = mx_gemm_tile(a.R, a.C, cus, out_mx);
+    if (out_mx) {
+        switch (tile) {
+            case 0: return launch_z<256, 256>(a, stream);
+            case 1: return launch_z<256, 128>(a, stream);
+            default: return launch_z<128, 128>(a, stream);
+        }
     }
+    return tile == 0 ? launch_pipelined<256>(a, cus, stream) : launch_pipelined<128>(a, cus, stream);
 }
 
 hipError_t launch_mx_quantize(const uint16_t* A, int64_t lda, int R, int C, uint8_t* Q, int64_t ldq, uint8_t* S,

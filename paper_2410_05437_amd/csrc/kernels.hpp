@@ -123,8 +123,9 @@ struct MxGemmArgs {
     int R, C, D;
     int cpad;                           // MX-FP8 output: columns written, round_up(C, 128)
 };
-// Tile of the MX GEMM for R x C outputs (0: 256 x 256, 1: 256 x 128, 2: 128 x 128).
-int mx_gemm_tile(int R, int C, int cus);
+// Tile of the MX GEMM for R x C outputs (0: 256 x 256, 1: 256 x 128, 2: 128 x 128;
+// 2 only for MX-FP8 output).
+int mx_gemm_tile(int R, int C, int cus, int out_mx);
 // out_mx: write MX-FP8 (codes and scales along the columns) instead of bf16.
 // hipErrorInvalidValue when an operand spans 2^31 bytes or more.
 hipError_t launch_gemm_mx(const MxGemmArgs& a, int out_mx, int cus, hipStream_t stream);

@@ -1,19 +1,22 @@
 """Parity criteria of the MX-FP8 path (element-wise, against the oracle).
 
-Accumulation model.  The products run on gfx950's block-scaled MFMA
-(v_mfma_scale_f32_16x16x128_f8f6f4), one instruction per 128 of depth, each
-adding its block-scaled dot product to the running fp32 sum C.  Measured on
-the hardware (random operands and scales, 600 instructions with C = 0 and 600
-with |C| from 1e-3 to 1e3 times the products' magnitude), one instruction's
-result differs from the exact C + sum(a·b) by at most 2^-11.6 of
-sum|a·b| (C = 0) and 2^-12.2 of |C| + sum|a·b| (C != 0): the instruction
+Accumulation model.  The products run on gfx950's block-scaled MFMAs, each
+instruction adding its block-scaled dot product to the running fp32 sum C:
+the projection on v_mfma_scale_f32_16x16x128_f8f6f4 (one instruction per
+128 of depth), the expansion on v_mfma_scale_f32_32x32x64_f8f6f4 (one per
+64).  Measured on the hardware, one instruction's result differs from the
+exact C + sum(a·b) by at most 2^-11.6 of sum|a·b| (C = 0) and 2^-12.2 of
+|C| + sum|a·b| (C != 0) for the 16x16x128 form (600 + 600 random trials),
+and by at most 2^-11.55 of |C| + sum|a·b| for the 32x32x64 form (1200
+trials, |C| from 0 to 1e3 times the products' magnitude): the instruction
 rounds inside.  The bound here takes eps = 2^-10 per instruction, so after
-step t of a product
+instruction t of a product
 
     |computed - exact| <= eps · sum_{s<=t} (|P_{s-1}| + S_s)
 
-with P_s the exact partial sum after step s and S_s = sum over step s of
-|a·b| (block scales applied), both evaluated by the oracle side in float64.
+with P_s the exact partial sum after instruction s and S_s = sum over its
+depth of |a·b| (block scales applied), both evaluated by the oracle side in
+float64; `step` is the depth of one instruction.
 
 Z's re-quantisation.  The projection quantises its fp32 Z; the oracle's
 exact Z may sit on the other side of a rounding boundary.  A GPU scale byte
@@ -28,7 +31,8 @@ import torch
 import oracle
 
 EPS_MFMA = 2.0 ** -10
-STEP = 128
+STEP_PROJECT = 128    # depth of one MFMA of the projection (16x16x128)
+STEP_EXPAND = 64      # of the expansion (32x32x64)
 U_BF16 = 2.0 ** -8
 
 
@@ -55,14 +59,15 @@ def gpu_mx(m, rows=None):
     return _TABLE[codes[:, :m.cols]], scales[:, :nb].astype(np.int64), codes, scales
 
 
-def chain_bound(A, B):
+def chain_bound(A, B, step):
     """(exact product A·Bᵀ, element bound of the MFMA chain) for real-valued
-    operands A [R][D], B [C][D] (block scales applied), depth in steps of 128."""
+    operands A [R][D], B [C][D] (block scales applied), one instruction per
+    `step` of depth."""
     R, D = A.shape
     P = np.zeros((R, B.shape[0]))
     E = np.zeros_like(P)
-    for t0 in range(0, D, STEP):
-        At, Bt = A[:, t0:t0 + STEP], B[:, t0:t0 + STEP]
+    for t0 in range(0, D, step):
+        At, Bt = A[:, t0:t0 + step], B[:, t0:t0 + step]
         S = np.abs(At) @ np.abs(Bt).T
         E += EPS_MFMA * (np.abs(P) + S)
         P += At @ Bt.T

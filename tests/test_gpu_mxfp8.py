@@ -73,7 +73,11 @@ def _check_quantized(m, q, b, what):
     assert not scales[:, -(-m.cols // 32):cp // 32].any(), f"{what}: padding scale bytes not zero"
 
 
-SHAPES = [(512, 384, 200, 300), (1024, 2048, 256, 4096), (704, 1000, 520, 1000)]
+# (K, M, L, N).  The last two: more 256 x 256 expansion tiles than CUs (264:
+# workgroups take a second tile, whose first two steps the first one loads),
+# and a ragged width (M % 8 = 4: element-wise stores) with one depth step.
+SHAPES = [(512, 384, 200, 300), (1024, 2048, 256, 4096), (704, 1000, 520, 1000), (256, 8448, 256, 2048),
+          (300, 1100, 100, 333)]
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "K%d_M%d_L%d_N%d" % s)
@@ -93,7 +97,7 @@ def test_mxfp8_layer(E, shape):
     Z = E.espace_project_mxfp8(Pt, X)
     torch.cuda.synchronize()
     Xd, Pd, Wd = oracle.mx_dequantize(c.Xq, c.Xb), oracle.mx_dequantize(c.Pq, c.Pb), oracle.mx_dequantize(c.Wq, c.Wb)
-    Zx, Ez = MP.chain_bound(Xd, Pd)
+    Zx, Ez = MP.chain_bound(Xd, Pd, MP.STEP_PROJECT)
     assert np.allclose(Zx, oracle.mx_project(c.Xq, c.Xb, c.Pq, c.Pb), rtol=1e-12, atol=0)
     zv, zb, _, _ = MP.gpu_mx(Z)
     same = MP.check_mx_codes(Zx, Ez, zv, zb, "Z")
@@ -103,7 +107,7 @@ def test_mxfp8_layer(E, shape):
     Zo, Zob = oracle.mx_quantize(Zx)
     Zod = oracle.mx_dequantize(Zo, Zob)
     Zin = E.espace_quantize_mxfp8(dev_mat(bf16_bits_from_f64(Zod), "bf16", dev)) if _bf16_exact(Zod) else None
-    Yo, Ey = MP.chain_bound(Zod, Wd)
+    Yo, Ey = MP.chain_bound(Zod, Wd, MP.STEP_EXPAND)
     if Zin is not None:
         _check_quantized(Zin, Zo, Zob, "Z (oracle's, through the GPU quantiser)")
         Ye = E.espace_expand_mxfp8(Zin, Wf, out_mat(N, M, "bf16", dev))
@@ -190,11 +194,11 @@ def test_mxfp8_llama2_7b_qkv_sampled(E):
     rows = np.sort(np.random.default_rng(11).choice(N, 256, replace=False))
     Xd = oracle.mx_dequantize(Xq[rows], Xb[rows])
     Pd, Wd = oracle.mx_dequantize(Pq, Pb), oracle.mx_dequantize(Wq, Wb)
-    Zx, Ez = MP.chain_bound(Xd, Pd)
+    Zx, Ez = MP.chain_bound(Xd, Pd, MP.STEP_PROJECT)
     zv, zb, _, _ = MP.gpu_mx(Z, rows)
     same = MP.check_mx_codes(Zx, Ez, zv, zb, "Z")
     Zo, Zob = oracle.mx_quantize(Zx)
-    Yo, Ey = MP.chain_bound(oracle.mx_dequantize(Zo, Zob), Wd)
+    Yo, Ey = MP.chain_bound(oracle.mx_dequantize(Zo, Zob), Wd, MP.STEP_EXPAND)
     spread = MP.z_value_width(Zx, Ez) @ np.abs(Wd).T
     B = Ey + spread * (1 + 1 / 8) + MP.U_BF16 * (np.abs(Yo) + Ey + spread)
     ratio, rel = MP.check_bound(host64(Y)[rows], Yo, B, "layer")
