@@ -78,6 +78,11 @@ hipError_t launch_skinny_tn_bf16(const GemmArgs& g, hipStream_t stream);
 // splits, partial unused); gemv_supported says whether the tokens fit its LDS.
 bool gemv_supported(int R, int D);
 hipError_t launch_gemv_tn_bf16(const GemmArgs& g, hipStream_t stream);
+// Persistent streaming product for up to 16 tokens with the many-row operand
+// streamed through an LDS ring (tile, splits, partial unused); stream_supported
+// says whether the tokens and depth fit (depth up to 6144).
+bool stream_supported(int R, int D);
+hipError_t launch_stream_tn_bf16(const GemmArgs& g, hipStream_t stream);
 hipError_t launch_splitk_reduce(const float* P, int S, int64_t split_stride, int64_t ldp,
                                 void* C, int64_t ldc, int R, int Cc, int out_bf16,
                                 hipStream_t stream);

@@ -98,6 +98,24 @@ def test_decode_plans(E, shape):
     _check_entry_points(E, "bf16", shape, seed=45)
 
 
+# 3 to 16 tokens on weights of at least 16 rows per CU (the persistent
+# streaming kernel on the expansion and the dense product): a ragged last
+# group of 16 rows (4100, 8200), workgroups taking two or more groups (8200
+# rows), depths whose last 512-element piece holds 1, 131 and 188 elements
+# (the piece straddling the depth masked in registers) and the deepest
+# supported depth (6144, twelve pieces).
+STREAM_PLANS = [
+    (1600, 4100, 1537, 3),
+    (6144, 4096, 131, 8),
+    (700, 8200, 700, 16),
+]
+
+
+@pytest.mark.parametrize("shape", STREAM_PLANS, ids=lambda s: "K%d_M%d_L%d_N%d" % s)
+def test_stream_plans(E, shape):
+    _check_entry_points(E, "bf16", shape, seed=47)
+
+
 def _check_entry_points(E, dtype, shape, seed=0):
     dev = need_gpu()
     K, M, L, N = shape
