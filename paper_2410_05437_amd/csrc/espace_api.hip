@@ -132,11 +132,14 @@ Plan plan_skinny(int R, int Cc, int D, int cus) {
     // whatever its size, so the depth is split only when the tokens make
     // each workgroup's loads heavy or the depth is very large; 8 waves with
     // 6 loads in flight fit 48-step depths exactly; 32-row groups halve the
-    // token re-reads from L2 when there are 9 or more tokens.  With at most 8
-    // tokens and fewer 16-row groups than half the CUs (the projection,
+    // token re-reads from L2 when there are 9 or more tokens.  With fewer
+    // 16-row groups than half the CUs (the projection,
     // L = 1536 rows), two depth segments per MFMA operand double the
     // workgroups in one launch (K = 4096: 5.6 against 7.5 µs; K = 11008:
-    // 12.5 against 17.6 µs with a three-way split); with 128 or more groups
+    // 12.5 against 17.6 µs with a three-way split), and with 9 to 16 tokens
+    // as two token groups of 8 sharing the weight operand (K = 4096: 7.9
+    // against 8.1 µs at 16 tokens, 7.4 against 7.8 at 12, with a two-way
+    // split and its reduction launch); with 128 or more groups
     // one depth range is fastest up to 256 steps (K = 6144, L = 3686: 12.3
     // against 17.6 µs with two ranges).
     Plan p;
@@ -147,8 +150,9 @@ Plan plan_skinny(int R, int Cc, int D, int cus) {
     if (nb1 >= target) {
         if (R > 8) p.tile = espace::SKINNY_RG2_W4;
         else p.tile = (steps <= 48) ? espace::SKINNY_RG1_W8_U6 : espace::SKINNY_RG1_W8_U8;
-    } else if (R <= 8 && nb1 < cus / 2 && steps <= 384) {
-        p.tile = steps <= 128 ? espace::SKINNY_SEG2_W8_U8 : espace::SKINNY_SEG2_W16_U4;
+    } else if (R <= 16 && nb1 < cus / 2 && steps <= 384) {
+        if (R <= 8) p.tile = steps <= 128 ? espace::SKINNY_SEG2_W8_U8 : espace::SKINNY_SEG2_W16_U4;
+        else p.tile = steps <= 128 ? espace::SKINNY_SEG2_TG2_W8_U8 : espace::SKINNY_SEG2_TG2_W16_U4;
     } else {
         p.tile = espace::SKINNY_RG1_W8_U8;
         int s = R > 8 ? 2 : 1;

@@ -30,6 +30,8 @@ enum TileKind {
     SKINNY_RG1_W16_U4 = 21,
     SKINNY_SEG2_W8_U8 = 22,  // 8 rows x 2 depth segments per MFMA operand, N <= 8
     SKINNY_SEG2_W16_U4 = 23,
+    SKINNY_SEG2_TG2_W8_U8 = 24,   // the same with two groups of 8 tokens, N <= 16
+    SKINNY_SEG2_TG2_W16_U4 = 25,
 };
 
 // Limit of the bounded cross-workgroup waits and the device counter of the

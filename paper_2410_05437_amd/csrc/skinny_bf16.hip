@@ -15,7 +15,8 @@
 // write fp32 partials that a second kernel sums in a fixed order, so results
 // do not depend on scheduling.
 //
-// Depth segments (SEG = 2 or 4, at most 16/SEG tokens).  With few rows of B
+// Depth segments (SEG = 2 or 4, 16/SEG tokens per token group, one or two
+// groups).  With few rows of B
 // (the projection, L rows) 16-row groups leave most CUs idle, and a depth
 // split costs a second launch.  Instead the 16 rows of the MFMA operand are
 // 16/SEG rows of B times SEG depth segments: operand row r is row r/SEG of
@@ -24,7 +25,8 @@
 // 16x16 result hold the per-segment partial dot products; the SEG of them
 // for one (row, token) sit in SEG neighbouring lanes and are summed with
 // lane exchanges in a fixed order.  A workgroup then owns 16/SEG rows, so
-// SEG times as many workgroups share the stream, in one launch.
+// SEG times as many workgroups share the stream, in one launch.  With two
+// token groups both MFMAs of a step share the weight operand.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -41,7 +43,7 @@ void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
                            void* __restrict__ Cout, int64_t ldc,
                            int R, int Cc, int D, int steps_per_split,
                            int out_f32, int64_t split_stride) {
-    static_assert(SEG == 1 || (TG == 1 && (SEG == 2 || SEG == 4)), "segments: 2 or 4, one token group");
+    static_assert(SEG == 1 || (TG <= 2 && (SEG == 2 || SEG == 4)), "segments: 2 or 4, one or two token groups");
     constexpr int GROWS = 16 / SEG;    // rows of B per 16-row operand
     __shared__ f32x4_t red[WAVES - 1][RG * TG][64];
 
@@ -69,12 +71,13 @@ void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
         j = j < Cc ? j : Cc - 1;
         brow[g] = B + (int64_t)j * ldb;
     }
-    // token rows beyond R read row 0 and are zeroed with a mask
+    // token rows beyond R read row 0 and are zeroed with a mask; a token
+    // group holds 16 / SEG tokens
     const uint16_t* arow[TG];
     uint32_t amask[TG];
 #pragma unroll
     for (int t = 0; t < TG; ++t) {
-        const int n = t * 16 + lr / SEG;
+        const int n = t * (16 / SEG) + lr / SEG;
         amask[t] = n < R ? 0xffffffffu : 0u;
         arow[t] = A + (int64_t)(n < R ? n : 0) * lda;
     }
@@ -166,15 +169,16 @@ void skinny_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
         // column l%16.  Its diagonal entries are i = seg + SEG*c, for the
         // 4/SEG consecutive rows c; the SEG lanes of one token add theirs.
         constexpr int OUTS = 4 / SEG;
-        const int n = lr / SEG;
 #pragma unroll
-        for (int g = 0; g < RG; ++g) {
+        for (int gt = 0; gt < RG * TG; ++gt) {
+            const int g = gt / TG, t = gt % TG;
+            const int n = t * (16 / SEG) + lr / SEG;
             float d[OUTS];
 #pragma unroll
             for (int c = 0; c < OUTS; ++c) {
-                float v = acc[g][0][SEG * c];
+                float v = acc[g][t][SEG * c];
 #pragma unroll
-                for (int h = 1; h < SEG; ++h) v = seg == h ? acc[g][0][SEG * c + h] : v;
+                for (int h = 1; h < SEG; ++h) v = seg == h ? acc[g][t][SEG * c + h] : v;
                 d[c] = v;
             }
 #pragma unroll
@@ -237,7 +241,7 @@ template <int RG, int TG, int WAVES, int UNROLL, int SEG = 1>
 hipError_t launch_skinny_cfg(const GemmArgs& g, hipStream_t stream) {
     const int nsteps = ((g.D + STEP - 1) / STEP + SEG - 1) / SEG;
     const int S = g.splits;
-    if (SEG > 1 && (S != 1 || g.R > 16 / SEG)) return hipErrorInvalidValue;
+    if (SEG > 1 && (S != 1 || g.R > TG * (16 / SEG))) return hipErrorInvalidValue;
     const int sps = (nsteps + S - 1) / S;
     const int rows = 16 / SEG * RG;
     dim3 grid((g.Cc + rows - 1) / rows, S);
@@ -284,6 +288,8 @@ hipError_t launch_skinny_tn_bf16(const GemmArgs& g, hipStream_t stream) {
         case SKINNY_RG1_W16_U4: return launch_skinny_tg<1, 16, 4>(g, stream);
         case SKINNY_SEG2_W8_U8: return launch_skinny_cfg<1, 1, 8, 8, 2>(g, stream);
         case SKINNY_SEG2_W16_U4: return launch_skinny_cfg<1, 1, 16, 4, 2>(g, stream);
+        case SKINNY_SEG2_TG2_W8_U8: return launch_skinny_cfg<1, 2, 8, 8, 2>(g, stream);
+        case SKINNY_SEG2_TG2_W16_U4: return launch_skinny_cfg<1, 2, 16, 4, 2>(g, stream);
         default: return hipErrorInvalidValue;
     }
 }

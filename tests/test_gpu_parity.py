@@ -75,9 +75,15 @@ DEGENERATE = [
 # 1003, 1536, 131 and 136), two depth segments per MFMA operand with 16 waves (the
 # projection at 8 tokens, 9 row groups over 141 steps) and with 8 waves (its
 # expansion, 57 row groups over 5 steps); one depth range of 132 steps for 132
-# row groups (3 and 5 tokens).
+# row groups (3 and 5 tokens); two depth segments with two token groups of
+# eight (9 to 16 tokens: 12 tokens on the 141-step projection with 16 waves,
+# 16 tokens on a 125-step projection and its 10-step expansion with 8 waves,
+# 9 tokens, the second group holding one, over 32 and 5 steps).
 DECODE_PLANS = [
     (4500, 900, 136, 8),
+    (4500, 900, 136, 12),
+    (4000, 700, 300, 16),
+    (1003, 517, 131, 9),
     (4500, 900, 136, 1),
     (4500, 700, 1536, 2),
     (4500, 2100, 4200, 3),
@@ -103,11 +109,14 @@ def test_decode_plans(E, shape):
 # group of 16 rows (4100, 8200), workgroups taking two or more groups (8200
 # rows), depths whose last 512-element piece holds 1, 131 and 188 elements
 # (the piece straddling the depth masked in registers) and the deepest
-# supported depth (6144, twelve pieces).
+# supported depth (6144, twelve pieces); workgroups with one group more than
+# others (5000 and 22016 rows: 313 and 1376 groups over the CUs).
 STREAM_PLANS = [
     (1600, 4100, 1537, 3),
     (6144, 4096, 131, 8),
     (700, 8200, 700, 16),
+    (1000, 5000, 700, 5),
+    (2000, 22016, 1536, 16),
 ]
 
 
