@@ -16,10 +16,13 @@
 //   loads of step + 2 between them; persistent tiles, the next tile's first
 //   two steps loaded during the last two of the current one.
 // * The projection (MX-FP8 output, a few hundred tiles at most) runs a
-//   two-stage kernel on v_mfma_scale_f32_16x16x128_f8f6f4 with tiles small
-//   enough to give every CU work (128 x 128 tiles, two workgroups per CU, for
-//   the 4096 x 1536 projections: 43 us against 54-60 us with the pipelined
-//   kernel's 256 x 128 or 256 x 256 tiles on 192 or 96 CUs).
+//   simpler kernel on v_mfma_scale_f32_16x16x128_f8f6f4 with tiles small
+//   enough to give every CU work: for the 4096 x 1536 projections 128 x 192
+//   tiles (256 of them) with three LDS stages, the loads of a step issued two
+//   steps ahead (measured on operands rotated through HBM: 38 against 41 us
+//   with 128 x 128 tiles on two stages and two workgroups per CU at depth
+//   4096, 110 against 131 us at depth 11008; the pipelined kernel's 256 x 128
+//   or 256 x 256 tiles on 192 or 96 CUs took 54-60 us at depth 4096).
 //
 // v_mfma_scale_f32_32x32x64_f8f6f4 (operands "A" then "B"), as measured on
 // the device:
@@ -118,35 +121,46 @@ constexpr int MX_BK = 128;   // depth of one step: one block-scaled MFMA
 // fragment read touches then fall on distinct bank groups
 __device__ __forceinline__ int mx_swz(int r) { return (r >> 1) & 7; }
 
-// Tile BT tokens x BW output columns, 4 waves as 2 x 2, each BT/2 x BW/2.
-// A stage holds the tile's BT + BW rows of 128 code bytes (token rows first),
-// then one scale dword (the 4 blocks of the step) per row.
-template <int BT, int BW>
+// Tile BT tokens x BW output columns, 4 waves as 2 x 2, each BT/2 x BW/2,
+// NS LDS stages (the loads of step t + NS - 1 are issued at the start of
+// step t).  A stage holds the tile's BT + BW rows of 128 code bytes (token
+// rows first), then one scale dword (the 4 blocks of the step) per row.
+template <int BT, int BW, int NS>
 struct MxZCfg {
     static constexpr int ROWS = BT + BW;
     static constexpr int DATA = ROWS * MX_BK;
     static constexpr int STAGE = DATA + ROWS * 4;
-    static constexpr int SMEM = 2 * STAGE;
+    static constexpr int SMEM = NS * STAGE;
     static constexpr int WT = BT / 2, WW = BW / 2;
     static constexpr int NI = WT / 16, NJ = WW / 16;
     static constexpr int NDL = ROWS / 8;    // 1 KB code loads per stage (8 rows each)
     static constexpr int NSL = ROWS / 64;   // 256-byte scale loads per stage (64 rows each)
+    static constexpr int LPD = NDL / 4;     // code loads per wave and stage
+    static constexpr int LPS = (NSL + 3) / 4;   // scale loads per wave (uniform: extra ones repeat a load)
+    static constexpr int LPW = LPD + LPS;
     static_assert(BT % 64 == 0 && BW % 64 == 0 && NDL % 4 == 0, "tile");
+    static_assert((NS == 2 || NS == 3) && (NS - 2) * LPW < 64 && SMEM <= 160 * 1024, "stages");
 };
+
+// s_barrier that the compiler moves no memory access across (the loads of
+// other waves into LDS are invisible to it), after this wave's LDS reads
+// have completed; unlike __syncthreads() it does not wait for this wave's
+// loads still in flight
+__device__ __forceinline__ void mx_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // Issue the direct-to-LDS loads of depth step t into `stage`: codes (16
 // bytes per lane) and scale dwords (4 bytes per lane).  Rows past the matrix
 // read its last row (their results are never stored).
-template <int BT, int BW>
+template <int BT, int BW, int NS>
 __device__ __forceinline__ void mx_issue(unsigned char* stage, const MxGemmArgs& a, int row0, int col0, int t,
                                          int wave, int lane) {
-    using C = MxZCfg<BT, BW>;
+    using C = MxZCfg<BT, BW, NS>;
     const auto tr = __builtin_amdgcn_make_buffer_rsrc((void*)a.T, (short)0, (int)(a.R * a.ldt), 0x00020000);
     const auto wr = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, (short)0, (int)(a.C * a.ldw), 0x00020000);
     const auto ts = __builtin_amdgcn_make_buffer_rsrc((void*)a.Ts, (short)0, (int)(a.R * a.ldts), 0x00020000);
     const auto ws = __builtin_amdgcn_make_buffer_rsrc((void*)a.Ws, (short)0, (int)(a.C * a.ldws), 0x00020000);
 #pragma unroll
-    for (int j = 0; j < C::NDL / 4; ++j) {
+    for (int j = 0; j < C::LPD; ++j) {
         const int q = wave + 4 * j;
         const int rr = 8 * q + (lane >> 3);
         const int c = (lane & 7) ^ mx_swz(rr);
@@ -160,7 +174,9 @@ __device__ __forceinline__ void mx_issue(unsigned char* stage, const MxGemmArgs&
                                                      (int)(g * a.ldw + 16 * c), t * MX_BK, 0, 0);
         }
     }
-    for (int s = wave; s < C::NSL; s += 4) {
+#pragma unroll
+    for (int j = 0; j < C::LPS; ++j) {
+        const int s = (wave + 4 * j) % C::NSL;
         const int rr = 64 * s + lane;
         if (64 * s < BT) {
             const int g = min(row0 + rr, a.R - 1);
@@ -183,14 +199,12 @@ __device__ __forceinline__ i32x8_t mx_frag(const unsigned char* stage, int rr, i
     return i32x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
 }
 
-__device__ __forceinline__ void mx_wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-
 // Tile BT tokens x BW columns, MX-FP8 output along the columns (codes and
 // one scale byte per 32 columns, up to cpad columns); one workgroup per tile.
-template <int BT, int BW>
+template <int BT, int BW, int NS>
 __global__ __launch_bounds__(256, (BT + BW) <= 256 ? 2 : 1)
 void gemm_mx_z_kernel(MxGemmArgs a) {
-    using C = MxZCfg<BT, BW>;
+    using C = MxZCfg<BT, BW, NS>;
     __shared__ __attribute__((aligned(1024))) unsigned char smem[C::SMEM];
 
     const int tiles_c = (a.C + BW - 1) / BW;
@@ -211,14 +225,19 @@ void gemm_mx_z_kernel(MxGemmArgs a) {
         for (int j = 0; j < C::NJ; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     const int steps = (a.D + MX_BK - 1) / MX_BK;
-    mx_issue<BT, BW>(smem, a, row0, col0, 0, wave, lane);
-    mx_wait_vm0();
-    __syncthreads();
+    for (int t = 0; t < NS - 1 && t < steps; ++t)
+        mx_issue<BT, BW, NS>(smem + t * C::STAGE, a, row0, col0, t, wave, lane);
     for (int t = 0; t < steps; ++t) {
-        const unsigned char* cur = smem + (t & 1) * C::STAGE;
-        // the other stage was last read in step t - 1, before the barrier
-        // that ended it
-        if (t + 1 < steps) mx_issue<BT, BW>(smem + ((t + 1) & 1) * C::STAGE, a, row0, col0, t + 1, wave, lane);
+        // this wave's loads of step t have landed (those of the newer steps
+        // may stay in flight); after the barrier every wave's have, and
+        // every wave is done with step t - 1, whose stage receives step
+        // t + NS - 1
+        if (NS == 3 && t + 1 < steps) v3_wait_vm<(NS - 2) * C::LPW>();
+        else v3_wait_vm<0>();
+        mx_barrier();
+        if (t + NS - 1 < steps)
+            mx_issue<BT, BW, NS>(smem + ((t + NS - 1) % NS) * C::STAGE, a, row0, col0, t + NS - 1, wave, lane);
+        const unsigned char* cur = smem + (t % NS) * C::STAGE;
         i32x8_t tf[C::NI];
         int tsc[C::NI];
 #pragma unroll
@@ -237,10 +256,6 @@ void gemm_mx_z_kernel(MxGemmArgs a) {
                 acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(wf, tf[i], acc[i][j], 0, 0, 0, wsc, 0,
                                                                             tsc[i]);
         }
-        // step t + 1 has landed in the other stage, and every wave is done
-        // with this one before the next step's loads overwrite it
-        mx_wait_vm0();
-        __syncthreads();
     }
 
     // ---- epilogue: lane holds token row wt0 + 16 i + lr, output columns
@@ -794,10 +809,10 @@ hipError_t launch_pipelined(const MxGemmArgs& a, int cus, hipStream_t stream) {
     return hipGetLastError();
 }
 
-template <int BT, int BW>
+template <int BT, int BW, int NS>
 hipError_t launch_z(const MxGemmArgs& a, hipStream_t stream) {
     const int tiles = ((a.R + BT - 1) / BT) * ((a.C + BW - 1) / BW);
-    hipLaunchKernelGGL((gemm_mx_z_kernel<BT, BW>), dim3(tiles), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL((gemm_mx_z_kernel<BT, BW, NS>), dim3(tiles), dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -807,9 +822,13 @@ int mx_gemm_tile(int R, int C, int cus, int out_mx) {
     const long long t256 = (long long)((R + 255) / 256) * ((C + 255) / 256);
     const long long t128 = (long long)((R + 255) / 256) * ((C + 127) / 128);
     if (out_mx) {
-        // the largest tile that still gives every CU a tile, else the smallest
+        // the largest tile that still gives every CU a tile; else 128 x 192
+        // tiles with three stages when they make one round on more than half
+        // of the CUs; else the smallest
+        const long long t192 = (long long)((R + 127) / 128) * ((C + 191) / 192);
         if (t256 >= cus) return 0;
         if (t128 >= cus) return 1;
+        if (2 * t192 > cus && t192 <= cus) return 3;
         return 2;
     }
     // 256 x 256 tiles when they give every CU a tile or when 256 x 128 tiles
@@ -827,9 +846,10 @@ hipError_t launch_gemm_mx(const MxGemmArgs& a, int out_mx, int cus, hipStream_t 
     const int tile = mx_gemm_tile(a.R, a.C, cus, out_mx);
     if (out_mx) {
         switch (tile) {
-            case 0: return launch_z<256, 256>(a, stream);
-            case 1: return launch_z<256, 128>(a, stream);
-            default: return launch_z<128, 128>(a, stream);
+            case 0: return launch_z<256, 256, 2>(a, stream);
+            case 1: return launch_z<256, 128, 2>(a, stream);
+            case 3: return launch_z<128, 192, 3>(a, stream);
+            default: return launch_z<128, 128, 2>(a, stream);
         }
     }
     return tile == 0 ? launch_pipelined<256>(a, cus, stream) : launch_pipelined<128>(a, cus, stream);

@@ -73,11 +73,14 @@ def _check_quantized(m, q, b, what):
     assert not scales[:, -(-m.cols // 32):cp // 32].any(), f"{what}: padding scale bytes not zero"
 
 
-# (K, M, L, N).  The last two: more 256 x 256 expansion tiles than CUs (264:
-# workgroups take a second tile, whose first two steps the first one loads),
-# and a ragged width (M % 8 = 4: element-wise stores) with one depth step.
+# (K, M, L, N).  The fourth and fifth: more 256 x 256 expansion tiles than CUs
+# (264: workgroups take a second tile, whose first two steps the first one
+# loads), and a ragged width (M % 8 = 4: element-wise stores) with one depth
+# step.  The last three: projections on 128 x 192 tiles with three stages
+# (between 128 and 256 tiles): ragged tokens, width and depth over 25 steps,
+# and depths of two steps and one step.
 SHAPES = [(512, 384, 200, 300), (1024, 2048, 256, 4096), (704, 1000, 520, 1000), (256, 8448, 256, 2048),
-          (300, 1100, 100, 333)]
+          (300, 1100, 100, 333), (3100, 256, 3000, 2000), (250, 200, 200, 9000), (100, 64, 100, 20000)]
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "K%d_M%d_L%d_N%d" % s)
