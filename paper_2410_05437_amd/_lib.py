@@ -443,10 +443,12 @@ class MXTensor:
 
 
 def mx_empty(rows, cols, device):
-    """Uninitialised MX-FP8 matrix with the smallest leading dimensions."""
+    """Uninitialised MX-FP8 matrix: codes at the smallest leading dimension,
+    scale rows padded to 16 bytes (the layout the kernels load fastest)."""
     cp = (cols + 127) // 128 * 128
+    lds = (cp // 32 + 15) // 16 * 16
     return MXTensor(torch.empty((rows, cp), dtype=torch.uint8, device=device),
-                    torch.empty((rows, cp // 32), dtype=torch.uint8, device=device), cols)
+                    torch.empty((rows, lds), dtype=torch.uint8, device=device)[:, :cp // 32], cols)
 
 
 def _mx(m, name, rows=None, cols=None):

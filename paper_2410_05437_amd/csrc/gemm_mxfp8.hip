@@ -9,7 +9,8 @@
 //   pipeline (gemm_bf16_v3.hip) on fp8 operands: a depth step of 128 codes is
 //   two sub-steps of 64, each with its own LDS half-stage of 64-byte rows laid
 //   out exactly as the bf16 kernel's (same loads, same chunk swizzle), plus
-//   one scale dword per row (the four 32-blocks of the step).  Per sub-step a
+//   one scale dword per row (the four 32-blocks of the step), loaded with
+//   the first half-stage only.  Per sub-step a
 //   wave issues NI x NJ v_mfma_scale_f32_32x32x64_f8f6f4 (16 for the
 //   256 x 256 tile, as long on the matrix pipe as the bf16 kernel's 64
 //   16x16x32 MFMAs) with the fragment reads of the next sub-step and the
@@ -68,26 +69,31 @@ typedef int i32x4_t __attribute__((ext_vector_type(4)));
 // Tile 256 tokens x BW output columns (BW = 256 or 128), four waves as 2 x 2,
 // each owning 128 tokens x BW/2 columns as NI x NJ blocks of 32 x 32.  The
 // code half-stages are the bf16 kernel's (V3Cfg<BW>: token rows first, 64
-// bytes each); after the four of them, four scale areas of one dword per
-// row.
+// bytes each); after the four of them, two scale areas of one dword per row,
+// one per stage (the scale loads of a step go with its first half-stage: a
+// scale load gathers 64 rows, one memory line each; loaded with both halves
+// they took 88 against 82 us on the 4096 x 12288 x 1536 expansion).
 template <int BW>
 struct MxCfg {
     using V = V3Cfg<BW>;
     static constexpr int NI = 4, NJ = BW / 64;
     static constexpr int ROWS = V::ROWS;
-    static constexpr int SCB = ROWS * 4;              // scale bytes of a half-stage
-    static constexpr int NSC = ROWS / 64;             // 256-byte scale loads per half-stage
+    static constexpr int SCB = ROWS * 4;              // scale bytes of a stage
+    static constexpr int NSC = ROWS / 64;             // 256-byte scale loads per stage
     static constexpr int LSC = (NSC + 3) / 4;         // per wave (uniform: extra ones repeat a load)
-    static constexpr int LPH = V::LPH + LSC;          // loads per wave and half-stage
+    // loads per wave of a step's first half-stage (codes, and the step's
+    // scale dwords, which only that half's area receives) and of its second
+    static constexpr int LPH0 = V::LPH + LSC, LPH1 = V::LPH;
+    static constexpr int LPS = LPH0 + LPH1;           // per step
     static constexpr int NMF = NI * NJ;               // MFMAs per sub-step
     static constexpr int NRD = 2 * (NI + NJ);         // code fragment reads per sub-step
     static constexpr int NSR = NI + NJ;               // scale dword reads per step
     static constexpr int NST = 2 * NI * NJ;           // 16-byte stores per wave (bf16 output)
-    static constexpr int SMEM = 4 * V::HS + 4 * SCB;
+    static constexpr int SMEM = 4 * V::HS + 2 * SCB;
     static_assert(BW == 256 || BW == 128, "tile");
-    static_assert(2 * LPH + NST < 64 && 3 * LPH + NST < 64, "vmcnt");
-    // MFMA after which load y of a sub-step is issued
-    static constexpr int load_slot(int y) { return y * NMF / LPH + NMF / (2 * LPH); }
+    static_assert(LPS + NST < 64, "vmcnt");
+    // MFMA after which load y of a sub-step's n is issued
+    static constexpr int load_slot(int y, int n) { return y * NMF / n + NMF / (2 * n); }
     // MFMA after which read x of a sub-step is issued (n reads in all)
     static constexpr int read_slot(int x, int n) { return x * NMF / n; }
 };
@@ -124,13 +130,20 @@ __device__ __forceinline__ int mx_swz(int r) { return (r >> 1) & 7; }
 // Tile BT tokens x BW output columns, 4 waves as 2 x 2, each BT/2 x BW/2,
 // NS LDS stages (the loads of step t + NS - 1 are issued at the start of
 // step t).  A stage holds the tile's BT + BW rows of 128 code bytes (token
-// rows first), then one scale dword (the 4 blocks of the step) per row.
-template <int BT, int BW, int NS>
+// rows first).  The scale dwords (the 4 blocks of a step) of SS steps are
+// loaded together: SS = 1, one dword per row after the codes of each stage;
+// SS = 4 (scale rows 16-byte aligned), 16 bytes per row into one of two
+// areas after the stages, with the codes of every fourth step.  A scale load
+// gathers 64 rows, one memory line each, so a quarter of them as 16-byte
+// loads saves most of their cost (4096 x 1536 projections: 37.6 -> 36.7 us
+// at depth 4096, 107.7 -> 89.6 us at depth 11008).
+template <int BT, int BW, int NS, int SS>
 struct MxZCfg {
     static constexpr int ROWS = BT + BW;
     static constexpr int DATA = ROWS * MX_BK;
-    static constexpr int STAGE = DATA + ROWS * 4;
-    static constexpr int SMEM = NS * STAGE;
+    static constexpr int STAGE = SS == 1 ? DATA + ROWS * 4 : DATA;
+    static constexpr int SAREA = ROWS * 16;           // four steps' scale dwords (SS = 4)
+    static constexpr int SMEM = NS * STAGE + (SS == 1 ? 0 : 2 * SAREA);
     static constexpr int WT = BT / 2, WW = BW / 2;
     static constexpr int NI = WT / 16, NJ = WW / 16;
     static constexpr int NDL = ROWS / 8;    // 1 KB code loads per stage (8 rows each)
@@ -140,6 +153,12 @@ struct MxZCfg {
     static constexpr int LPW = LPD + LPS;
     static_assert(BT % 64 == 0 && BW % 64 == 0 && NDL % 4 == 0, "tile");
     static_assert((NS == 2 || NS == 3) && (NS - 2) * LPW < 64 && SMEM <= 160 * 1024, "stages");
+    static_assert(SS == 1 || SS == 4, "scale steps");
+    // whether step t's loads include scales, and where step t's scale bytes are
+    static __device__ __forceinline__ bool scales_with(int t) { return SS == 1 || (t & 3) == 0; }
+    static __device__ __forceinline__ int scale_area(int t) {
+        return SS == 1 ? (t % NS) * STAGE + DATA : NS * STAGE + ((t >> 2) & 1) * SAREA;
+    }
 };
 
 // s_barrier that the compiler moves no memory access across (the loads of
@@ -148,13 +167,16 @@ struct MxZCfg {
 // loads still in flight
 __device__ __forceinline__ void mx_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// Issue the direct-to-LDS loads of depth step t into `stage`: codes (16
-// bytes per lane) and scale dwords (4 bytes per lane).  Rows past the matrix
-// read its last row (their results are never stored).
-template <int BT, int BW, int NS>
-__device__ __forceinline__ void mx_issue(unsigned char* stage, const MxGemmArgs& a, int row0, int col0, int t,
+// Issue the direct-to-LDS loads of depth step t into its stage: codes (16
+// bytes per lane) and, with the steps that carry them, scale dwords (4 or 16
+// bytes per lane).  Rows past the matrix read its last row (their results
+// are never stored); the 16-byte scale loads of a last group may read past
+// the matrix's steps (bytes never used; past the buffer they read zeros).
+template <int BT, int BW, int NS, int SS>
+__device__ __forceinline__ void mx_issue(unsigned char* smem, const MxGemmArgs& a, int row0, int col0, int t,
                                          int wave, int lane) {
-    using C = MxZCfg<BT, BW, NS>;
+    using C = MxZCfg<BT, BW, NS, SS>;
+    unsigned char* stage = smem + (t % NS) * C::STAGE;
     const auto tr = __builtin_amdgcn_make_buffer_rsrc((void*)a.T, (short)0, (int)(a.R * a.ldt), 0x00020000);
     const auto wr = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, (short)0, (int)(a.C * a.ldw), 0x00020000);
     const auto ts = __builtin_amdgcn_make_buffer_rsrc((void*)a.Ts, (short)0, (int)(a.R * a.ldts), 0x00020000);
@@ -174,19 +196,21 @@ __device__ __forceinline__ void mx_issue(unsigned char* stage, const MxGemmArgs&
                                                      (int)(g * a.ldw + 16 * c), t * MX_BK, 0, 0);
         }
     }
+    if (!C::scales_with(t)) return;
+    unsigned char* area = smem + C::scale_area(t);
 #pragma unroll
     for (int j = 0; j < C::LPS; ++j) {
         const int s = (wave + 4 * j) % C::NSL;
         const int rr = 64 * s + lane;
-        if (64 * s < BT) {
-            const int g = min(row0 + rr, a.R - 1);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(ts, (__attribute__((address_space(3))) void*)(stage + C::DATA + s * 256),
-                                                     4, (int)(g * a.ldts), 4 * t, 0, 0);
-        } else {
-            const int g = min(col0 + rr - BT, a.C - 1);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(ws, (__attribute__((address_space(3))) void*)(stage + C::DATA + s * 256),
-                                                     4, (int)(g * a.ldws), 4 * t, 0, 0);
-        }
+        const bool tok = 64 * s < BT;
+        const int g = tok ? min(row0 + rr, a.R - 1) : min(col0 + rr - BT, a.C - 1);
+        const int off = g * (int)(tok ? a.ldts : a.ldws);
+        if constexpr (SS == 1)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(tok ? ts : ws, (__attribute__((address_space(3))) void*)(area + s * 256),
+                                                     4, off, 4 * t, 0, 0);
+        else
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(tok ? ts : ws, (__attribute__((address_space(3))) void*)(area + s * 1024),
+                                                     16, off, 4 * t, 0, 0);
     }
 }
 
@@ -201,10 +225,10 @@ __device__ __forceinline__ i32x8_t mx_frag(const unsigned char* stage, int rr, i
 
 // Tile BT tokens x BW columns, MX-FP8 output along the columns (codes and
 // one scale byte per 32 columns, up to cpad columns); one workgroup per tile.
-template <int BT, int BW, int NS>
+template <int BT, int BW, int NS, int SS>
 __global__ __launch_bounds__(256, (BT + BW) <= 256 ? 2 : 1)
 void gemm_mx_z_kernel(MxGemmArgs a) {
-    using C = MxZCfg<BT, BW, NS>;
+    using C = MxZCfg<BT, BW, NS, SS>;
     __shared__ __attribute__((aligned(1024))) unsigned char smem[C::SMEM];
 
     const int tiles_c = (a.C + BW - 1) / BW;
@@ -225,32 +249,36 @@ void gemm_mx_z_kernel(MxGemmArgs a) {
         for (int j = 0; j < C::NJ; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     const int steps = (a.D + MX_BK - 1) / MX_BK;
-    for (int t = 0; t < NS - 1 && t < steps; ++t)
-        mx_issue<BT, BW, NS>(smem + t * C::STAGE, a, row0, col0, t, wave, lane);
+    for (int t = 0; t < NS - 1 && t < steps; ++t) mx_issue<BT, BW, NS, SS>(smem, a, row0, col0, t, wave, lane);
     for (int t = 0; t < steps; ++t) {
         // this wave's loads of step t have landed (those of the newer steps
         // may stay in flight); after the barrier every wave's have, and
         // every wave is done with step t - 1, whose stage receives step
-        // t + NS - 1
-        if (NS == 3 && t + 1 < steps) v3_wait_vm<(NS - 2) * C::LPW>();
-        else v3_wait_vm<0>();
+        // t + NS - 1 (and whose scale area, with four-step groups, is not
+        // rewritten before step t + 4)
+        if (NS == 3 && t + 1 < steps) {
+            if (C::scales_with(t + 1)) v3_wait_vm<C::LPW>();
+            else v3_wait_vm<C::LPD>();
+        } else {
+            v3_wait_vm<0>();
+        }
         mx_barrier();
-        if (t + NS - 1 < steps)
-            mx_issue<BT, BW, NS>(smem + ((t + NS - 1) % NS) * C::STAGE, a, row0, col0, t + NS - 1, wave, lane);
+        if (t + NS - 1 < steps) mx_issue<BT, BW, NS, SS>(smem, a, row0, col0, t + NS - 1, wave, lane);
         const unsigned char* cur = smem + (t % NS) * C::STAGE;
+        const unsigned char* sc = smem + C::scale_area(t) + (SS == 1 ? 0 : 4 * (t & 3));
         i32x8_t tf[C::NI];
         int tsc[C::NI];
 #pragma unroll
         for (int i = 0; i < C::NI; ++i) {
             const int rr = wt0 + 16 * i + lr;
             tf[i] = mx_frag(cur, rr, lane);
-            tsc[i] = cur[C::DATA + 4 * rr + q];
+            tsc[i] = sc[4 * SS * rr + q];
         }
 #pragma unroll
         for (int j = 0; j < C::NJ; ++j) {
             const int rr = BT + ww0 + 16 * j + lr;
             const i32x8_t wf = mx_frag(cur, rr, lane);
-            const int wsc = cur[C::DATA + 4 * rr + q];
+            const int wsc = sc[4 * SS * rr + q];
 #pragma unroll
             for (int i = 0; i < C::NI; ++i)
                 acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(wf, tf[i], acc[i][j], 0, 0, 0, wsc, 0,
@@ -405,7 +433,7 @@ struct MxLoad {
             const auto rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(tok ? Ts : Ws), (short)0,
                                                                 (int)(tok ? tsbytes : wsbytes), 0x00020000);
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rsrc, (__attribute__((address_space(3))) void*)(smem + 4 * C::V::HS + u * C::SCB + 256 * s), 4,
+                rsrc, (__attribute__((address_space(3))) void*)(smem + 4 * C::V::HS + (u >> 1) * C::SCB + 256 * s), 4,
                 soff[j], 4 * kt, 0, 0);
         }
     }
@@ -414,8 +442,9 @@ struct MxLoad {
 // One sub-step: NMF MFMAs on (cur, the shifted scales tsc / wsc) with
 // op_sel_hi SEL; between them the NRD code reads of the next sub-step into
 // nxt from rd, with SREADS also the NSR scale dwords of the next step from
-// sd into tsr / wsr, and with do_load the LPH loads of half h of step lkt
-// into half-stage u.  FIRST: the accumulators start from zero.
+// sd into tsr / wsr, and with do_load the loads of half h of step lkt into
+// half-stage u (h = SEL1: LPH0 loads in sub-step 0, LPH1 in sub-step 1).
+// FIRST: the accumulators start from zero.
 template <int BW, bool FIRST, bool SEL1, bool SREADS>
 __device__ __forceinline__ void mx_substep(f32x16_t (&acc)[4][BW / 64], const MxFrag<BW / 64>& cur,
                                            const int* tsc, const int* wsc, MxFrag<BW / 64>& nxt,
@@ -445,25 +474,27 @@ __device__ __forceinline__ void mx_substep(f32x16_t (&acc)[4][BW / 64], const Mx
                     if (x < C::NRD) mx_read<NJ>(x, nxt, rd);
                     else mx_read_scale<NJ>(x - C::NRD, tsr, wsr, sd);
                 }
+            constexpr int NL = SEL1 ? C::LPH1 : C::LPH0;
 #pragma unroll
-            for (int y = 0; y < C::LPH; ++y)
-                if (C::load_slot(y) == m && do_load) ld.load(smem, lkt, h, u, y);
+            for (int y = 0; y < NL; ++y)
+                if (C::load_slot(y, NL) == m && do_load) ld.load(smem, lkt, h, u, y);
         }
 }
 
-// vmcnt(n) for the counts the steps need (k sub-steps of LPH loads, plus the
-// previous tile's NST stores); any other n waits for everything
+// vmcnt(n) for the counts the steps need (half-steps of LPH0 and LPH1
+// loads, plus the previous tile's NST stores); any other n waits for
+// everything
 template <class C>
 __device__ __forceinline__ void mx_wait_vm_n(int n) {
-    constexpr int L = C::LPH, S = C::NST;
+    constexpr int L0 = C::LPH0, L1 = C::LPH1, S = C::NST;
     if (n == 0) v3_wait_vm<0>();
-    else if (n == L) v3_wait_vm<L>();
-    else if (n == 2 * L) v3_wait_vm<2 * L>();
-    else if (n == 3 * L) v3_wait_vm<3 * L>();
+    else if (n == L0) v3_wait_vm<L0>();
+    else if (n == L1) v3_wait_vm<L1>();
+    else if (n == L0 + L1) v3_wait_vm<L0 + L1>();
     else if (n == S) v3_wait_vm<S>();
-    else if (n == L + S) v3_wait_vm<L + S>();
-    else if (n == 2 * L + S) v3_wait_vm<2 * L + S>();
-    else if (n == 3 * L + S) v3_wait_vm<3 * L + S>();
+    else if (n == S + L0) v3_wait_vm<S + L0>();
+    else if (n == S + L1) v3_wait_vm<S + L1>();
+    else if (n == S + L0 + L1) v3_wait_vm<S + L0 + L1>();
     else v3_wait_vm<0>();
 }
 
@@ -531,8 +562,8 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
         m.th = trow + c_hi + (unsigned)(u * V::HS);
         m.wl = wrow + c_lo + (unsigned)(u * V::HS);
         m.wh = wrow + c_hi + (unsigned)(u * V::HS);
-        m.ts = tsca + (unsigned)(u * C::SCB);
-        m.ws = wsca + (unsigned)(u * C::SCB);
+        m.ts = tsca + (unsigned)((u >> 1) * C::SCB);   // a stage's scale area (first half-stages only)
+        m.ws = wsca + (unsigned)((u >> 1) * C::SCB);
         return m;
     };
     const int shift = 8 * lh;                         // block lh of a sub-step at byte 0 (or 2)
@@ -561,22 +592,22 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
         if (ahead) {
             // the first step's loads, then the second's and the previous
             // tile's stores were issued
-            v3_wait_vm<2 * C::LPH + C::NST>();
+            v3_wait_vm<C::LPS + C::NST>();
         } else {
             // the half-stages may still be read by a wave finishing the previous tile
             if (item != (int)blockIdx.x) __syncthreads();
             v3_offsets<V>(ld.voff, row0, col0, a.R, a.C, a.ldt / 2, a.ldw / 2, wave, lane);
             ld.scale_offsets(a, row0, col0, lane);
 #pragma unroll
-            for (int y = 0; y < C::LPH; ++y) ld.load(smem, 0, 0, hs(0, 0), y);
+            for (int y = 0; y < C::LPH0; ++y) ld.load(smem, 0, 0, hs(0, 0), y);
 #pragma unroll
-            for (int y = 0; y < C::LPH; ++y) ld.load(smem, 0, 1, hs(0, 1), y);
+            for (int y = 0; y < C::LPH1; ++y) ld.load(smem, 0, 1, hs(0, 1), y);
             if (ktiles > 1) {
 #pragma unroll
-                for (int y = 0; y < C::LPH; ++y) ld.load(smem, 1, 0, hs(1, 0), y);
+                for (int y = 0; y < C::LPH0; ++y) ld.load(smem, 1, 0, hs(1, 0), y);
 #pragma unroll
-                for (int y = 0; y < C::LPH; ++y) ld.load(smem, 1, 1, hs(1, 1), y);
-                v3_wait_vm<2 * C::LPH>();
+                for (int y = 0; y < C::LPH1; ++y) ld.load(smem, 1, 1, hs(1, 1), y);
+                v3_wait_vm<C::LPS>();
             } else {
                 v3_wait_vm<0>();
             }
@@ -630,11 +661,11 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
             const bool k0 = load_kind(0, lkt);
             mx_substep<BW, F, false, false>(acc, f0, tsc, wsc, f1, rel ? A3 : A1, A0, tsr, wsr, smem, ld, lkt, 0,
                                             hs(rel, 0), k0);
-            const int n0 = k0 ? C::LPH : 0;
+            const int n0 = k0 ? C::LPH0 : 0;
             v3_wait_lgkm0();
             if (kt + 1 < ktiles || ahead_next) {
                 // the next step's first half has landed (the loads just issued may stay in flight)
-                if (kt + 1 < ktiles) mx_wait_vm_n<C>(C::LPH + stores + n0);
+                if (kt + 1 < ktiles) mx_wait_vm_n<C>(C::LPH1 + stores + n0);
                 __builtin_amdgcn_s_barrier();
             }
             // sub-step 1: fragments and scales of the next step's sub-step 0
@@ -642,7 +673,7 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
             const bool k1 = load_kind(1, lkt);
             mx_substep<BW, false, true, true>(acc, f1, tsc, wsc, f0, rel ? A0 : A2, rel ? A0 : A2, tsr, wsr, smem,
                                               ld, lkt, 1, hs(rel, 1), k1);
-            const int n1 = k1 ? C::LPH : 0;
+            const int n1 = k1 ? C::LPH1 : 0;
             v3_wait_lgkm0();
             if (kt + 1 < ktiles) {
                 // the next step's second half has landed
@@ -662,23 +693,23 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
             mx_substep<BW, false, false, false>(acc, f0, tsc, wsc, f1, A3, A3, tsr, wsr, smem, ld, kt + 2, 0,
                                                 hs(1, 0), true);
             v3_wait_lgkm0();
-            v3_wait_vm<2 * C::LPH>();
+            v3_wait_vm<C::LPS>();
             __builtin_amdgcn_s_barrier();
             mx_substep<BW, false, true, true>(acc, f1, tsc, wsc, f0, A0, A0, tsr, wsr, smem, ld, kt + 2, 1,
                                               hs(1, 1), true);
             v3_wait_lgkm0();
-            v3_wait_vm<2 * C::LPH>();
+            v3_wait_vm<C::LPS>();
             __builtin_amdgcn_s_barrier();
             shift_scales();
             mx_substep<BW, false, false, false>(acc, f0, tsc, wsc, f1, A1, A1, tsr, wsr, smem, ld, kt + 3, 0,
                                                 hs(0, 0), true);
             v3_wait_lgkm0();
-            v3_wait_vm<2 * C::LPH>();
+            v3_wait_vm<C::LPS>();
             __builtin_amdgcn_s_barrier();
             mx_substep<BW, false, true, true>(acc, f1, tsc, wsc, f0, A2, A2, tsr, wsr, smem, ld, kt + 3, 1,
                                               hs(0, 1), true);
             v3_wait_lgkm0();
-            v3_wait_vm<2 * C::LPH>();
+            v3_wait_vm<C::LPS>();
             __builtin_amdgcn_s_barrier();
             kt += 2;
         }
@@ -812,7 +843,10 @@ hipError_t launch_pipelined(const MxGemmArgs& a, int cus, hipStream_t stream) {
 template <int BT, int BW, int NS>
 hipError_t launch_z(const MxGemmArgs& a, hipStream_t stream) {
     const int tiles = ((a.R + BT - 1) / BT) * ((a.C + BW - 1) / BW);
-    hipLaunchKernelGGL((gemm_mx_z_kernel<BT, BW, NS>), dim3(tiles), dim3(256), 0, stream, a);
+    // four steps' scales per 16-byte load where every scale row starts on 16 bytes
+    const bool s4 = a.ldts % 16 == 0 && a.ldws % 16 == 0 && (uintptr_t)a.Ts % 16 == 0 && (uintptr_t)a.Ws % 16 == 0;
+    if (s4) hipLaunchKernelGGL((gemm_mx_z_kernel<BT, BW, NS, 4>), dim3(tiles), dim3(256), 0, stream, a);
+    else hipLaunchKernelGGL((gemm_mx_z_kernel<BT, BW, NS, 1>), dim3(tiles), dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 

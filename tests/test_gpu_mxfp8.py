@@ -207,3 +207,42 @@ def test_mxfp8_llama2_7b_qkv_sampled(E):
     ratio, rel = MP.check_bound(host64(Y)[rows], Yo, B, "layer")
     print(f"llama2-7b qkv mxfp8: Z codes equal to the oracle's {same:.4f}, worst error/bound {ratio:.3f}, "
           f"rel_fro {rel:.2e}")
+
+
+# (N, L, K) of projections whose operands' scale rows are laid out twice: at
+# the smallest leading dimension (not a multiple of 16 bytes: one scale
+# dword per row and step) and padded to 16 bytes as the library allocates
+# them (four steps' scales per 16-byte load), on 128 x 192 tiles with three stages (6 steps: a last group
+# of two), 128 x 128 tiles with two stages, and 256 x 256 tiles (33 steps).
+SCALE_LAYOUTS = [(5000, 700, 700), (1000, 300, 700), (4096, 4096, 4100)]
+
+
+@pytest.mark.parametrize("shape", SCALE_LAYOUTS, ids=lambda s: "N%d_L%d_K%d" % s)
+def test_mxfp8_projection_scale_layouts(E, shape):
+    """The projection gives the same codes and scale bytes, bit for bit,
+    whichever scale-load path the operands' layout selects."""
+    dev = need_gpu()
+    N, L, K = shape
+    gen = torch.Generator(device="cpu").manual_seed(N + L + K)
+    X = E.padded_empty(N, K, torch.bfloat16, dev)
+    X.copy_(torch.randn(N, K, generator=gen).to(torch.bfloat16))
+    Pt = E.padded_empty(L, K, torch.bfloat16, dev)
+    Pt.copy_((torch.randn(L, K, generator=gen) * K ** -0.5).to(torch.bfloat16))
+    cp = (K + 127) // 128 * 128
+    assert (cp // 32) % 16 != 0, "the smallest scale rows must not be 16-byte multiples"
+    spad = (cp // 32 + 15) // 16 * 16
+
+    def tight(rows):
+        return E.MXTensor(torch.empty((rows, cp), dtype=torch.uint8, device=dev),
+                          torch.empty((rows, cp // 32), dtype=torch.uint8, device=dev), K)
+
+    X1 = E.espace_quantize_mxfp8(X, out=tight(N))
+    P1 = E.espace_quantize_mxfp8(Pt, out=tight(L))
+    X4, P4 = E.espace_quantize_mxfp8(X), E.espace_quantize_mxfp8(Pt)
+    assert X4.scales.stride(0) == spad and P4.scales.stride(0) == spad
+    Z1, Z4 = E.espace_project_mxfp8(P1, X1), E.espace_project_mxfp8(P4, X4)
+    torch.cuda.synchronize()
+    assert torch.equal(X1.scales, X4.scales) and torch.equal(P1.scales, P4.scales)
+    assert torch.equal(Z1.codes, Z4.codes), "Z codes differ between the scale layouts"
+    assert torch.equal(Z1.scales, Z4.scales), "Z scale bytes differ between the scale layouts"
+    assert Z1.codes[:, :L].any(), "Z is all zero"
