@@ -8,7 +8,8 @@
 // * The expansion (bf16 output) runs the four-wave bfloat16 kernel's
 //   pipeline (gemm_bf16_v3.hip) on fp8 operands: a depth step of 128 codes is
 //   two sub-steps of 64, each with its own LDS half-stage of 64-byte rows laid
-//   out exactly as the bf16 kernel's (same loads, same chunk swizzle), plus
+//   out as the bf16 kernel's (same loads; the chunk swizzle suits reads of
+//   32 rows), plus
 //   one scale dword per row (the four 32-blocks of the step), loaded with
 //   the first half-stage only.  Per sub-step a
 //   wave issues NI x NJ v_mfma_scale_f32_32x32x64_f8f6f4 (16 for the
@@ -546,10 +547,14 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
 
     // fragment addresses: a lane reads row lane % 32 of each 32-row block,
     // chunks lh and 2 + lh; the swizzle depends on the row only through
-    // lane % 32 (blocks start at multiples of 32 rows)
+    // lane % 32 (blocks start at multiples of 32 rows).  Chunk c of a row
+    // sits at c ^ ((row >> 2) & 3): with the bf16 kernel's (row >> 1) & 3
+    // these reads of 32 rows took two passes of the LDS banks each (measured
+    // with the bank-conflict counter, on the kernel and on a probe of the
+    // read pattern alone; the kernel's time did not change measurably)
     const int lr = lane & 31;
     const int lh = lane >> 5;
-    const int sw = v3_swz(lr);
+    const int sw = (lr >> 2) & 3;
     const unsigned sbase = (unsigned)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
     const unsigned c_lo = (unsigned)((lh ^ sw) * 16), c_hi = (unsigned)(((2 + lh) ^ sw) * 16);
     const unsigned trow = sbase + (unsigned)((wrow0 + lr) * V3_ROWB);
@@ -596,7 +601,7 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
         } else {
             // the half-stages may still be read by a wave finishing the previous tile
             if (item != (int)blockIdx.x) __syncthreads();
-            v3_offsets<V>(ld.voff, row0, col0, a.R, a.C, a.ldt / 2, a.ldw / 2, wave, lane);
+            v3_offsets<V, 2>(ld.voff, row0, col0, a.R, a.C, a.ldt / 2, a.ldw / 2, wave, lane);
             ld.scale_offsets(a, row0, col0, lane);
 #pragma unroll
             for (int y = 0; y < C::LPH0; ++y) ld.load(smem, 0, 0, hs(0, 0), y);
@@ -635,7 +640,7 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
             lkt = kt + 2 - ktiles;
             if (!ahead_next) return false;
             if (kt + 2 == ktiles && h == 0) {
-                v3_offsets<V>(ld.voff, ntr * V3_BM, ntc * BW, a.R, a.C, a.ldt / 2, a.ldw / 2, wave, lane);
+                v3_offsets<V, 2>(ld.voff, ntr * V3_BM, ntc * BW, a.R, a.C, a.ldt / 2, a.ldw / 2, wave, lane);
                 ld.scale_offsets(a, ntr * V3_BM, ntc * BW, lane);
             }
             return true;

@@ -174,9 +174,10 @@ enum { V3_BF16 = 0, V3_F32 = 1, V3_PAIR = 2 };
 
 // byte offsets of this lane's 16-byte chunk of each wave-load (depth offset
 // excluded) for the tile at (row0, col0): row 16q + lane/4 of the A|B tile,
-// logical chunk (lane % 4) ^ swz(row); rows past the matrix are clamped to
-// its last row
-template <class C>
+// logical chunk (lane % 4) ^ swz(row), swz(row) = (row >> SH) & 3 (SH = 1
+// is v3_swz, for the bf16 fragment reads of 16 rows; the fp8 kernel's reads
+// of 32 rows take SH = 2); rows past the matrix are clamped to its last row
+template <class C, int SH = 1>
 __device__ __forceinline__ void v3_offsets(int* voff, int row0, int col0, int R, int Cc, int64_t lda,
                                            int64_t ldb, int wave, int lane) {
 #pragma unroll
@@ -184,7 +185,7 @@ __device__ __forceinline__ void v3_offsets(int* voff, int row0, int col0, int R,
         const int q = wave + 4 * j;
         const bool isA = j < 4;
         const int rr = q * 16 + (lane >> 2) - (isA ? 0 : V3_BM);
-        const int lc = (lane & 3) ^ v3_swz(rr);
+        const int lc = (lane & 3) ^ ((rr >> SH) & 3);
         int gr = (isA ? row0 : col0) + rr;
         const int lim = isA ? R : Cc;
         gr = gr < lim ? gr : lim - 1;
