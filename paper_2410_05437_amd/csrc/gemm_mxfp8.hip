@@ -74,25 +74,31 @@ typedef int i32x4_t __attribute__((ext_vector_type(4)));
 // one per stage (the scale loads of a step go with its first half-stage: a
 // scale load gathers 64 rows, one memory line each; loaded with both halves
 // they took 88 against 82 us on the 4096 x 12288 x 1536 expansion).
-template <int BW>
+template <int BW, int SS>
 struct MxCfg {
     using V = V3Cfg<BW>;
     static constexpr int NI = 4, NJ = BW / 64;
     static constexpr int ROWS = V::ROWS;
-    static constexpr int SCB = ROWS * 4;              // scale bytes of a stage
-    static constexpr int NSC = ROWS / 64;             // 256-byte scale loads per stage
+    static constexpr int SROW = 4 * SS;               // scale bytes per row in an area
+    static constexpr int SCB = ROWS * SROW;           // bytes of a scale area
+    static constexpr int NSC = ROWS / 64;             // scale loads (64 rows each) per area
     static constexpr int LSC = (NSC + 3) / 4;         // per wave (uniform: extra ones repeat a load)
-    // loads per wave of a step's first half-stage (codes, and the step's
-    // scale dwords, which only that half's area receives) and of its second
+    // loads per wave of a step's first half-stage when it carries scales
+    // (codes, and SS steps' scale dwords, which only that half loads) and of
+    // a half-stage of codes alone
     static constexpr int LPH0 = V::LPH + LSC, LPH1 = V::LPH;
-    static constexpr int LPS = LPH0 + LPH1;           // per step
+    static constexpr int LPS = LPH0 + LPH1;           // per step with scales
     static constexpr int NMF = NI * NJ;               // MFMAs per sub-step
     static constexpr int NRD = 2 * (NI + NJ);         // code fragment reads per sub-step
     static constexpr int NSR = NI + NJ;               // scale dword reads per step
     static constexpr int NST = 2 * NI * NJ;           // 16-byte stores per wave (bf16 output)
     static constexpr int SMEM = 4 * V::HS + 2 * SCB;
     static_assert(BW == 256 || BW == 128, "tile");
+    static_assert(SS == 1 || SS == 4, "scale steps");
     static_assert(LPS + NST < 64, "vmcnt");
+    // whether step kt's first half carries scales, and its loads per wave
+    static __device__ __forceinline__ constexpr bool scales_with(int kt) { return SS == 1 || (kt & 3) == 0; }
+    static __device__ __forceinline__ constexpr int n0(int kt) { return scales_with(kt) ? LPH0 : LPH1; }
     // MFMA after which load y of a sub-step's n is issued
     static constexpr int load_slot(int y, int n) { return y * NMF / n + NMF / (2 * n); }
     // MFMA after which read x of a sub-step is issued (n reads in all)
@@ -382,14 +388,14 @@ __device__ __forceinline__ void mx_read(int x, MxFrag<NJ>& f, const MxAddr& a) {
 }
 
 // Scale read x of a step (token blocks 0 .. 3, then weight blocks; 32 rows,
-// 128 bytes, apart) into the raw dwords.
-template <int NJ>
+// 32 SROW bytes, apart) into the raw dwords.
+template <int NJ, int SROW>
 __device__ __forceinline__ void mx_read_scale(int x, int* tsr, int* wsr, const MxAddr& a) {
 #define MX_S(n)                                                                           \
     if constexpr (n < 4 + NJ) {                                                           \
         if (x == n) {                                                                     \
-            if constexpr (n < 4) MX_READ32(tsr[n], a.ts, n * 128);                        \
-            else MX_READ32(wsr[n - 4], a.ws, (n - 4) * 128);                              \
+            if constexpr (n < 4) MX_READ32(tsr[n], a.ts, n * 32 * SROW);                  \
+            else MX_READ32(wsr[n - 4], a.ws, (n - 4) * 32 * SROW);                        \
         }                                                                                 \
     }
     MX_S(0) MX_S(1) MX_S(2) MX_S(3) MX_S(4) MX_S(5) MX_S(6) MX_S(7)
@@ -399,9 +405,9 @@ __device__ __forceinline__ void mx_read_scale(int x, int* tsr, int* wsr, const M
 // What a sub-step's loads need: the code operands as 16-bit arrays (the
 // bf16 kernel's load helpers; one step of 128 codes is 64 of their
 // elements), the scale arrays, and this lane's per-load row offsets.
-template <int BW>
+template <int BW, int SS>
 struct MxLoad {
-    using C = MxCfg<BW>;
+    using C = MxCfg<BW, SS>;
     const uint16_t* T;
     const uint16_t* W;
     unsigned tbytes, wbytes;
@@ -423,19 +429,25 @@ struct MxLoad {
         }
     }
 
-    // load y of half h of step kt into half-stage u
-    __device__ __forceinline__ void load(unsigned char* smem, int kt, int h, int u, int y) const {
+    // load y of half h of step kt into half-stage u; a scale load (SS
+    // steps' dwords per row, only with a step that carries them) goes to
+    // scale area `area` (SS = 1: the stage's own, u / 2).  The 16-byte loads
+    // of a last group may read past the matrix's steps: bytes never used,
+    // zeros past the buffer.
+    __device__ __forceinline__ void load(unsigned char* smem, int kt, int h, int u, int y, int area) const {
         if (y < C::V::LPH) {
             v3_load<typename C::V>(smem, T, W, tbytes, wbytes, voff, wave, kt, h, u, y);
-        } else {
+        } else if (C::scales_with(kt)) {
             const int j = y - C::V::LPH;
             const int s = (wave + 4 * j) % C::NSC;
             const bool tok = s < 4;
             const auto rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(tok ? Ts : Ws), (short)0,
                                                                 (int)(tok ? tsbytes : wsbytes), 0x00020000);
+            const int ar = SS == 1 ? (u >> 1) : area;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rsrc, (__attribute__((address_space(3))) void*)(smem + 4 * C::V::HS + (u >> 1) * C::SCB + 256 * s), 4,
-                soff[j], 4 * kt, 0, 0);
+                rsrc,
+                (__attribute__((address_space(3))) void*)(smem + 4 * C::V::HS + ar * C::SCB + 64 * C::SROW * s),
+                C::SROW, soff[j], 4 * kt, 0, 0);
         }
     }
 };
@@ -446,13 +458,13 @@ struct MxLoad {
 // sd into tsr / wsr, and with do_load the loads of half h of step lkt into
 // half-stage u (h = SEL1: LPH0 loads in sub-step 0, LPH1 in sub-step 1).
 // FIRST: the accumulators start from zero.
-template <int BW, bool FIRST, bool SEL1, bool SREADS>
+template <int BW, int SS, bool FIRST, bool SEL1, bool SREADS>
 __device__ __forceinline__ void mx_substep(f32x16_t (&acc)[4][BW / 64], const MxFrag<BW / 64>& cur,
                                            const int* tsc, const int* wsc, MxFrag<BW / 64>& nxt,
                                            const MxAddr& rd, const MxAddr& sd, int* tsr, int* wsr,
-                                           unsigned char* smem, const MxLoad<BW>& ld, int lkt, int h, int u,
-                                           bool do_load) {
-    using C = MxCfg<BW>;
+                                           unsigned char* smem, const MxLoad<BW, SS>& ld, int lkt, int h, int u,
+                                           int area, bool do_load) {
+    using C = MxCfg<BW, SS>;
     constexpr int NJ = C::NJ;
     constexpr int NR = C::NRD + (SREADS ? C::NSR : 0);
 #pragma unroll
@@ -473,28 +485,28 @@ __device__ __forceinline__ void mx_substep(f32x16_t (&acc)[4][BW / 64], const Mx
             for (int x = 0; x < NR; ++x)
                 if (C::read_slot(x, NR) == m) {
                     if (x < C::NRD) mx_read<NJ>(x, nxt, rd);
-                    else mx_read_scale<NJ>(x - C::NRD, tsr, wsr, sd);
+                    else mx_read_scale<NJ, C::SROW>(x - C::NRD, tsr, wsr, sd);
                 }
             constexpr int NL = SEL1 ? C::LPH1 : C::LPH0;
 #pragma unroll
             for (int y = 0; y < NL; ++y)
-                if (C::load_slot(y, NL) == m && do_load) ld.load(smem, lkt, h, u, y);
+                if (C::load_slot(y, NL) == m && do_load) ld.load(smem, lkt, h, u, y, area);
         }
 }
 
-// vmcnt(n) for the counts the steps need (half-steps of LPH0 and LPH1
-// loads, plus the previous tile's NST stores); any other n waits for
+// vmcnt(n) for the counts the steps need (half-steps of LPH0 or LPH1 and
+// LPH1 loads, plus the previous tile's NST stores); any other n waits for
 // everything
 template <class C>
 __device__ __forceinline__ void mx_wait_vm_n(int n) {
     constexpr int L0 = C::LPH0, L1 = C::LPH1, S = C::NST;
     if (n == 0) v3_wait_vm<0>();
-    else if (n == L0) v3_wait_vm<L0>();
     else if (n == L1) v3_wait_vm<L1>();
+    else if (n == 2 * L1) v3_wait_vm<2 * L1>();
     else if (n == L0 + L1) v3_wait_vm<L0 + L1>();
     else if (n == S) v3_wait_vm<S>();
-    else if (n == S + L0) v3_wait_vm<S + L0>();
     else if (n == S + L1) v3_wait_vm<S + L1>();
+    else if (n == S + 2 * L1) v3_wait_vm<S + 2 * L1>();
     else if (n == S + L0 + L1) v3_wait_vm<S + L0 + L1>();
     else v3_wait_vm<0>();
 }
@@ -518,11 +530,15 @@ __device__ __forceinline__ f32x16_t mx_acc_read(const f32x16_t& a) {
 // each taking tiles blockIdx.x, blockIdx.x + gridDim.x, ...  As in the bf16
 // kernel, when the output is bf16 with C a multiple of 8, the last two steps
 // of a tile load the next tile's first two, and the tile's results leave with
-// exactly NST stores per wave.  Output: bf16 Y [R][ldo].
-template <int BW>
+// exactly NST stores per wave.  Output: bf16 Y [R][ldo].  SS = 4 (scale
+// rows 16-byte aligned): the scale dwords of four steps per 16-byte load,
+// with every fourth step, into two areas taken in turn by the workgroup's
+// successive groups of four steps (tile after tile), so that a group's area
+// is rewritten only after its last step's scales were read.
+template <int BW, int SS>
 __global__ __launch_bounds__(256, 1)
 void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
-    using C = MxCfg<BW>;
+    using C = MxCfg<BW, SS>;
     using V = typename C::V;
     constexpr int NJ = C::NJ;
     __shared__ __attribute__((aligned(1024))) unsigned char smem[C::SMEM];
@@ -534,7 +550,7 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
     const int wcol0 = (wave & 1) * (BW / 2);          // its output columns
     const bool ahead_ok = (a.C & 7) == 0 && ktiles >= 2;
 
-    MxLoad<BW> ld;
+    MxLoad<BW, SS> ld;
     ld.T = reinterpret_cast<const uint16_t*>(a.T);
     ld.W = reinterpret_cast<const uint16_t*>(a.W);
     ld.tbytes = (unsigned)((uint64_t)a.R * a.ldt);
@@ -559,8 +575,8 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
     const unsigned c_lo = (unsigned)((lh ^ sw) * 16), c_hi = (unsigned)(((2 + lh) ^ sw) * 16);
     const unsigned trow = sbase + (unsigned)((wrow0 + lr) * V3_ROWB);
     const unsigned wrow = sbase + (unsigned)((V3_BM + wcol0 + lr) * V3_ROWB);
-    const unsigned tsca = sbase + (unsigned)(4 * V::HS + 4 * (wrow0 + lr));
-    const unsigned wsca = sbase + (unsigned)(4 * V::HS + 4 * (V3_BM + wcol0 + lr));
+    const unsigned tsca = sbase + (unsigned)(4 * V::HS + C::SROW * (wrow0 + lr));
+    const unsigned wsca = sbase + (unsigned)(4 * V::HS + C::SROW * (V3_BM + wcol0 + lr));
     auto addr = [&](int u) {
         MxAddr m;
         m.tl = trow + c_lo + (unsigned)(u * V::HS);
@@ -572,6 +588,23 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
         return m;
     };
     const int shift = 8 * lh;                         // block lh of a sub-step at byte 0 (or 2)
+    int gb = 0;             // SS = 4: the workgroup's group count at this tile's first step
+    // scale addresses of step k of this tile (SS = 1: its stage's area, as
+    // in the stage's addresses st)
+    auto sca = [&](const MxAddr& st, int k) {
+        MxAddr m = st;
+        if constexpr (SS == 4) {
+            const unsigned off = (unsigned)(((gb + (k >> 2)) & 1) * C::SCB + 4 * (k & 3));
+            m.ts = tsca + off;
+            m.ws = wsca + off;
+        }
+        return m;
+    };
+    // vmcnt with the loads of half 0 of step k (and a half 1) in flight
+    auto wait_step = [&](int k) {
+        if (C::scales_with(k)) v3_wait_vm<C::LPS>();
+        else v3_wait_vm<2 * C::LPH1>();
+    };
 
     f32x16_t acc[4][NJ];
     MxFrag<NJ> f0, f1;
@@ -587,6 +620,7 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
         const int col0 = tile_c * BW;
         const int next = item + (int)gridDim.x;
         const bool ahead_next = ahead_ok && next < ntiles;
+        const int gb_next = gb + (ktiles + 3) / 4;
         int ntr = 0, ntc = 0;
         if (next < ntiles) tile_coords<4>(next, ntiles, tiles_c, 0, ntr, ntc);
 
@@ -597,22 +631,22 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
         if (ahead) {
             // the first step's loads, then the second's and the previous
             // tile's stores were issued
-            v3_wait_vm<C::LPS + C::NST>();
+            v3_wait_vm<C::n0(1) + C::LPH1 + C::NST>();
         } else {
             // the half-stages may still be read by a wave finishing the previous tile
             if (item != (int)blockIdx.x) __syncthreads();
             v3_offsets<V, 2>(ld.voff, row0, col0, a.R, a.C, a.ldt / 2, a.ldw / 2, wave, lane);
             ld.scale_offsets(a, row0, col0, lane);
 #pragma unroll
-            for (int y = 0; y < C::LPH0; ++y) ld.load(smem, 0, 0, hs(0, 0), y);
+            for (int y = 0; y < C::LPH0; ++y) ld.load(smem, 0, 0, hs(0, 0), y, gb & 1);
 #pragma unroll
-            for (int y = 0; y < C::LPH1; ++y) ld.load(smem, 0, 1, hs(0, 1), y);
+            for (int y = 0; y < C::LPH1; ++y) ld.load(smem, 0, 1, hs(0, 1), y, gb & 1);
             if (ktiles > 1) {
 #pragma unroll
-                for (int y = 0; y < C::LPH0; ++y) ld.load(smem, 1, 0, hs(1, 0), y);
+                for (int y = 0; y < C::LPH0; ++y) ld.load(smem, 1, 0, hs(1, 0), y, gb & 1);
 #pragma unroll
-                for (int y = 0; y < C::LPH1; ++y) ld.load(smem, 1, 1, hs(1, 1), y);
-                v3_wait_vm<C::LPS>();
+                for (int y = 0; y < C::LPH1; ++y) ld.load(smem, 1, 1, hs(1, 1), y, gb & 1);
+                v3_wait_vm<C::n0(1) + C::LPH1>();
             } else {
                 v3_wait_vm<0>();
             }
@@ -621,7 +655,7 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
 #pragma unroll
         for (int x = 0; x < C::NRD; ++x) mx_read<NJ>(x, f0, A0);
 #pragma unroll
-        for (int x = 0; x < C::NSR; ++x) mx_read_scale<NJ>(x, tsr, wsr, A0);
+        for (int x = 0; x < C::NSR; ++x) mx_read_scale<NJ, C::SROW>(x, tsr, wsr, sca(A0, 0));
         v3_wait_lgkm0();
         // the first sub-step loads step 2 into the half-stage just read:
         // every wave's reads of it must be complete before any wave issues them
@@ -631,13 +665,15 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
         int rel = 0;          // stage of step kt relative to s0
         // the loads of sub-step h of step kt: half h of step kt + 2 of this
         // tile, or of the next tile's first steps once this one has none left
-        // (step lkt of that tile); false: none
-        auto load_kind = [&](int h, int& lkt) -> bool {
+        // (step lkt of that tile, scale area larea); false: none
+        auto load_kind = [&](int h, int& lkt, int& larea) -> bool {
             if (kt + 2 < ktiles) {
                 lkt = kt + 2;
+                larea = (gb + (lkt >> 2)) & 1;
                 return true;
             }
             lkt = kt + 2 - ktiles;
+            larea = (gb_next + (lkt >> 2)) & 1;
             if (!ahead_next) return false;
             if (kt + 2 == ktiles && h == 0) {
                 v3_offsets<V, 2>(ld.voff, ntr * V3_BM, ntc * BW, a.R, a.C, a.ldt / 2, a.ldw / 2, wave, lane);
@@ -662,11 +698,11 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
             // tile's stores in flight behind the loads of its second step
             const int stores = (F && ahead) ? C::NST : 0;
             shift_scales();
-            int lkt;
-            const bool k0 = load_kind(0, lkt);
-            mx_substep<BW, F, false, false>(acc, f0, tsc, wsc, f1, rel ? A3 : A1, A0, tsr, wsr, smem, ld, lkt, 0,
-                                            hs(rel, 0), k0);
-            const int n0 = k0 ? C::LPH0 : 0;
+            int lkt, larea;
+            const bool k0 = load_kind(0, lkt, larea);
+            mx_substep<BW, SS, F, false, false>(acc, f0, tsc, wsc, f1, rel ? A3 : A1, A0, tsr, wsr, smem, ld, lkt,
+                                                0, hs(rel, 0), larea, k0);
+            const int n0 = k0 ? C::n0(lkt) : 0;
             v3_wait_lgkm0();
             if (kt + 1 < ktiles || ahead_next) {
                 // the next step's first half has landed (the loads just issued may stay in flight)
@@ -675,9 +711,9 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
             }
             // sub-step 1: fragments and scales of the next step's sub-step 0
             // (after the last step the reads are of no use but harmless)
-            const bool k1 = load_kind(1, lkt);
-            mx_substep<BW, false, true, true>(acc, f1, tsc, wsc, f0, rel ? A0 : A2, rel ? A0 : A2, tsr, wsr, smem,
-                                              ld, lkt, 1, hs(rel, 1), k1);
+            const bool k1 = load_kind(1, lkt, larea);
+            mx_substep<BW, SS, false, true, true>(acc, f1, tsc, wsc, f0, rel ? A0 : A2, sca(rel ? A0 : A2, kt + 1),
+                                                  tsr, wsr, smem, ld, lkt, 1, hs(rel, 1), larea, k1);
             const int n1 = k1 ? C::LPH1 : 0;
             v3_wait_lgkm0();
             if (kt + 1 < ktiles) {
@@ -694,27 +730,28 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
         // half-stage the next sub-step reads, with the two newer half-steps of
         // loads in flight
         while (kt + 3 < ktiles) {
+            const int a2 = (gb + ((kt + 2) >> 2)) & 1, a3 = (gb + ((kt + 3) >> 2)) & 1;
             shift_scales();
-            mx_substep<BW, false, false, false>(acc, f0, tsc, wsc, f1, A3, A3, tsr, wsr, smem, ld, kt + 2, 0,
-                                                hs(1, 0), true);
+            mx_substep<BW, SS, false, false, false>(acc, f0, tsc, wsc, f1, A3, A3, tsr, wsr, smem, ld, kt + 2, 0,
+                                                    hs(1, 0), a2, true);
             v3_wait_lgkm0();
-            v3_wait_vm<C::LPS>();
+            wait_step(kt + 2);
             __builtin_amdgcn_s_barrier();
-            mx_substep<BW, false, true, true>(acc, f1, tsc, wsc, f0, A0, A0, tsr, wsr, smem, ld, kt + 2, 1,
-                                              hs(1, 1), true);
+            mx_substep<BW, SS, false, true, true>(acc, f1, tsc, wsc, f0, A0, sca(A0, kt + 1), tsr, wsr, smem, ld,
+                                                  kt + 2, 1, hs(1, 1), a2, true);
             v3_wait_lgkm0();
-            v3_wait_vm<C::LPS>();
+            wait_step(kt + 2);
             __builtin_amdgcn_s_barrier();
             shift_scales();
-            mx_substep<BW, false, false, false>(acc, f0, tsc, wsc, f1, A1, A1, tsr, wsr, smem, ld, kt + 3, 0,
-                                                hs(0, 0), true);
+            mx_substep<BW, SS, false, false, false>(acc, f0, tsc, wsc, f1, A1, A1, tsr, wsr, smem, ld, kt + 3, 0,
+                                                    hs(0, 0), a3, true);
             v3_wait_lgkm0();
-            v3_wait_vm<C::LPS>();
+            wait_step(kt + 3);
             __builtin_amdgcn_s_barrier();
-            mx_substep<BW, false, true, true>(acc, f1, tsc, wsc, f0, A2, A2, tsr, wsr, smem, ld, kt + 3, 1,
-                                              hs(0, 1), true);
+            mx_substep<BW, SS, false, true, true>(acc, f1, tsc, wsc, f0, A2, sca(A2, kt + 2), tsr, wsr, smem, ld,
+                                                  kt + 3, 1, hs(0, 1), a3, true);
             v3_wait_lgkm0();
-            v3_wait_vm<C::LPS>();
+            wait_step(kt + 3);
             __builtin_amdgcn_s_barrier();
             kt += 2;
         }
@@ -787,6 +824,7 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
         tile_r = ntr;
         tile_c = ntc;
         s0 = (s0 + ktiles) & 1;
+        gb = gb_next;
         ahead = ahead_next;
     }
 }
@@ -836,12 +874,20 @@ void mx_quantize_kernel(const uint16_t* A, int64_t lda, int R, int C, uint8_t* Q
     S[(int64_t)r * lds + b] = (uint8_t)sb;
 }
 
+bool scale_rows_16(const MxGemmArgs& a) {
+    return a.ldts % 16 == 0 && a.ldws % 16 == 0 && (uintptr_t)a.Ts % 16 == 0 && (uintptr_t)a.Ws % 16 == 0;
+}
+
 template <int BW>
 hipError_t launch_pipelined(const MxGemmArgs& a, int cus, hipStream_t stream) {
     const int tiles_c = (a.C + BW - 1) / BW;
     const int ntiles = tiles_c * ((a.R + 255) / 256);
     const int grid = ntiles < cus ? ntiles : cus;
-    hipLaunchKernelGGL((gemm_mx_kernel<BW>), dim3(grid), dim3(256), 0, stream, a, tiles_c, ntiles);
+    // four steps' scales per 16-byte load where every scale row starts on 16 bytes
+    if (scale_rows_16(a))
+        hipLaunchKernelGGL((gemm_mx_kernel<BW, 4>), dim3(grid), dim3(256), 0, stream, a, tiles_c, ntiles);
+    else
+        hipLaunchKernelGGL((gemm_mx_kernel<BW, 1>), dim3(grid), dim3(256), 0, stream, a, tiles_c, ntiles);
     return hipGetLastError();
 }
 
@@ -849,8 +895,7 @@ template <int BT, int BW, int NS>
 hipError_t launch_z(const MxGemmArgs& a, hipStream_t stream) {
     const int tiles = ((a.R + BT - 1) / BT) * ((a.C + BW - 1) / BW);
     // four steps' scales per 16-byte load where every scale row starts on 16 bytes
-    const bool s4 = a.ldts % 16 == 0 && a.ldws % 16 == 0 && (uintptr_t)a.Ts % 16 == 0 && (uintptr_t)a.Ws % 16 == 0;
-    if (s4) hipLaunchKernelGGL((gemm_mx_z_kernel<BT, BW, NS, 4>), dim3(tiles), dim3(256), 0, stream, a);
+    if (scale_rows_16(a)) hipLaunchKernelGGL((gemm_mx_z_kernel<BT, BW, NS, 4>), dim3(tiles), dim3(256), 0, stream, a);
     else hipLaunchKernelGGL((gemm_mx_z_kernel<BT, BW, NS, 1>), dim3(tiles), dim3(256), 0, stream, a);
     return hipGetLastError();
 }

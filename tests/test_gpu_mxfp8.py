@@ -246,3 +246,39 @@ def test_mxfp8_projection_scale_layouts(E, shape):
     assert torch.equal(Z1.codes, Z4.codes), "Z codes differ between the scale layouts"
     assert torch.equal(Z1.scales, Z4.scales), "Z scale bytes differ between the scale layouts"
     assert Z1.codes[:, :L].any(), "Z is all zero"
+
+
+# (N, M, L) of expansions run on both scale layouts: 6 steps over 528 tiles of
+# 256 x 256 (workgroups take two or three tiles, the next tile's first steps
+# loaded ahead, groups of four steps continuing across tiles), 11 steps on
+# the same tiles, and 5 and 25 steps on 256 x 128 tiles.
+EXPAND_LAYOUTS = [(4096, 8448, 700), (4096, 8448, 1400), (2000, 1000, 600), (1000, 3000, 3100)]
+
+
+@pytest.mark.parametrize("shape", EXPAND_LAYOUTS, ids=lambda s: "N%d_M%d_L%d" % s)
+def test_mxfp8_expansion_scale_layouts(E, shape):
+    """The expansion gives the same output, bit for bit, with one scale dword
+    per step loaded (scale rows not 16-byte multiples) and with four steps'
+    scales per load (the library's padded rows)."""
+    dev = need_gpu()
+    N, M, L = shape
+    gen = torch.Generator(device="cpu").manual_seed(N + M + L)
+    Zb = E.padded_empty(N, L, torch.bfloat16, dev)
+    Zb.copy_(torch.randn(N, L, generator=gen).to(torch.bfloat16))
+    Wb = E.padded_empty(M, L, torch.bfloat16, dev)
+    Wb.copy_((torch.randn(M, L, generator=gen) * L ** -0.5).to(torch.bfloat16))
+    cp = (L + 127) // 128 * 128
+    assert (cp // 32) % 16 != 0, "the smallest scale rows must not be 16-byte multiples"
+
+    def tight(rows):
+        return E.MXTensor(torch.empty((rows, cp), dtype=torch.uint8, device=dev),
+                          torch.empty((rows, cp // 32), dtype=torch.uint8, device=dev), L)
+
+    Z1, W1 = E.espace_quantize_mxfp8(Zb, out=tight(N)), E.espace_quantize_mxfp8(Wb, out=tight(M))
+    Z4, W4 = E.espace_quantize_mxfp8(Zb), E.espace_quantize_mxfp8(Wb)
+    assert Z4.scales.stride(0) % 16 == 0 and W4.scales.stride(0) % 16 == 0
+    Y1 = E.espace_expand_mxfp8(Z1, W1, out_mat(N, M, "bf16", dev))
+    Y4 = E.espace_expand_mxfp8(Z4, W4, out_mat(N, M, "bf16", dev))
+    torch.cuda.synchronize()
+    assert torch.equal(Y1, Y4), "Y differs between the scale layouts"
+    assert torch.isfinite(Y4.float()).all() and Y4.abs().sum() > 0
