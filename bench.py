@@ -150,8 +150,8 @@ def traffic_sources():
     import hashlib
     h = hashlib.sha256()
     for f in ("paper_2410_05437_amd/csrc/gemm_bf16_v3.hip", "paper_2410_05437_amd/csrc/gemm_bf16_v2.hip",
-              "paper_2410_05437_amd/csrc/common.hpp", "paper_2410_05437_amd/csrc/kernels.hpp",
-              "paper_2410_05437_amd/csrc/espace_api.hip"):
+              "paper_2410_05437_amd/csrc/v3_core.hpp", "paper_2410_05437_amd/csrc/common.hpp",
+              "paper_2410_05437_amd/csrc/kernels.hpp", "paper_2410_05437_amd/csrc/espace_api.hip"):
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
@@ -188,6 +188,7 @@ def kernel_probe(E, dev, stream, args, Xr, Pr, Wfr, Ws, Y, ws, Z, wsz, wse, R):
       project, expand, dense   - the Llama2-7B QKV layer's kernels (N=4096)
       layer_N{n}, dense_N{n}   - the Llama2-7B FFN up+gate layer and its dense
                                  layer at decode token counts n = 1, 8, 16
+      mx_project, mx_expand    - the MX-FP8 products of the QKV layer
     Every phase rotates its weights over copies larger than the last-level
     cache.  Prints the phase list as JSON."""
     import torch
@@ -238,6 +239,17 @@ def kernel_probe(E, dev, stream, args, Xr, Pr, Wfr, Ws, Y, ws, Z, wsz, wse, R):
         X = X0[:N]
         phase(f"layer_N{N}", lambda i: E.espace_projected_linear(X, Pl[i], Wfl[i], Yn, wsn), Rl)
         phase(f"dense_N{N}", lambda i: E.espace_dense_linear(X, Wl[i], Yn, wsdn), Rw)
+    torch.cuda.synchronize()
+    del Pl, Wfl, Wl, bufs
+    # MX-FP8 products of the QKV layer, operands quantised once
+    Xq = [E.espace_quantize_mxfp8(x) for x in Xr]
+    Pq = [E.espace_quantize_mxfp8(p) for p in Pr]
+    Wq = [E.espace_quantize_mxfp8(w) for w in Wfr]
+    Zq = E.mx_empty(Xr[0].shape[0], Pr[0].shape[0], dev)
+    E.espace_project_mxfp8(Pq[0], Xq[0], Zq)
+    torch.cuda.synchronize()
+    phase("mx_project", lambda i: E.espace_project_mxfp8(Pq[i], Xq[i], Zq), R)
+    phase("mx_expand", lambda i: E.espace_expand_mxfp8(Zq, Wq[i], Y), R)
     torch.cuda.synchronize()
     print(json.dumps({"kernel_probe": phases, "launches_per_phase": S, "copy_probe_bytes": COPY_PROBE_BYTES,
                       "qkv": {"K": 4096, "M": 12288, "L": 1536, "N": 4096},

@@ -32,7 +32,13 @@ OWN = ("gemm_tn", "skinny_tn", "gemv_", "splitk_reduce", "espace::")
 
 
 def _short(name):
-    return name.replace("espace::(anonymous namespace)::", "").split("(unsigned")[0].split("(float")[0]
+    return (name.replace("espace::(anonymous namespace)::", "").split("(unsigned")[0].split("(float")[0]
+            .split("(espace::")[0])
+
+
+def _own(name):
+    """A kernel of this library (namespace espace), not torch's."""
+    return "espace::" in name
 
 
 def _dur_us(r):
@@ -44,15 +50,15 @@ def stats(args):
     groups = collections.defaultdict(list)
     for r in rows:
         grid = f'{r["Grid_Size_X"]} x {r.get("Grid_Size_Y", "1")}'
-        groups[(_short(r["Kernel_Name"]), grid)].append(_dur_us(r))
+        groups[(_short(r["Kernel_Name"]), grid, _own(r["Kernel_Name"]))].append(_dur_us(r))
     lines = ["# Kernel statistics: projected linear, Llama2-7B fused QKV "
              "(K=4096, M=12288, L=1536, N=4096), bf16", "",
              "Command (from the repository root, on one MI355X):", "", "```", args.cmd, "```", "",
              "Per launch shape (grid in threads x split), durations from the kernel trace:", "",
              "| kernel | grid | launches | average (us) | median (us) |", "|---|---|---|---|---|"]
     other = [0, 0.0]
-    for (k, grid), v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
-        if "espace" not in k and "gemm_tn" not in k and "skinny" not in k and "splitk" not in k:
+    for (k, grid, own), v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        if not own:
             other[0] += len(v)
             other[1] += sum(v)
             continue
@@ -96,7 +102,7 @@ def stats(args):
               "median duration:", "", "| kernel | streamed bytes | median (us) | GB/s | HBM fraction (8 TB/s) |",
               "|---|---|---|---|---|"]
     for name, k, grid, nbytes in dec:
-        v = sorted(d for (gk, gg), ds in groups.items() if gk.endswith(k) and gg == grid for d in ds)
+        v = sorted(d for (gk, gg, _), ds in groups.items() if gk.endswith(k) and gg == grid for d in ds)
         if v:
             med = v[len(v) // 2]
             lines.append(f"| {name} | {nbytes} | {med:.1f} | {nbytes / med / 1e3:.0f} | "
@@ -108,7 +114,7 @@ def stats(args):
 MARKER = "spin_kernel"           # torch.cuda._sleep, around each of the probe's phases
 # the phases of bench.py --kernel-probe, in launch order
 PROBE_PHASES = ["project", "expand", "dense", "layer_N1", "dense_N1", "layer_N8", "dense_N8",
-                "layer_N16", "dense_N16"]
+                "layer_N16", "dense_N16", "mx_project", "mx_expand"]
 
 
 def _dispatches(path):
@@ -174,6 +180,15 @@ def _alg(phase, probe):
     """(algorithmic flops, algorithmic bytes) of one launch of a probe phase."""
     from paper_2410_05437_amd import accounting as acc
     q, d = probe["qkv"], probe["decode"]
+
+    def mx(r, c):   # MX-FP8 matrix bytes: codes, then one scale byte per 32
+        cp = (c + 127) // 128 * 128
+        return r * cp + r * cp // 32
+
+    if phase == "mx_project":
+        return 2 * q["N"] * q["L"] * q["K"], mx(q["N"], q["K"]) + mx(q["L"], q["K"]) + mx(q["N"], q["L"])
+    if phase == "mx_expand":
+        return 2 * q["N"] * q["M"] * q["L"], mx(q["N"], q["L"]) + mx(q["M"], q["L"]) + 2 * q["N"] * q["M"]
     if phase == "project":
         return acc.gemm_flops(q["N"], q["L"], q["K"]), acc.gemm_bytes(q["N"], q["L"], q["K"])
     if phase == "expand":
@@ -209,13 +224,14 @@ def counters(args):
     lines = ["# Hardware counters: the projected linear layer's kernels and the dense layer's", "",
              "Llama2-7B fused QKV (K=4096, M=12288, L=1536, N=4096): project, expand and dense GEMMs; "
              "Llama2-7B FFN up+gate (K=4096, M=22016, L=1536) at decode token counts N = 1, 8, 16: "
-             "every kernel of the layer and of the dense layer.  bf16, weights rotated over copies "
+             "every kernel of the layer and of the dense layer; the MX-FP8 products of the QKV layer "
+             "(mx_project, mx_expand).  bf16 (MX-FP8 in the mx phases), weights rotated over copies "
              "larger than the last-level cache.", "",
              "Counter runs (from the repository root, on one MI355X), one run per counter set:", "", "```"]
     lines += [cmd for _, cmd in args.run] + ["```", ""]
     lines += ["Columns are means per launch.  MFMA busy: the derived `MfmaUtil` (SQ_VALU_MFMA_BUSY_CYCLES "
-              "over GRBM_GUI_ACTIVE times the SIMD count).  MFMA flops: SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512, "
-              "against the product's 2·R·C·D.  Bytes: FETCH_SIZE and WRITE_SIZE (KiB) scaled by the "
+              "over GRBM_GUI_ACTIVE times the SIMD count).  MFMA flops: (SQ_INSTS_VALU_MFMA_MOPS_BF16 + "
+              "SQ_INSTS_VALU_MFMA_MOPS_F8) x 512, against the product's 2·R·C·D.  Bytes: FETCH_SIZE and WRITE_SIZE (KiB) scaled by the "
               "1 GiB copy of the same run "
               + ", ".join(f"({c} x {v:.4f})" for c, v in sorted(scale.items())) + ".", "",
               "| phase | kernel | grid | launches | MFMA busy % | MFMA flops / algorithmic | "
@@ -226,7 +242,8 @@ def counters(args):
         n = max(len(v) for v in ent.values())
         fl, by = _alg(ph, probe)
         busy = f"{mean['MfmaUtil']:.1f}" if "MfmaUtil" in mean else ""
-        mops = f"{mean['SQ_INSTS_VALU_MFMA_MOPS_BF16'] * 512 / fl:.3f}" if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in mean else ""
+        mo = [mean[c] for c in ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_VALU_MFMA_MOPS_F8") if c in mean]
+        mops = f"{sum(mo) * 512 / fl:.3f}" if mo else ""
         fb = mean.get("FETCH_SIZE", 0.0) * 1024 * scale.get("FETCH_SIZE", 0.0)
         wb = mean.get("WRITE_SIZE", 0.0) * 1024 * scale.get("WRITE_SIZE", 0.0)
         phase_bytes[ph] += fb + wb
