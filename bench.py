@@ -287,7 +287,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
-              "this build has no multi-GPU path", file=sys.stderr)
+              "the library has no multi-GPU path (how it would shard is described in its design notes)", file=sys.stderr)
         sys.exit(2)
 
     import torch
