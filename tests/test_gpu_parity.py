@@ -597,11 +597,14 @@ def test_decode_layer_shapes(E, shape):
         assert torch.equal(E.espace_projected_linear(X, Pt, Wf, workspace=ws), Y), fill
 
 
-def test_decode_layer_under_graph_replay(E):
+@pytest.mark.parametrize("N", [1, 16])
+def test_decode_layer_under_graph_replay(E, N):
     """The decode layer captured in a HIP graph and replayed with new tokens
-    copied in between: every replay equals the eager call bitwise."""
+    copied in between: every replay equals the eager call bitwise (one token:
+    the whole-row kernels; 16 tokens: the depth-segmented projection and the
+    LDS-ring expansion)."""
     dev = need_gpu()
-    K, M, L, N = 4096, 12288, 1536, 1
+    K, M, L = 4096, 12288, 1536
     inps = [_inputs(K, M, L, N, "bf16", seed=95 + i) for i in range(2)]
     X, Pt, W = _dev_inputs(inps[0], dev)
     Wf = E.espace_fold_weights(W, Pt)
