@@ -123,6 +123,10 @@ struct Plan {
     int splits = 1;
     int pair = 0;               // splits == 2 combined inside the GEMM kernel
     size_t partial_bytes = 0;   // fp32 partial sums for splits > 1 (and pair state words)
+    // tiled products in two launches by rows: rows [0, rows1) as above, the
+    // rest with (tile2, splits2, pair2); 0: one launch
+    int rows1 = 0;
+    int tile2 = 0, splits2 = 1, pair2 = 0;
 };
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
@@ -193,7 +197,7 @@ void set_partial_bytes(Plan& p, int64_t R, int64_t Cc) {
     }
 }
 
-Plan plan_tiled(int R, int Cc, int D, int cus) {
+Plan plan_tiled_one(int R, int Cc, int D, int cus, double* cost_out) {
     // Estimated time of each tile shape (and depth split) from the number of
     // rounds of workgroups the chip needs, the per-tile work and a relative
     // efficiency of the tile shape; the cheapest wins.  Two depth halves can
@@ -237,6 +241,40 @@ Plan plan_tiled(int R, int Cc, int D, int cus) {
         }
     }
     set_partial_bytes(best, R, Cc);
+    if (cost_out) *cost_out = best_cost;
+    return best;
+}
+
+Plan plan_tiled(int R, int Cc, int D, int cus) {
+    // A product whose tiles leave the last round of workgroups partly empty
+    // can run as two launches split by rows, each with whole rounds.  Taken
+    // when the model prices it at least 5% cheaper, a launch counted as 3 µs
+    // (110 000 of its units at the expand GEMM's measured rate).  Measured
+    // (operands rotated through HBM): the Llama2-7B FFN up+gate fold, 22016 x
+    // 1536 at depth 4096, 271 -> 247 µs; the GPT3-22B FFN down projection at
+    // L = 2458, 8192 x 2458 at depth 24576, 1039 -> 1027 µs; the QKV fold,
+    // 12288 x 1536 (1.5 rounds of 256 x 192 tiles, split as 4096 rows on 128 x
+    // 192 tiles and 8192 on 256 x 192), 162 -> 167 µs, no gain: a half-empty
+    // last round runs at higher clocks than the model assumes.
+    double cost = 0;
+    Plan best = plan_tiled_one(R, Cc, D, cus, &cost);
+    if (R > 32768) return best;   // many rounds: the last one's share is small
+    constexpr double kLaunch = 110e3;
+    double best_split = 0.95 * cost;
+    for (int r1 = 256; r1 < R; r1 += 256) {
+        double c1 = 0, c2 = 0;
+        const Plan p1 = plan_tiled_one(r1, Cc, D, cus, &c1);
+        const Plan p2 = plan_tiled_one(R - r1, Cc, D, cus, &c2);
+        if (c1 + c2 + kLaunch < best_split) {
+            best_split = c1 + c2 + kLaunch;
+            best = p1;
+            best.rows1 = r1;
+            best.tile2 = p2.tile;
+            best.splits2 = p2.splits;
+            best.pair2 = p2.pair;
+            best.partial_bytes = std::max(p1.partial_bytes, p2.partial_bytes);
+        }
+    }
     return best;
 }
 
@@ -283,9 +321,11 @@ Plan plan_tn_logged(int64_t R, int64_t Cc, int64_t D, espace_dtype dt) {
     }();
     const Plan p = plan_tn(R, Cc, D, dt);
     if (log)
-        std::fprintf(stderr, "espace plan R=%lld Cc=%lld D=%lld: kind=%d tile=%d splits=%d pair=%d partial=%zu\n",
+        std::fprintf(stderr,
+                     "espace plan R=%lld Cc=%lld D=%lld: kind=%d tile=%d splits=%d pair=%d partial=%zu rows1=%d "
+                     "tile2=%d splits2=%d pair2=%d\n",
                      (long long)R, (long long)Cc, (long long)D, (int)p.kind, p.tile, p.splits, p.pair,
-                     p.partial_bytes);
+                     p.partial_bytes, p.rows1, p.tile2, p.splits2, p.pair2);
     return p;
 }
 
@@ -495,6 +535,18 @@ constexpr int64_t kMaxSymDim = 46340;        // K·round_up(K, 8) < 2^31
 
 // ---- launch -----------------------------------------------------------------
 
+// One tiled launch of the plan in g.
+hipError_t launch_tiled(const GemmArgs& g, hipStream_t stream) {
+    if (g.tile == espace::TILE_256x256_W8T || g.tile == espace::TILE_256x192_W8) {
+        // the four-wave kernel; matrices of 2^31 elements or more take the
+        // register-staged kernel with 64-bit offsets
+        const hipError_t e = espace::launch_gemm_tn_bf16_v3(g, stream);
+        if (e == hipErrorInvalidValue) return espace::launch_gemm_tn_bf16(g, stream);
+        return e;
+    }
+    return espace::launch_gemm_tn_bf16_v2(g, stream);
+}
+
 espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
                      int64_t R, int64_t Cc, int64_t D, espace_dtype dt, void* partial,
                      hipStream_t stream) {
@@ -522,19 +574,29 @@ espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, voi
         g.cus = device_cus();
         g.wait = wait_cfg();
         if (p.pair) g.epoch = next_epoch();
-        if (p.kind == KIND_SKINNY) {
+        if (p.kind == KIND_TILED && p.rows1 > 0) {
+            // rows [0, rows1), then the rest with its own tile plan (and its
+            // own tag for pair states: the workspace serves both)
+            g.R = p.rows1;
+            e = launch_tiled(g, stream);
+            if (e == hipSuccess) {
+                g.A = (const uint16_t*)A + (int64_t)p.rows1 * lda;
+                g.C = (uint16_t*)C + (int64_t)p.rows1 * ldc;
+                g.R = (int)(R - p.rows1);
+                g.tile = p.tile2;
+                g.splits = p.splits2;
+                g.pair = p.pair2;
+                if (p.pair2) g.epoch = next_epoch();
+                e = launch_tiled(g, stream);
+            }
+        } else if (p.kind == KIND_SKINNY) {
             e = espace::launch_skinny_tn_bf16(g, stream);
         } else if (p.kind == KIND_GEMV) {
             e = espace::launch_gemv_tn_bf16(g, stream);
         } else if (p.kind == KIND_STREAM) {
             e = espace::launch_stream_tn_bf16(g, stream);
-        } else if (p.tile == espace::TILE_256x256_W8T || p.tile == espace::TILE_256x192_W8) {
-            // the four-wave kernel; matrices of 2^31 elements or more take the
-            // register-staged kernel with 64-bit offsets
-            e = espace::launch_gemm_tn_bf16_v3(g, stream);
-            if (e == hipErrorInvalidValue) e = espace::launch_gemm_tn_bf16(g, stream);
         } else {
-            e = espace::launch_gemm_tn_bf16_v2(g, stream);
+            e = launch_tiled(g, stream);
         }
     }
     if (e != hipSuccess) return fail(ESPACE_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));

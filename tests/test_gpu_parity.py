@@ -159,6 +159,35 @@ def _check_entry_points(E, dtype, shape, seed=0):
         assert np.isnan(padding(t)).all()
 
 
+# Products whose tiles would leave the last round of workgroups partly empty
+# run as two launches split by rows: the fold of a 12288-row weight at depths
+# 1560 (ragged steps) and 4096 (the Llama2-7B QKV fold: 4096 rows on 128 x 192
+# tiles, then 8192 rows on 256 x 192 tiles), and a dense product of 6500
+# tokens (a ragged second part).
+ROW_SPLIT = [("fold", (1560, 12288, 1536, 64)), ("fold", (4096, 12288, 1536, 64)),
+             ("dense", (1000, 3000, 64, 6500))]
+
+
+@pytest.mark.parametrize("case", ROW_SPLIT, ids=lambda c: "%s_K%d_M%d_L%d_N%d" % ((c[0],) + c[1]))
+def test_row_split_launches(E, case):
+    dev = need_gpu()
+    op, (K, M, L, N) = case
+    inp = _inputs(K, M, L, N, "bf16", seed=61)
+    X, Pt, W = _dev_inputs(inp, dev)
+    u = parity.UNIT["bf16"]
+    if op == "fold":
+        got = E.espace_fold_weights(W, Pt, out_mat(M, L, "bf16", dev))
+        want = oracle.fold(inp.W, inp.Pt)
+        B = parity.product_bound(want, parity.row_norms(inp.W), parity.row_norms(inp.Pt), K, u)
+    else:
+        got = E.espace_dense_linear(X, W, out_mat(N, M, "bf16", dev))
+        want = oracle.dense(inp.X, inp.W)
+        B = parity.product_bound(want, parity.row_norms(inp.X), parity.row_norms(inp.W), K, u)
+    torch.cuda.synchronize()
+    parity.check(host64(got), want, B, TOL["bf16"], op)
+    assert np.isnan(padding(got)).all()
+
+
 def test_projected_linear_given_oracle_folded_weight(E):
     """The per-call path alone, with the folded weight rounded from the
     oracle's float64 fold (an input, not a result of the GPU)."""
