@@ -248,11 +248,13 @@ Plan plan_tiled_one(int R, int Cc, int D, int cus, double* cost_out) {
 Plan plan_tiled(int R, int Cc, int D, int cus) {
     // A product whose tiles leave the last round of workgroups partly empty
     // can run as two launches split by rows, each with whole rounds.  Taken
-    // when the model prices it at least 5% cheaper, a launch counted as 3 µs
+    // when the model prices it at least 3% cheaper, a launch counted as 3 µs
     // (110 000 of its units at the expand GEMM's measured rate).  Measured
     // (operands rotated through HBM): the Llama2-7B FFN up+gate fold, 22016 x
-    // 1536 at depth 4096, 271 -> 247 µs; the GPT3-22B FFN down projection at
-    // L = 2458, 8192 x 2458 at depth 24576, 1039 -> 1027 µs; the QKV fold,
+    // 1536 at depth 4096, 271 -> 247 µs; the GPT3-22B FFN up projection at
+    // L = 2458, 8192 x 2458 at depth 6144, 258 -> 240 µs, and the down one,
+    // depth 24576, 1039 -> 1027 µs; the up+gate dense product (4096 x 22016 x
+    // 4096) 593 -> 597 µs, within the noise; the QKV fold,
     // 12288 x 1536 (1.5 rounds of 256 x 192 tiles, split as 4096 rows on 128 x
     // 192 tiles and 8192 on 256 x 192), 162 -> 167 µs, no gain: a half-empty
     // last round runs at higher clocks than the model assumes.
@@ -260,7 +262,7 @@ Plan plan_tiled(int R, int Cc, int D, int cus) {
     Plan best = plan_tiled_one(R, Cc, D, cus, &cost);
     if (R > 32768) return best;   // many rounds: the last one's share is small
     constexpr double kLaunch = 110e3;
-    double best_split = 0.95 * cost;
+    double best_split = 0.97 * cost;
     for (int r1 = 256; r1 < R; r1 += 256) {
         double c1 = 0, c2 = 0;
         const Plan p1 = plan_tiled_one(r1, Cc, D, cus, &c1);
