@@ -3,6 +3,7 @@
     python profile_summary.py stats TRACE_CSV OUT_MD CMD [--steps S --warmup W]
     python profile_summary.py traffic FETCH_CSV WRITE_CSV OUT_MD CMD_FETCH CMD_WRITE
     python profile_summary.py counters OUT_MD --run CSV CMD [--run CSV CMD ...]
+    python profile_summary.py loadpath OUT_MD --run CSV CMD [--run CSV CMD ...]
 
 `stats` reads a `--kernel-trace --output-format csv` trace and tabulates
 launches per kernel and grid; the 256x256 GEMM launches that serve both the
@@ -14,7 +15,11 @@ what the same counters read for the 1 GiB elementwise copy of that run.
 splits each run's dispatches into the probe's phases at its marker kernels
 and tabulates every counter per phase and kernel, with the MFMA busy ratio,
 the MFMA flops against the algorithmic flops, and the byte counters scaled
-by the copy calibration.
+by the copy calibration.  `loadpath` reads `--pmc` runs of the same probe
+with the memory-pipeline counters and tabulates, for the tiled GEMMs, how
+busy and how stalled the load path of the CUs (TA, TD, TCP) and the L2
+channels were, the share of wave time spent in s_waitcnt, and the L2
+requests against the operand bytes the tiles read.
 """
 import argparse
 import collections
@@ -265,6 +270,73 @@ def counters(args):
     print("\n".join(lines))
 
 
+# operand bytes the tiles of a tiled GEMM read from L2 per launch: tiles x
+# (tile rows + tile columns) x depth x element bytes
+LOADPATH_PHASES = {
+    "project": ("4096 x 1536, depth 4096, 128 x 192 tiles", 32 * 8 * (128 + 192) * 4096 * 2),
+    "expand": ("4096 x 12288, depth 1536, 256 x 256 tiles", 16 * 48 * 512 * 1536 * 2),
+    "dense": ("4096 x 12288, depth 4096, 256 x 256 tiles", 16 * 48 * 512 * 4096 * 2),
+}
+
+
+def loadpath(args):
+    """Per-CU load path of the tiled GEMMs.  The per-unit counters are sums
+    over their instances: TA, TD and TCP one per CU (256), TCC one per L2
+    channel (16 per XCD, 128); GRBM_GUI_ACTIVE sums the 8 XCDs' active
+    cycles, so one unit's share of the kernel's cycles is counter /
+    (GRBM_GUI_ACTIVE / 8 x units)."""
+    table = collections.defaultdict(lambda: collections.defaultdict(list))
+    kname = {}
+    for path, _ in args.run:
+        ds = _dispatches(path)
+        for ph, rows in _phases(ds, PROBE_PHASES).items():
+            if ph not in LOADPATH_PHASES:
+                continue
+            for d in rows:
+                if "gemm_tn" not in d["name"]:
+                    continue
+                kname[ph] = _short(d["name"])
+                for c, v in d["c"].items():
+                    table[ph][c].append(v)
+    lines = ["# Load-path counters of the tiled GEMMs: Llama2-7B fused QKV (K=4096, M=12288, L=1536, N=4096)", "",
+             "The projection, the expand GEMM and the dense baseline of `bench.py --kernel-probe` (bf16, "
+             "weights rotated over copies larger than the last-level cache).  Counter runs (from the "
+             "repository root, on one MI355X):", "", "```"]
+    lines += [cmd for _, cmd in args.run] + ["```", ""]
+    lines += ["Per launch.  Unit shares: counter / (GRBM_GUI_ACTIVE / 8 x units), units = 256 (TA, TD, "
+              "TCP: one per CU) or 128 (TCC: one per L2 channel).  TA busy: the address unit; TA stalled: "
+              "cycles the TA could not pass addresses to the TCP (TA_ADDR_STALLED_BY_TC_CYCLES); TD busy / "
+              "TD stalled: the data-return unit and its cycles waiting for the TCP (TD_TC_STALL); TCP pending: "
+              "cycles the L1 waited for data from L2 (TCP_PENDING_STALL_CYCLES); L2 busy: TCC_BUSY.  "
+              "waitcnt: SQ_WAIT_INST_ANY over SQ_WAVE_CYCLES.  Bytes per L2 request: the operand bytes the "
+              "tiles read over TCC_HIT + TCC_MISS (which also count the output writes).", "",
+              "| phase | kernel | shape | MFMA busy % | waitcnt % | TA busy % | TA stalled % | TD busy % | "
+              "TD stalled % | TCP pending % | L2 busy % | L2 hit % | L2 requests (M) | operand B / request |",
+              "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for ph, (shape, opb) in LOADPATH_PHASES.items():
+        if ph not in table:
+            continue
+        m = {c: sum(v) / len(v) for c, v in table[ph].items()}
+        cyc = m.get("GRBM_GUI_ACTIVE", 0.0) / 8.0
+
+        def share(c, units):
+            return f"{100.0 * m[c] / (cyc * units):.0f}" if c in m and cyc else ""
+
+        busy = f"{100.0 * m['SQ_VALU_MFMA_BUSY_CYCLES'] / (cyc * 1024):.0f}" \
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in m and cyc else ""
+        wait = f"{100.0 * m['SQ_WAIT_INST_ANY'] / m['SQ_WAVE_CYCLES']:.0f}" \
+            if "SQ_WAIT_INST_ANY" in m and m.get("SQ_WAVE_CYCLES") else ""
+        req = m.get("TCC_HIT", 0.0) + m.get("TCC_MISS", 0.0)
+        hit = f"{100.0 * m['TCC_HIT'] / req:.0f}" if req else ""
+        lines.append(f"| {ph} | `{kname[ph]}` | {shape} | {busy} | {wait} | {share('TA_TA_BUSY', 256)} | "
+                     f"{share('TA_ADDR_STALLED_BY_TC_CYCLES', 256)} | {share('TD_TD_BUSY', 256)} | "
+                     f"{share('TD_TC_STALL', 256)} | {share('TCP_PENDING_STALL_CYCLES', 256)} | "
+                     f"{share('TCC_BUSY', 128)} | {hit} | {req / 1e6:.2f} | "
+                     f"{opb / req:.0f} |" if req else "")
+    open(args.out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="mode", required=True)
@@ -283,8 +355,11 @@ def main():
     c = sub.add_parser("counters")
     c.add_argument("out")
     c.add_argument("--run", nargs=2, action="append", metavar=("CSV", "CMD"), required=True)
+    d = sub.add_parser("loadpath")
+    d.add_argument("out")
+    d.add_argument("--run", nargs=2, action="append", metavar=("CSV", "CMD"), required=True)
     args = ap.parse_args()
-    {"stats": stats, "traffic": traffic, "counters": counters}[args.mode](args)
+    {"stats": stats, "traffic": traffic, "counters": counters, "loadpath": loadpath}[args.mode](args)
 
 
 if __name__ == "__main__":
