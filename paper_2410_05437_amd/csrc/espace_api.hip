@@ -341,8 +341,11 @@ int64_t z_ld(int64_t L, int64_t N, espace_dtype dt) {
     return round_up(L, 64) + (N <= 32 ? 32 : 0);
 }
 
+// Bytes of Z in the workspace: N rows of z_ld elements, or for prefill
+// (N > 32) as many row pairs of 2 z_ld elements (the row-pair layout, below)
 size_t z_bytes(int64_t N, int64_t L, espace_dtype dt) {
-    return align_ws((size_t)N * z_ld(L, N, dt) * elem_size(dt));
+    const int64_t rows = N > 32 ? round_up(N, 2) : N;
+    return align_ws((size_t)rows * z_ld(L, N, dt) * elem_size(dt));
 }
 
 // Workspace of the training-view gradients: transposed operands (the GEMM
@@ -541,17 +544,19 @@ constexpr int64_t kMaxSymDim = 46340;        // K·round_up(K, 8) < 2^31
 hipError_t launch_tiled(const GemmArgs& g, hipStream_t stream) {
     if (g.tile == espace::TILE_256x256_W8T || g.tile == espace::TILE_256x192_W8) {
         // the four-wave kernel; matrices of 2^31 elements or more take the
-        // register-staged kernel with 64-bit offsets
+        // register-staged kernel with 64-bit offsets (plain layouts only)
         const hipError_t e = espace::launch_gemm_tn_bf16_v3(g, stream);
-        if (e == hipErrorInvalidValue) return espace::launch_gemm_tn_bf16(g, stream);
+        if (e == hipErrorInvalidValue && !g.a_pairs && !g.c_pairs) return espace::launch_gemm_tn_bf16(g, stream);
         return e;
     }
     return espace::launch_gemm_tn_bf16_v2(g, stream);
 }
 
+// a_pairs / c_pairs: A is read, C written in the row-pair layout (GemmArgs);
+// only for the tiled plans z_pairs admits
 espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
                      int64_t R, int64_t Cc, int64_t D, espace_dtype dt, void* partial,
-                     hipStream_t stream) {
+                     hipStream_t stream, int a_pairs = 0, int c_pairs = 0) {
     hipError_t e;
     if (dt == ESPACE_F32) {
         e = espace::launch_gemm_tn_f32((const float*)A, lda, (const float*)B, ldb, (float*)C, ldc,
@@ -575,7 +580,11 @@ espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, voi
         g.pair = p.pair;
         g.cus = device_cus();
         g.wait = wait_cfg();
+        g.a_pairs = a_pairs;
+        g.c_pairs = c_pairs;
         if (p.pair) g.epoch = next_epoch();
+        if ((a_pairs || c_pairs) && (p.kind != KIND_TILED || p.rows1 > 0))
+            return fail(ESPACE_ERR_HIP, "row-pair layout on a plan that does not take it");
         if (p.kind == KIND_TILED && p.rows1 > 0) {
             // rows [0, rows1), then the rest with its own tile plan (and its
             // own tag for pair states: the workspace serves both)
@@ -605,14 +614,42 @@ espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, voi
     return ESPACE_OK;
 }
 
+// Whether the layer keeps Z in the row-pair layout (GemmArgs): every 128-byte
+// line then holds the 32-deep blocks of two tokens, so the expand GEMM's
+// 64-byte half-rows of Z arrive as whole lines, half the L2 requests for
+// that operand (the load path of the CUs bounds these GEMMs; in a probe of
+// the expand's operand stream with the fragment reads, 121 -> 114 µs).
+// Taken for prefill when the projection is one tiled launch whose kernel
+// writes bf16 itself (one depth range or the pair combine) and the expand
+// GEMM is one single-range launch of the four-wave kernel.
+bool z_pairs(int64_t N, int64_t L, int64_t K, int64_t M, int64_t ldx, int64_t ldp, int64_t ldwf, int64_t ldy,
+             espace_dtype dt) {
+    if (dt != ESPACE_BF16 || N <= 32) return false;
+    const Plan a = plan_tn(N, L, K, dt);
+    const Plan b = plan_tn(N, M, L, dt);
+    if (a.kind != KIND_TILED || a.rows1 > 0 || (a.splits > 1 && !(a.pair && a.splits == 2))) return false;
+    if (b.kind != KIND_TILED || b.rows1 > 0 || b.splits != 1) return false;
+    if (b.tile != espace::TILE_256x256_W8T && b.tile != espace::TILE_256x192_W8) return false;
+    // the kernels' 32-bit offsets (the register-staged fallback keeps plain layouts)
+    const int64_t lim = (int64_t)1 << 31;
+    const int64_t ldzp = 2 * z_ld(L, N, dt);
+    return N * ldx < lim && L * ldp < lim && N * ldzp < lim && M * ldwf < lim && N * ldy < lim;
+}
+
 // The layer's launches after validation: Z and the partial sums in
 // `workspace` (ws_bytes(ESPACE_OP_PROJECTED_LINEAR, ...) bytes).
 espace_status projected_linear_launch(const void* X, int64_t ldx, const void* Pt, int64_t ldp, const void* Wf,
                                       int64_t ldwf, void* Y, int64_t ldy, int64_t M, int64_t K, int64_t L,
                                       int64_t N, espace_dtype dt, void* workspace, hipStream_t stream) {
-    const int64_t ldz = z_ld(L, N, dt);
     void* Z = workspace;
     void* partial = (char*)workspace + z_bytes(N, L, dt);
+    if (z_pairs(N, L, K, M, ldx, ldp, ldwf, ldy, dt)) {
+        const int64_t ldzp = 2 * z_ld(L, N, dt);   // elements per row pair
+        ESPACE_TRY(run_tn(X, ldx, Pt, ldp, Z, ldzp, N, L, K, dt, partial, stream, 0, 1));
+        ESPACE_TRY(run_tn(Z, ldzp, Wf, ldwf, Y, ldy, N, M, L, dt, partial, stream, 1, 0));
+        return ESPACE_OK;
+    }
+    const int64_t ldz = z_ld(L, N, dt);
     ESPACE_TRY(run_tn(X, ldx, Pt, ldp, Z, ldz, N, L, K, dt, partial, stream));
     ESPACE_TRY(run_tn(Z, ldz, Wf, ldwf, Y, ldy, N, M, L, dt, partial, stream));
     return ESPACE_OK;

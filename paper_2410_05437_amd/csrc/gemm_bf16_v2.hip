@@ -294,7 +294,7 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
                             void* __restrict__ Cout, int64_t ldc,
                             int R, int Cc, int D, int tiles_c, int ktiles_per_split,
                             int64_t split_stride, int map, unsigned long long* tile_state,
-                            float* pair_part, unsigned long long epoch, WaitCfg wc) {
+                            float* pair_part, unsigned long long epoch, WaitCfg wc, int c_pairs) {
     using T = Cfg<BM, BN, WM, WN, BK, STAGES, MI>;
     using Acc = typename AccOf<MI>::type;
     __shared__ __attribute__((aligned(1024))) unsigned char smem[T::SMEM];
@@ -460,7 +460,9 @@ void gemm_tn_bf16_v2_kernel(const uint16_t* __restrict__ A, int64_t lda,
             if (!lane_used || rl >= T::WTM) continue;
             const u32x4_t v = *reinterpret_cast<const u32x4_t*>(ep + rl * T::EPI_LD + cl * 2);
             if (r < R) {
-                uint16_t* p = C + (int64_t)r * ldc + c;
+                // c is a multiple of 8: the chunk stays inside one 32-column
+                // block of the row-pair layout
+                uint16_t* p = C + (c_pairs ? pair_offset(r, c, ldc) : (int64_t)r * ldc + c);
                 if (c + 8 <= Cc) {
                     *reinterpret_cast<u32x4_t*>(p) = v;
                 } else if (c < Cc) {
@@ -485,7 +487,7 @@ hipError_t launch_v2(const GemmArgs& g, hipStream_t stream) {
     if (S == 1) {
         hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_BF16, MI>), grid, block,
                            0, stream, g.A, g.lda, g.B, g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c,
-                           ktps, (int64_t)0, 0, nullptr, nullptr, 0ull, g.wait);
+                           ktps, (int64_t)0, 0, nullptr, nullptr, 0ull, g.wait, g.c_pairs);
         return hipGetLastError();
     }
     if (S == 2 && g.pair) {
@@ -496,14 +498,14 @@ hipError_t launch_v2(const GemmArgs& g, hipStream_t stream) {
             reinterpret_cast<unsigned long long*>(g.partial + (size_t)ntiles * BM * BN);
         hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_PAIR, MI>), grid, block,
                            0, stream, g.A, g.lda, g.B, g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c,
-                           ktps, (int64_t)0, 0, state, g.partial, g.epoch, g.wait);
+                           ktps, (int64_t)0, 0, state, g.partial, g.epoch, g.wait, g.c_pairs);
         return hipGetLastError();
     }
     const int64_t ldp = splitk_ld(g.Cc);
     const int64_t split_stride = (int64_t)g.R * ldp;
     hipLaunchKernelGGL((gemm_tn_bf16_v2_kernel<BM, BN, WM, WN, BK, STAGES, MODE_F32, MI>), grid, block, 0,
                        stream, g.A, g.lda, g.B, g.ldb, (void*)g.partial, ldp, g.R, g.Cc, g.D,
-                       tiles_c, ktps, split_stride, 0, nullptr, nullptr, 0ull, g.wait);
+                       tiles_c, ktps, split_stride, 0, nullptr, nullptr, 0ull, g.wait, 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_splitk_reduce(g.partial, S, split_stride, ldp, g.C, g.ldc, g.R, g.Cc,
@@ -534,8 +536,14 @@ void tile_dims(int tile, int* bm, int* bn) {
 // offsets).
 hipError_t launch_gemm_tn_bf16_v2(const GemmArgs& g, hipStream_t stream) {
     const int64_t lim = (int64_t)1 << 31;
-    if ((int64_t)g.R * g.lda >= lim || (int64_t)g.Cc * g.ldb >= lim || g.c_f32)
+    // a row-pair output: one depth range or the pair combine, whole 64-element
+    // blocks per pair; A is always plain here
+    if (g.a_pairs || (g.c_pairs && ((g.splits > 1 && !(g.pair && g.splits == 2)) || g.ldc % 64 || g.c_f32)))
+        return hipErrorNotSupported;
+    if ((int64_t)g.R * g.lda >= lim || (int64_t)g.Cc * g.ldb >= lim || g.c_f32) {
+        if (g.c_pairs) return hipErrorNotSupported;
         return launch_gemm_tn_bf16(g, stream);   // runs a pair plan as one depth range
+    }
     switch (g.tile) {
         case TILE_256x128: return launch_v2<256, 128, 2, 2, 64, 2>(g, stream);
         case TILE_128x256: return launch_v2<128, 256, 2, 2, 64, 2>(g, stream);

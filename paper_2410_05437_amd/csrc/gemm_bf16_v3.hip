@@ -48,15 +48,17 @@ namespace {
 // per wave (out-of-range lanes use an offset past the buffer, which the
 // hardware drops), so the next item waits for its first step with
 // vmcnt(2 LPH + NST).  MODE_PAIR: two depth ranges (blockIdx.y) of a tile
-// meet in v3_pair; `tile_state` and `pair_part` as there.
-template <int MODE, int BN>
+// meet in v3_pair; `tile_state` and `pair_part` as there.  APAIR: A is in
+// the row-pair layout (pair_offset, lda its pair pitch); c_pairs: the bf16
+// output is written in that layout (ldc its pair pitch).
+template <int MODE, int BN, int APAIR = 0>
 __global__ __launch_bounds__(256, 1)
 void gemm_tn_bf16_v3_kernel(const uint16_t* __restrict__ A, int64_t lda,
                             const uint16_t* __restrict__ B, int64_t ldb,
                             void* __restrict__ Cout, int64_t ldc,
                             int R, int Cc, int D, int tiles_c, int ntiles, int ktiles_per_split,
                             int64_t split_stride, int map, unsigned long long* tile_state,
-                            float* pair_part, unsigned long long epoch, WaitCfg wc) {
+                            float* pair_part, unsigned long long epoch, WaitCfg wc, int c_pairs) {
     using C = V3Cfg<BN>;
     constexpr int NBJ = C::NBJ;
     __shared__ __attribute__((aligned(1024))) unsigned char smem[C::SMEM];
@@ -74,7 +76,7 @@ void gemm_tn_bf16_v3_kernel(const uint16_t* __restrict__ A, int64_t lda,
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wrow0 = (wave >> 1) * V3_WT;
     const int wcol0 = (wave & 1) * (BN / 2);
-    const unsigned ra = (unsigned)((uint64_t)R * lda * 2u);
+    const unsigned ra = (unsigned)((uint64_t)(APAIR ? (R + 1) / 2 : R) * lda * 2u);
     const unsigned rb = (unsigned)((uint64_t)Cc * ldb * 2u);
 
     // fragment row addresses: a lane reads row lane % 16 of each 16-row block
@@ -119,12 +121,12 @@ void gemm_tn_bf16_v3_kernel(const uint16_t* __restrict__ A, int64_t lda,
         } else {
             // the half-stages may still be read by a wave finishing the previous item
             if (item != (int)blockIdx.x) __syncthreads();
-            v3_offsets<C>(voff, row0, col0, R, Cc, lda, ldb, wave, lane);
-            int later = v3_load_half<C>(smem, A, B, ra, rb, voff, wave, lane, kt0, 0, hs(0, 0), D);
-            later = v3_load_half<C>(smem, A, B, ra, rb, voff, wave, lane, kt0, 1, hs(0, 1), D);
+            v3_offsets<C, 1, APAIR != 0>(voff, row0, col0, R, Cc, lda, ldb, wave, lane);
+            int later = v3_load_half<C, APAIR != 0>(smem, A, B, ra, rb, voff, wave, lane, kt0, 0, hs(0, 0), D);
+            later = v3_load_half<C, APAIR != 0>(smem, A, B, ra, rb, voff, wave, lane, kt0, 1, hs(0, 1), D);
             if (nsteps > 1) {
-                later = v3_load_half<C>(smem, A, B, ra, rb, voff, wave, lane, kt0 + 1, 0, hs(1, 0), D);
-                later += v3_load_half<C>(smem, A, B, ra, rb, voff, wave, lane, kt0 + 1, 1, hs(1, 1), D);
+                later = v3_load_half<C, APAIR != 0>(smem, A, B, ra, rb, voff, wave, lane, kt0 + 1, 0, hs(1, 0), D);
+                later += v3_load_half<C, APAIR != 0>(smem, A, B, ra, rb, voff, wave, lane, kt0 + 1, 1, hs(1, 1), D);
             } else {
                 later = 0;
             }
@@ -156,7 +158,7 @@ void gemm_tn_bf16_v3_kernel(const uint16_t* __restrict__ A, int64_t lda,
             lkt = kt0 + (kt + 2 - kt_end);
             if (!ahead_next) return 0;
             if (kt + 2 == kt_end && h == 0)
-                v3_offsets<C>(voff, ntr * V3_BM, ntc * BN, R, Cc, lda, ldb, wave, lane);
+                v3_offsets<C, 1, APAIR != 0>(voff, ntr * V3_BM, ntc * BN, R, Cc, lda, ldb, wave, lane);
             return 1;
         };
         // one step with the stage chosen at run time (the first one and the
@@ -169,9 +171,9 @@ void gemm_tn_bf16_v3_kernel(const uint16_t* __restrict__ A, int64_t lda,
             // sub-step 0: fragments of sub-step 1 from the second half-stage
             int lkt;
             const int k0 = load_kind(0, lkt);
-            v3_substep<C, F, true, true>(acc, fa0, fb0, fa1, fb1, rel ? aA3 : aA1, rel ? aB3 : aB1, smem,
+            v3_substep<C, F, true, true, APAIR != 0>(acc, fa0, fb0, fa1, fb1, rel ? aA3 : aA1, rel ? aB3 : aB1, smem,
                                          A, B, ra, rb, voff, wave, lkt, 0, hs(rel, 0), k0 == 1);
-            if (k0 == 2) v3_load_half<C>(smem, A, B, ra, rb, voff, wave, lane, lkt, 0, hs(rel, 0), D);
+            if (k0 == 2) v3_load_half<C, APAIR != 0>(smem, A, B, ra, rb, voff, wave, lane, lkt, 0, hs(rel, 0), D);
             const int n0 = k0 == 1 ? C::LPH : 0;
             v3_wait_lgkm0();
             if (kt + 1 < kt_end || ahead_next) {
@@ -183,9 +185,9 @@ void gemm_tn_bf16_v3_kernel(const uint16_t* __restrict__ A, int64_t lda,
             // last step the reads are of no use but harmless: one code path
             // keeps the accumulators in place)
             const int k1 = load_kind(1, lkt);
-            v3_substep<C, false, true, true>(acc, fa1, fb1, fa0, fb0, rel ? aA0 : aA2, rel ? aB0 : aB2,
+            v3_substep<C, false, true, true, APAIR != 0>(acc, fa1, fb1, fa0, fb0, rel ? aA0 : aA2, rel ? aB0 : aB2,
                                              smem, A, B, ra, rb, voff, wave, lkt, 1, hs(rel, 1), k1 == 1);
-            if (k1 == 2) v3_load_half<C>(smem, A, B, ra, rb, voff, wave, lane, lkt, 1, hs(rel, 1), D);
+            if (k1 == 2) v3_load_half<C, APAIR != 0>(smem, A, B, ra, rb, voff, wave, lane, lkt, 1, hs(rel, 1), D);
             const int n1 = k1 == 1 ? C::LPH : 0;
             v3_wait_lgkm0();
             if (kt + 1 < kt_end) {
@@ -202,22 +204,22 @@ void gemm_tn_bf16_v3_kernel(const uint16_t* __restrict__ A, int64_t lda,
         // barrier waits for the half-stage the next sub-step reads, with the
         // two newer half-steps of loads in flight
         while (kt + 3 < nfull) {
-            v3_substep<C, false, true, true>(acc, fa0, fb0, fa1, fb1, aA3, aB3, smem, A, B, ra, rb, voff,
+            v3_substep<C, false, true, true, APAIR != 0>(acc, fa0, fb0, fa1, fb1, aA3, aB3, smem, A, B, ra, rb, voff,
                                              wave, kt + 2, 0, hs(1, 0));
             v3_wait_lgkm0();
             v3_wait_vm<2 * C::LPH>();
             __builtin_amdgcn_s_barrier();
-            v3_substep<C, false, true, true>(acc, fa1, fb1, fa0, fb0, aA0, aB0, smem, A, B, ra, rb, voff,
+            v3_substep<C, false, true, true, APAIR != 0>(acc, fa1, fb1, fa0, fb0, aA0, aB0, smem, A, B, ra, rb, voff,
                                              wave, kt + 2, 1, hs(1, 1));
             v3_wait_lgkm0();
             v3_wait_vm<2 * C::LPH>();
             __builtin_amdgcn_s_barrier();
-            v3_substep<C, false, true, true>(acc, fa0, fb0, fa1, fb1, aA1, aB1, smem, A, B, ra, rb, voff,
+            v3_substep<C, false, true, true, APAIR != 0>(acc, fa0, fb0, fa1, fb1, aA1, aB1, smem, A, B, ra, rb, voff,
                                              wave, kt + 3, 0, hs(0, 0));
             v3_wait_lgkm0();
             v3_wait_vm<2 * C::LPH>();
             __builtin_amdgcn_s_barrier();
-            v3_substep<C, false, true, true>(acc, fa1, fb1, fa0, fb0, aA2, aB2, smem, A, B, ra, rb, voff,
+            v3_substep<C, false, true, true, APAIR != 0>(acc, fa1, fb1, fa0, fb0, aA2, aB2, smem, A, B, ra, rb, voff,
                                              wave, kt + 3, 1, hs(0, 1));
             v3_wait_lgkm0();
             v3_wait_vm<2 * C::LPH>();
@@ -312,18 +314,21 @@ void gemm_tn_bf16_v3_kernel(const uint16_t* __restrict__ A, int64_t lda,
                 // exactly one store instruction per lane group and block
                 // pair, no branches; lanes outside the matrix get an offset
                 // past the buffer, which its range check drops
-                const unsigned cbytes = (unsigned)((uint64_t)R * ldc * 2u);
+                const unsigned cbytes = (unsigned)((uint64_t)(c_pairs ? (R + 1) / 2 : R) * ldc * 2u);
                 const auto crsrc = __builtin_amdgcn_make_buffer_rsrc((void*)Cb, (short)0, (int)cbytes, 0x00020000);
 #pragma unroll
                 for (int i = 0; i < V3_NB; ++i) {
                     if (i + C::PD < V3_NB) part_row(i + C::PD);
                     const int r = row0 + wrow0 + 16 * i + lr;
-                    const unsigned rowoff = (unsigned)r * (unsigned)ldc;
+                    // row pairs: row r's 32-column blocks are 64 elements apart
+                    const unsigned rowoff = c_pairs ? (unsigned)(r >> 1) * (unsigned)ldc + (unsigned)((r & 1) * 32)
+                                                    : (unsigned)r * (unsigned)ldc;
 #pragma unroll
                     for (int m = 0; m < NBJ / 2; ++m) {
                         const u32x4_t v = pair_row(i, m);
                         const int c = cl0 + 32 * m;
-                        const unsigned off = (r < R && c < Cc) ? (rowoff + (unsigned)c) * 2u : 0xFFFFFFF0u;
+                        const unsigned cc = c_pairs ? (unsigned)((c >> 5) * 64 + (c & 31)) : (unsigned)c;
+                        const unsigned off = (r < R && c < Cc) ? (rowoff + cc) * 2u : 0xFFFFFFF0u;
                         __builtin_amdgcn_raw_buffer_store_b128(v, crsrc, (int)off, 0, 0);
                     }
                 }
@@ -337,7 +342,7 @@ void gemm_tn_bf16_v3_kernel(const uint16_t* __restrict__ A, int64_t lda,
                         const u32x4_t v = pair_row(i, m);
                         const int c = cl0 + 32 * m;
                         if (r < R) {
-                            uint16_t* p = Cb + (int64_t)r * ldc + c;
+                            uint16_t* p = Cb + (c_pairs ? pair_offset(r, c, ldc) : (int64_t)r * ldc + c);
                             if (c + 8 <= Cc) {
                                 *reinterpret_cast<u32x4_t*>(p) = v;
                             } else if (c < Cc) {
@@ -385,9 +390,14 @@ hipError_t launch_v3(const GemmArgs& g, hipStream_t stream) {
         // one workgroup per CU, each taking every cus-th tile
         const int persistent = g.cus > 0 ? g.cus : 256;
         dim3 grid(ntiles < persistent ? ntiles : persistent, 1);
-        hipLaunchKernelGGL((gemm_tn_bf16_v3_kernel<V3_BF16, BN>), grid, block, 0, stream, g.A, g.lda, g.B,
-                           g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c, ntiles, ktps, (int64_t)0, map,
-                           nullptr, nullptr, 0ull, g.wait);
+        if (g.a_pairs)
+            hipLaunchKernelGGL((gemm_tn_bf16_v3_kernel<V3_BF16, BN, 1>), grid, block, 0, stream, g.A, g.lda, g.B,
+                               g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c, ntiles, ktps, (int64_t)0, map,
+                               nullptr, nullptr, 0ull, g.wait, g.c_pairs);
+        else
+            hipLaunchKernelGGL((gemm_tn_bf16_v3_kernel<V3_BF16, BN>), grid, block, 0, stream, g.A, g.lda, g.B,
+                               g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c, ntiles, ktps, (int64_t)0, map,
+                               nullptr, nullptr, 0ull, g.wait, g.c_pairs);
         return hipGetLastError();
     }
     dim3 grid(ntiles, S);
@@ -397,14 +407,14 @@ hipError_t launch_v3(const GemmArgs& g, hipStream_t stream) {
             reinterpret_cast<unsigned long long*>(g.partial + (size_t)ntiles * V3_BM * BN);
         hipLaunchKernelGGL((gemm_tn_bf16_v3_kernel<V3_PAIR, BN>), grid, block, 0, stream, g.A, g.lda, g.B,
                            g.ldb, g.C, g.ldc, g.R, g.Cc, g.D, tiles_c, ntiles, ktps, (int64_t)0, map,
-                           state, g.partial, g.epoch, g.wait);
+                           state, g.partial, g.epoch, g.wait, g.c_pairs);
         return hipGetLastError();
     }
     const int64_t ldp = splitk_ld(g.Cc);
     const int64_t split_stride = (int64_t)g.R * ldp;
     hipLaunchKernelGGL((gemm_tn_bf16_v3_kernel<V3_F32, BN>), grid, block, 0, stream, g.A, g.lda, g.B,
                        g.ldb, (void*)g.partial, ldp, g.R, g.Cc, g.D, tiles_c, ntiles, ktps, split_stride,
-                       map, nullptr, nullptr, 0ull, g.wait);
+                       map, nullptr, nullptr, 0ull, g.wait, 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_splitk_reduce(g.partial, S, split_stride, ldp, g.C, g.ldc, g.R, g.Cc, 1, stream);
@@ -423,7 +433,7 @@ hipError_t launch_v3_ranges(const GemmArgs& g, bool upper, int* ranges, hipStrea
     const int64_t ldp = splitk_ld(g.Cc);
     hipLaunchKernelGGL((gemm_tn_bf16_v3_kernel<V3_F32, BN>), dim3(ntiles, S), dim3(V3_NW * 64), 0, stream, g.A,
                        g.lda, g.B, g.ldb, (void*)g.partial, ldp, g.R, g.Cc, g.D, tiles_c, ntiles, ktps,
-                       (int64_t)g.R * ldp, upper ? 8 : 0, nullptr, nullptr, 0ull, g.wait);
+                       (int64_t)g.R * ldp, upper ? 8 : 0, nullptr, nullptr, 0ull, g.wait, 0);
     return hipGetLastError();
 }
 
@@ -452,6 +462,15 @@ hipError_t launch_gemm_tn_bf16_v3(const GemmArgs& g, hipStream_t stream) {
     if ((int64_t)g.R * g.lda >= lim || (int64_t)g.Cc * g.ldb >= lim || (int64_t)g.R * g.ldc >= lim ||
         g.c_f32)
         return hipErrorInvalidValue;
+    // row-pair A only on the single-range kernel; a row-pair output only where
+    // the kernel writes bf16 itself (one range or the pair combine); pair
+    // pitches are whole 64-element blocks
+    const int ktiles = (g.D + V3_BK - 1) / V3_BK;
+    const int S = g.splits < 1 ? 1 : g.splits;
+    const int nranges = (ktiles + (ktiles + S - 1) / S - 1) / ((ktiles + S - 1) / S);
+    if ((g.a_pairs && (nranges != 1 || g.lda % 64)) ||
+        (g.c_pairs && ((nranges != 1 && !(g.pair && nranges == 2)) || g.ldc % 64)))
+        return hipErrorNotSupported;
     switch (g.tile) {
         case TILE_256x256:
         case TILE_256x256_W8:

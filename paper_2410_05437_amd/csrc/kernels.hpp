@@ -61,7 +61,19 @@ struct GemmArgs {
     WaitCfg wait;       // bounded waits of the pair combine
     int pair = 0;       // splits == 2 combined inside the kernel (no reduce pass)
     unsigned long long epoch = 0;   // per-call tag of the pair state words
+    // Row-pair layout (a matrix the library keeps to itself: Z in the layer's
+    // workspace).  Element (r, k) sits at (r / 2) * ld + (k / 32) * 64 +
+    // (r % 2) * 32 + k % 32: every 128-byte block holds 32 consecutive
+    // elements of two neighbouring rows, so a 32-deep load of a row pair is
+    // one whole cache line.  ld (elements per row pair) is a multiple of 64.
+    int a_pairs = 0;    // A is in the row-pair layout (lda its pair pitch)
+    int c_pairs = 0;    // write C (bf16) in the row-pair layout (ldc its pair pitch)
 };
+
+// offset (elements) of element (r, k) of a row-pair matrix with pair pitch ld
+__host__ __device__ inline int64_t pair_offset(int64_t r, int64_t k, int64_t ld) {
+    return (r >> 1) * ld + (k >> 5) * 64 + (r & 1) * 32 + (k & 31);
+}
 
 // Tile size of a TileKind in the pair-combine kernel (rows, columns).
 void tile_dims(int tile, int* bm, int* bn);

@@ -99,30 +99,34 @@ __device__ __forceinline__ void v3_read_dyn(int x, bf16x8_t* fa, bf16x8_t* fb, u
 
 // Wave-load j of half h of depth step kt into half-stage u (full depth): it
 // covers rows 16q .. 16q+15 of the A|B tile, q = wave + 4j; j < 4 are A rows.
-template <class C>
+// APAIR: A in the row-pair layout, where the 32-deep block of half h of step
+// kt lies (2 kt + h) * 128 bytes into a row pair (twice the plain offset).
+template <class C, bool APAIR = false>
 __device__ __forceinline__ void v3_load(unsigned char* smem, const uint16_t* A, const uint16_t* B,
                                         unsigned a_bytes, unsigned b_bytes, const int* voff,
                                         int wave, int kt, int h, int u, int j) {
     const int q = wave + 4 * j;
     const auto rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(j < 4 ? A : B), (short)0,
                                                         (int)(j < 4 ? a_bytes : b_bytes), 0x00020000);
+    const int soff = (kt * V3_BK + 32 * h) * ((APAIR && j < 4) ? 4 : 2);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         rsrc, (__attribute__((address_space(3))) void*)(smem + u * C::HS + q * 1024), 16,
-        voff[j], (kt * V3_BK + 32 * h) * 2, 0, 0);
+        voff[j], soff, 0, 0);
 }
 
 // Half h of depth step kt into half-stage u for any step: full depth by
 // buffer_load ... lds (8 per wave, returns 8), the depth tail through
 // registers with the elements at or beyond D zeroed (returns 0: nothing of
 // it stays in flight).
-template <class C>
+template <class C, bool APAIR = false>
 __device__ __forceinline__ int v3_load_half(unsigned char* smem, const uint16_t* A, const uint16_t* B,
                                             unsigned a_bytes, unsigned b_bytes, const int* voff,
                                             int wave, int lane, int kt, int h, int u, int D) {
     const int k0 = kt * V3_BK + 32 * h;
     if (k0 + 32 <= D) {
 #pragma unroll
-        for (int j = 0; j < C::LPH; ++j) v3_load<C>(smem, A, B, a_bytes, b_bytes, voff, wave, kt, h, u, j);
+        for (int j = 0; j < C::LPH; ++j)
+            v3_load<C, APAIR>(smem, A, B, a_bytes, b_bytes, voff, wave, kt, h, u, j);
         return C::LPH;
     }
 #pragma unroll
@@ -130,7 +134,10 @@ __device__ __forceinline__ int v3_load_half(unsigned char* smem, const uint16_t*
         const int q = wave + 4 * j;
         const int rr = q * 16 + (lane >> 2) - (j < 4 ? 0 : V3_BM);
         const int lc = (lane & 3) ^ v3_swz(rr);
-        const uint16_t* rowp = (j < 4 ? A : B) + ((unsigned)voff[j] >> 1) - lc * 8;
+        // plain rows: the row start; row pairs: the row's 32-element block at
+        // depth k0 sits 2 k0 elements past its first block, so the element at
+        // depth k0 + e (e < 32) is at rowp + k0 + (k0 + e)
+        const uint16_t* rowp = (j < 4 ? A : B) + ((unsigned)voff[j] >> 1) - lc * 8 + ((APAIR && j < 4) ? k0 : 0);
         const u32x4_t v = load_chunk_masked(rowp, k0 + lc * 8, D);
         *reinterpret_cast<u32x4_t*>(smem + u * C::HS + q * 1024 + lane * 16) = v;
     }
@@ -142,7 +149,7 @@ __device__ __forceinline__ int v3_load_half(unsigned char* smem, const uint16_t*
 // y of half h of step kt into half-stage u when LOADS and do_load (uniform);
 // FIRST: the accumulators start from zero (the inline constant 0 as the
 // addend).
-template <class C, bool FIRST, bool READS, bool LOADS>
+template <class C, bool FIRST, bool READS, bool LOADS, bool APAIR = false>
 __device__ __forceinline__ void v3_substep(f32x4_t (&acc)[V3_NB][C::NBJ], const bf16x8_t* fa,
                                            const bf16x8_t* fb, bf16x8_t* ra, bf16x8_t* rb,
                                            unsigned aa, unsigned ab, unsigned char* smem,
@@ -165,7 +172,7 @@ __device__ __forceinline__ void v3_substep(f32x4_t (&acc)[V3_NB][C::NBJ], const 
 #pragma unroll
                 for (int y = 0; y < C::LPH; ++y)
                     if (x == C::load_slot(y) && do_load)
-                        v3_load<C>(smem, A, B, a_bytes, b_bytes, voff, wave, kt, h, u, y);
+                        v3_load<C, APAIR>(smem, A, B, a_bytes, b_bytes, voff, wave, kt, h, u, y);
             }
         }
 }
@@ -176,8 +183,11 @@ enum { V3_BF16 = 0, V3_F32 = 1, V3_PAIR = 2 };
 // excluded) for the tile at (row0, col0): row 16q + lane/4 of the A|B tile,
 // logical chunk (lane % 4) ^ swz(row), swz(row) = (row >> SH) & 3 (SH = 1
 // is v3_swz, for the bf16 fragment reads of 16 rows; the fp8 kernel's reads
-// of 32 rows take SH = 2); rows past the matrix are clamped to its last row
-template <class C, int SH = 1>
+// of 32 rows take SH = 2); rows past the matrix are clamped to its last row.
+// APAIR: A in the row-pair layout (lda its pair pitch); the four lanes of a
+// row then read one half of a 128-byte block whose other half the next
+// four lanes read for the row's partner, so a wave-load is 8 whole lines.
+template <class C, int SH = 1, bool APAIR = false>
 __device__ __forceinline__ void v3_offsets(int* voff, int row0, int col0, int R, int Cc, int64_t lda,
                                            int64_t ldb, int wave, int lane) {
 #pragma unroll
@@ -189,7 +199,10 @@ __device__ __forceinline__ void v3_offsets(int* voff, int row0, int col0, int R,
         int gr = (isA ? row0 : col0) + rr;
         const int lim = isA ? R : Cc;
         gr = gr < lim ? gr : lim - 1;
-        voff[j] = (int)(((unsigned)gr * (unsigned)(isA ? lda : ldb) + (unsigned)(lc * 8)) * 2u);
+        if (APAIR && isA)
+            voff[j] = (int)(((unsigned)(gr >> 1) * (unsigned)lda + (unsigned)((gr & 1) * 32 + lc * 8)) * 2u);
+        else
+            voff[j] = (int)(((unsigned)gr * (unsigned)(isA ? lda : ldb) + (unsigned)(lc * 8)) * 2u);
     }
 }
 
