@@ -588,6 +588,59 @@ def test_prefill_layer_shapes(E, shape):
         assert torch.equal(E.espace_projected_linear(X, Pt, Wf, workspace=ws), Y), fill
 
 
+# (K, M, L, N) of prefill layers that keep Z in the row-pair layout (an odd
+# token count, whose last pair has one token; a component count that is not a
+# multiple of 64, or of 8, with the expand GEMM's masked depth tail on row
+# pairs; the projection on the 128 x 192 tile and, at depth 11008, on the
+# four-wave 256 x 192 tile in two depth halves; a projection depth tail)
+ROW_PAIR_SHAPES = [(4096, 12288, 1536, 4095), (4096, 6000, 1500, 4095), (4100, 12288, 1300, 4095),
+                   (11008, 4096, 1536, 4095)]
+
+
+def _row_pairs(Z, ldp):
+    """Z [N][L] (float32 values of bf16 entries) in the row-pair layout with
+    pair pitch ldp: element (n, l) at (n // 2) * ldp + (l // 32) * 64 +
+    (n % 2) * 32 + l % 32; the unused places are left at zero."""
+    N, L = Z.shape
+    out = np.zeros(((N + 1) // 2) * ldp, dtype=np.float32)
+    n = np.arange(N)[:, None]
+    l = np.arange(L)[None, :]
+    out[(n // 2) * ldp + (l // 32) * 64 + (n % 2) * 32 + l % 32] = Z
+    return out
+
+
+@pytest.mark.parametrize("shape", ROW_PAIR_SHAPES, ids=lambda s: "K%d_M%d_L%d_N%d" % s)
+def test_prefill_layer_row_pair_z(E, shape):
+    """The prefill layer keeps Z in its workspace in row pairs (two tokens' 32
+    consecutive components per 128-byte block): the workspace's Z region holds
+    exactly the projection's Z in that layout, the layer's result equals the
+    projection followed by the expansion on a plain Z bitwise (the layout moves
+    no arithmetic), and it is within the oracle's bounds on every output."""
+    dev = need_gpu()
+    K, M, L, N = shape
+    inp = _inputs(K, M, L, N, "bf16", seed=85)
+    X, Pt, W = _dev_inputs(inp, dev)
+    Wf = E.espace_fold_weights(W, Pt)
+    need = E.espace_workspace_bytes(E.OP_PROJECTED_LINEAR, M, K, L, N, torch.bfloat16)
+    ws = torch.zeros(need, dtype=torch.uint8, device=dev)
+    Y = E.espace_projected_linear(X, Pt, Wf, out_mat(N, M, "bf16", dev), ws)
+    Z = E.espace_project(Pt, X)
+    Ye = E.espace_expand(Z, Wf)
+    torch.cuda.synchronize()
+    ldp = 2 * ((L + 63) // 64 * 64)
+    pairs = _row_pairs(Z.float().cpu().numpy(), ldp)
+    got = ws[:pairs.size * 2].view(torch.bfloat16).float().cpu().numpy()
+    keep = np.zeros(pairs.size, dtype=bool)
+    n = np.arange(N)[:, None]
+    l = np.arange(L)[None, :]
+    keep[(n // 2) * ldp + (l // 32) * 64 + (n % 2) * 32 + l % 32] = True
+    assert np.array_equal(got[keep], pairs[keep]), "workspace Z is not the projection in row pairs"
+    assert torch.equal(Y, Ye), "layer != project then expand"
+    Y64, B = _layer_ref(inp)
+    parity.check(host64(Y), Y64, B, TOL["bf16"], "prefill layer, Z in row pairs")
+    assert np.isnan(padding(Y)).all()
+
+
 # (K, M, L, N) of decode layers on the whole-row kernels: one and two tokens,
 # Wf rows of one to eight 512-element passes, projection depths with a
 # partial block of passes
