@@ -189,6 +189,8 @@ def kernel_probe(E, dev, stream, args, Xr, Pr, Wfr, Ws, Y, ws, Z, wsz, wse, R):
       layer_N{n}, dense_N{n}   - the Llama2-7B FFN up+gate layer and its dense
                                  layer at decode token counts n = 1, 8, 16
       mx_project, mx_expand    - the MX-FP8 products of the QKV layer
+      layer                    - the QKV layer itself (its expand GEMM reads Z
+                                 in the workspace's row-pair layout)
     Every phase rotates its weights over copies larger than the last-level
     cache.  Prints the phase list as JSON."""
     import torch
@@ -250,6 +252,9 @@ def kernel_probe(E, dev, stream, args, Xr, Pr, Wfr, Ws, Y, ws, Z, wsz, wse, R):
     torch.cuda.synchronize()
     phase("mx_project", lambda i: E.espace_project_mxfp8(Pq[i], Xq[i], Zq), R)
     phase("mx_expand", lambda i: E.espace_expand_mxfp8(Zq, Wq[i], Y), R)
+    torch.cuda.synchronize()
+    del Xq, Pq, Wq, Zq
+    phase("layer", lambda i: E.espace_projected_linear(Xr[i], Pr[i], Wfr[i], Y, ws), R)
     torch.cuda.synchronize()
     print(json.dumps({"kernel_probe": phases, "launches_per_phase": S, "copy_probe_bytes": COPY_PROBE_BYTES,
                       "qkv": {"K": 4096, "M": 12288, "L": 1536, "N": 4096},

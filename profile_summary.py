@@ -28,7 +28,7 @@ import os
 import sys
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
-EXPAND_KERNEL = "gemm_tn_bf16_v3_kernel<0, 256>"   # the four-wave 256x256 kernel, bf16 output
+EXPAND_KERNEL = "gemm_tn_bf16_v3_kernel<0, 256, 0>"   # the four-wave 256x256 kernel, bf16 output, plain A
 PROJECT_KERNEL = "gemm_tn_bf16_v2_kernel<128, 192"   # the projection's 128x192 tile
 EXPAND_GRID = 256 * 256                        # one workgroup of 256 threads per CU
 COPY_KERNELS = ("AUnaryFunctor<c10::BFloat16", "MulFunctor")   # torch.mul(bf16, 1.0)
@@ -91,8 +91,10 @@ def stats(args):
            ("expand, back-to-back loop (the roofline kernel)", own[pe + 2:pe + 2 + S]),
            ("dense baseline", own[pe + 2 + S + W:pe + 2 + 2 * S + W])]
     lines += ["", "The projection (128x192 tiles) and the 256x256 kernel (one workgroup per CU, 768 "
-              "tiles; it serves both the expand GEMM, depth L=1536, and the dense baseline, depth "
-              "K=4096), split by position in bench.py's launch order (timed launches only):", "",
+              "tiles: inside the layer the expand GEMM, depth L=1536, on Z in the workspace's row-pair "
+              "layout, `<0, 256, 1>`; the back-to-back expand GEMM on a plain Z and the dense baseline, "
+              "depth K=4096, `<0, 256, 0>`), split by position in bench.py's launch order (timed "
+              "launches only):", "",
               "| launches | count | average (us) | median (us) |", "|---|---|---|---|"]
     for name, rs in seg:
         d = sorted(_dur_us(r) for r in rs)
@@ -119,7 +121,7 @@ def stats(args):
 MARKER = "spin_kernel"           # torch.cuda._sleep, around each of the probe's phases
 # the phases of bench.py --kernel-probe, in launch order
 PROBE_PHASES = ["project", "expand", "dense", "layer_N1", "dense_N1", "layer_N8", "dense_N8",
-                "layer_N16", "dense_N16", "mx_project", "mx_expand"]
+                "layer_N16", "dense_N16", "mx_project", "mx_expand", "layer"]
 
 
 def _dispatches(path):
@@ -200,6 +202,9 @@ def _alg(phase, probe):
         return acc.gemm_flops(q["N"], q["M"], q["L"]), acc.gemm_bytes(q["N"], q["M"], q["L"])
     if phase == "dense":
         return acc.gemm_flops(q["N"], q["M"], q["K"]), acc.gemm_bytes(q["N"], q["M"], q["K"])
+    if phase == "layer":
+        return (acc.projected_flops(q["K"], q["M"], q["L"], q["N"]),
+                acc.projected_bytes(q["K"], q["M"], q["L"], q["N"]))
     n = int(phase.split("_N")[1])
     if phase.startswith("layer"):
         return acc.projected_flops(d["K"], d["M"], d["L"], n), acc.projected_bytes(d["K"], d["M"], d["L"], n)
@@ -245,7 +250,8 @@ def counters(args):
     for (ph, k, grid), ent in table.items():
         mean = {c: sum(v) / len(v) for c, v in ent.items()}
         n = max(len(v) for v in ent.values())
-        fl, by = _alg(ph, probe)
+        # a kernel of the layer phase against its own product
+        fl, by = _alg(("project" if "v2_kernel" in k else "expand") if ph == "layer" else ph, probe)
         busy = f"{mean['MfmaUtil']:.1f}" if "MfmaUtil" in mean else ""
         mo = [mean[c] for c in ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_VALU_MFMA_MOPS_F8") if c in mean]
         mops = f"{sum(mo) * 512 / fl:.3f}" if mo else ""
@@ -271,11 +277,17 @@ def counters(args):
 
 
 # operand bytes the tiles of a tiled GEMM read from L2 per launch: tiles x
-# (tile rows + tile columns) x depth x element bytes
+# (tile rows + tile columns) x depth x element bytes; per phase, by kernel
+# (the layer phase runs the projection, then the expand GEMM on Z in row pairs)
+_PROJ = ("4096 x 1536, depth 4096, 128 x 192 tiles", 32 * 8 * (128 + 192) * 4096 * 2)
+_EXP = ("4096 x 12288, depth 1536, 256 x 256 tiles", 16 * 48 * 512 * 1536 * 2)
 LOADPATH_PHASES = {
-    "project": ("4096 x 1536, depth 4096, 128 x 192 tiles", 32 * 8 * (128 + 192) * 4096 * 2),
-    "expand": ("4096 x 12288, depth 1536, 256 x 256 tiles", 16 * 48 * 512 * 1536 * 2),
-    "dense": ("4096 x 12288, depth 4096, 256 x 256 tiles", 16 * 48 * 512 * 4096 * 2),
+    "project": {"gemm_tn_bf16_v2_kernel<128, 192": _PROJ},
+    "expand": {"gemm_tn_bf16_v3_kernel<0, 256, 0>": _EXP},
+    "dense": {"gemm_tn_bf16_v3_kernel<0, 256, 0>": ("4096 x 12288, depth 4096, 256 x 256 tiles",
+                                                    16 * 48 * 512 * 4096 * 2)},
+    "layer": {"gemm_tn_bf16_v2_kernel<128, 192": _PROJ,
+              "gemm_tn_bf16_v3_kernel<0, 256, 1>": ("expand, Z in row pairs: " + _EXP[0], _EXP[1])},
 }
 
 
@@ -285,23 +297,22 @@ def loadpath(args):
     channel (16 per XCD, 128); GRBM_GUI_ACTIVE sums the 8 XCDs' active
     cycles, so one unit's share of the kernel's cycles is counter /
     (GRBM_GUI_ACTIVE / 8 x units)."""
-    table = collections.defaultdict(lambda: collections.defaultdict(list))
+    table = collections.defaultdict(lambda: collections.defaultdict(list))   # (phase, kernel key) -> counters
     kname = {}
     for path, _ in args.run:
         ds = _dispatches(path)
         for ph, rows in _phases(ds, PROBE_PHASES).items():
-            if ph not in LOADPATH_PHASES:
-                continue
             for d in rows:
-                if "gemm_tn" not in d["name"]:
-                    continue
-                kname[ph] = _short(d["name"])
-                for c, v in d["c"].items():
-                    table[ph][c].append(v)
+                for key in LOADPATH_PHASES.get(ph, {}):
+                    if key in d["name"]:
+                        kname[(ph, key)] = _short(d["name"])
+                        for c, v in d["c"].items():
+                            table[(ph, key)][c].append(v)
     lines = ["# Load-path counters of the tiled GEMMs: Llama2-7B fused QKV (K=4096, M=12288, L=1536, N=4096)", "",
-             "The projection, the expand GEMM and the dense baseline of `bench.py --kernel-probe` (bf16, "
-             "weights rotated over copies larger than the last-level cache).  Counter runs (from the "
-             "repository root, on one MI355X):", "", "```"]
+             "The projection, the expand GEMM (on a plain Z) and the dense baseline of `bench.py "
+             "--kernel-probe`, and the layer's own two kernels (its expand GEMM reads Z in the workspace's "
+             "row-pair layout); bf16, weights rotated over copies larger than the last-level cache.  Counter "
+             "runs (from the repository root, on one MI355X):", "", "```"]
     lines += [cmd for _, cmd in args.run] + ["```", ""]
     lines += ["Per launch.  Unit shares: counter / (GRBM_GUI_ACTIVE / 8 x units), units = 256 (TA, TD, "
               "TCP: one per CU) or 128 (TCC: one per L2 channel).  TA busy: the address unit; TA stalled: "
@@ -313,26 +324,27 @@ def loadpath(args):
               "| phase | kernel | shape | MFMA busy % | waitcnt % | TA busy % | TA stalled % | TD busy % | "
               "TD stalled % | TCP pending % | L2 busy % | L2 hit % | L2 requests (M) | operand B / request |",
               "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
-    for ph, (shape, opb) in LOADPATH_PHASES.items():
-        if ph not in table:
-            continue
-        m = {c: sum(v) / len(v) for c, v in table[ph].items()}
-        cyc = m.get("GRBM_GUI_ACTIVE", 0.0) / 8.0
+    for ph, kernels in LOADPATH_PHASES.items():
+        for key, (shape, opb) in kernels.items():
+            if (ph, key) not in table:
+                continue
+            m = {c: sum(v) / len(v) for c, v in table[(ph, key)].items()}
+            cyc = m.get("GRBM_GUI_ACTIVE", 0.0) / 8.0
 
-        def share(c, units):
-            return f"{100.0 * m[c] / (cyc * units):.0f}" if c in m and cyc else ""
+            def share(c, units):
+                return f"{100.0 * m[c] / (cyc * units):.0f}" if c in m and cyc else ""
 
-        busy = f"{100.0 * m['SQ_VALU_MFMA_BUSY_CYCLES'] / (cyc * 1024):.0f}" \
-            if "SQ_VALU_MFMA_BUSY_CYCLES" in m and cyc else ""
-        wait = f"{100.0 * m['SQ_WAIT_INST_ANY'] / m['SQ_WAVE_CYCLES']:.0f}" \
-            if "SQ_WAIT_INST_ANY" in m and m.get("SQ_WAVE_CYCLES") else ""
-        req = m.get("TCC_HIT", 0.0) + m.get("TCC_MISS", 0.0)
-        hit = f"{100.0 * m['TCC_HIT'] / req:.0f}" if req else ""
-        lines.append(f"| {ph} | `{kname[ph]}` | {shape} | {busy} | {wait} | {share('TA_TA_BUSY', 256)} | "
-                     f"{share('TA_ADDR_STALLED_BY_TC_CYCLES', 256)} | {share('TD_TD_BUSY', 256)} | "
-                     f"{share('TD_TC_STALL', 256)} | {share('TCP_PENDING_STALL_CYCLES', 256)} | "
-                     f"{share('TCC_BUSY', 128)} | {hit} | {req / 1e6:.2f} | "
-                     f"{opb / req:.0f} |" if req else "")
+            busy = f"{100.0 * m['SQ_VALU_MFMA_BUSY_CYCLES'] / (cyc * 1024):.0f}" \
+                if "SQ_VALU_MFMA_BUSY_CYCLES" in m and cyc else ""
+            wait = f"{100.0 * m['SQ_WAIT_INST_ANY'] / m['SQ_WAVE_CYCLES']:.0f}" \
+                if "SQ_WAIT_INST_ANY" in m and m.get("SQ_WAVE_CYCLES") else ""
+            req = m.get("TCC_HIT", 0.0) + m.get("TCC_MISS", 0.0)
+            hit = f"{100.0 * m['TCC_HIT'] / req:.0f}" if req else ""
+            lines.append(f"| {ph} | `{kname[(ph, key)]}` | {shape} | {busy} | {wait} | {share('TA_TA_BUSY', 256)} | "
+                         f"{share('TA_ADDR_STALLED_BY_TC_CYCLES', 256)} | {share('TD_TD_BUSY', 256)} | "
+                         f"{share('TD_TC_STALL', 256)} | {share('TCP_PENDING_STALL_CYCLES', 256)} | "
+                         f"{share('TCC_BUSY', 128)} | {hit} | {req / 1e6:.2f} | "
+                         f"{opb / req:.0f} |" if req else "")
     open(args.out, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
