@@ -416,11 +416,13 @@ size_t ws_bytes(espace_op op, int64_t M, int64_t K, int64_t L, int64_t N, espace
 // Columns of an MX-FP8 matrix as stored: whole 128-column steps of the MFMA.
 int64_t mx_cols(int64_t cols) { return (cols + 127) / 128 * 128; }
 
-// Workspace of the MX-FP8 layer: Z's codes [N][mx_cols(L)] and scale bytes
-// [N][mx_cols(L) / 32].
+// Workspace of the MX-FP8 layer: Z's codes in row pairs (round_up(N, 2) / 2
+// pairs of 2 mx_cols(L) bytes: each 128-byte block holds 64 consecutive codes
+// of two neighbouring tokens, so the expansion's 64-byte half-rows of Z are
+// read as whole cache lines) and its scale bytes [N][mx_cols(L) / 32].
 size_t mx_ws_bytes(int64_t M, int64_t L, int64_t N) {
     if (!N || !M) return 0;
-    return align_ws((size_t)N * mx_cols(L)) + align_ws((size_t)N * mx_cols(L) / 32);
+    return align_ws((size_t)round_up(N, 2) * mx_cols(L)) + align_ws((size_t)N * mx_cols(L) / 32);
 }
 
 
@@ -681,10 +683,13 @@ espace_status noalloc_scratch(void** out) {
 }  // namespace
 
 // The MX-FP8 products after validation.
+// z_pairs: Z's codes in row pairs (ldzq bytes per pair)
 espace_status mx_project_launch(const void* Ptq, int64_t ldpq, const void* Pts, int64_t ldps, const void* Xq,
                                 int64_t ldxq, const void* Xs, int64_t ldxs, void* Zq, int64_t ldzq, void* Zs,
-                                int64_t ldzs, int64_t K, int64_t L, int64_t N, hipStream_t stream) {
+                                int64_t ldzs, int64_t K, int64_t L, int64_t N, hipStream_t stream,
+                                int z_pairs = 0) {
     espace::MxGemmArgs a{};
+    a.out_pairs = z_pairs;
     a.T = (const uint8_t*)Xq; a.ldt = ldxq; a.Ts = (const uint8_t*)Xs; a.ldts = ldxs;
     a.W = (const uint8_t*)Ptq; a.ldw = ldpq; a.Ws = (const uint8_t*)Pts; a.ldws = ldps;
     a.out = Zq; a.ldo = ldzq; a.outs = (uint8_t*)Zs; a.ldos = ldzs;
@@ -696,8 +701,9 @@ espace_status mx_project_launch(const void* Ptq, int64_t ldpq, const void* Pts, 
 
 espace_status mx_expand_launch(const void* Zq, int64_t ldzq, const void* Zs, int64_t ldzs, const void* Wfq,
                                int64_t ldwq, const void* Wfs, int64_t ldws, void* Y, int64_t ldy, int64_t M,
-                               int64_t L, int64_t N, hipStream_t stream) {
+                               int64_t L, int64_t N, hipStream_t stream, int z_pairs = 0) {
     espace::MxGemmArgs a{};
+    a.t_pairs = z_pairs;
     a.T = (const uint8_t*)Zq; a.ldt = ldzq; a.Ts = (const uint8_t*)Zs; a.ldts = ldzs;
     a.W = (const uint8_t*)Wfq; a.ldw = ldwq; a.Ws = (const uint8_t*)Wfs; a.ldws = ldws;
     a.out = Y; a.ldo = ldy;
@@ -1170,11 +1176,12 @@ espace_status espace_projected_linear_mxfp8(const void* Xq, int64_t ldxq, const 
     ESPACE_TRY(check_alias(mat_range("Y", Y, N, ldy, ESPACE_BF16), ins, 7));
     ESPACE_TRY(check_alias(ins[6], ins, 6));
     ESPACE_TRY(check_device());
-    const int64_t ldzq = mx_cols(L), ldzs = mx_cols(L) / 32;
+    // Z's codes in row pairs (2 mx_cols(L) bytes per pair), then its scales
+    const int64_t ldzq = 2 * mx_cols(L), ldzs = mx_cols(L) / 32;
     unsigned char* Zq = static_cast<unsigned char*>(workspace);
-    unsigned char* Zs = Zq + align_ws((size_t)N * ldzq);
-    ESPACE_TRY(mx_project_launch(Ptq, ldpq, Pts, ldps, Xq, ldxq, Xs, ldxs, Zq, ldzq, Zs, ldzs, K, L, N, stream));
-    ESPACE_TRY(mx_expand_launch(Zq, ldzq, Zs, ldzs, Wfq, ldwq, Wfs, ldws, Y, ldy, M, L, N, stream));
+    unsigned char* Zs = Zq + align_ws((size_t)round_up(N, 2) * mx_cols(L));
+    ESPACE_TRY(mx_project_launch(Ptq, ldpq, Pts, ldps, Xq, ldxq, Xs, ldxs, Zq, ldzq, Zs, ldzs, K, L, N, stream, 1));
+    ESPACE_TRY(mx_expand_launch(Zq, ldzq, Zs, ldzs, Wfq, ldwq, Wfs, ldws, Y, ldy, M, L, N, stream, 1));
     return ok();
 }
 

@@ -319,7 +319,10 @@ void gemm_mx_z_kernel(MxGemmArgs a) {
                 const int sb = mx_scale_byte(amax);
                 const int nsh = 127 - sb;                    // multiply by 2^-S
                 if (n < a.R && cb < a.cpad) {
-                    uint8_t* p = Zq + (int64_t)n * a.ldo + cb + 4 * q;
+                    // row pairs: columns cb .. cb + 31 lie in one 64-code block
+                    const int c = cb + 4 * q;
+                    uint8_t* p = Zq + (a.out_pairs ? (int64_t)(n >> 1) * a.ldo + (c >> 6) * 128 + (n & 1) * 64 + (c & 63)
+                                                   : (int64_t)n * a.ldo + c);
                     *reinterpret_cast<uint32_t*>(p) =
                         mx_pack4(__builtin_amdgcn_ldexpf(v[0], nsh), __builtin_amdgcn_ldexpf(v[1], nsh),
                                  __builtin_amdgcn_ldexpf(v[2], nsh), __builtin_amdgcn_ldexpf(v[3], nsh));
@@ -405,7 +408,9 @@ __device__ __forceinline__ void mx_read_scale(int x, int* tsr, int* wsr, const M
 // What a sub-step's loads need: the code operands as 16-bit arrays (the
 // bf16 kernel's load helpers; one step of 128 codes is 64 of their
 // elements), the scale arrays, and this lane's per-load row offsets.
-template <int BW, int SS>
+// APAIR: the token codes in row pairs (each 128-byte block holds 64
+// consecutive codes of two neighbouring tokens).
+template <int BW, int SS, bool APAIR = false>
 struct MxLoad {
     using C = MxCfg<BW, SS>;
     const uint16_t* T;
@@ -436,7 +441,7 @@ struct MxLoad {
     // zeros past the buffer.
     __device__ __forceinline__ void load(unsigned char* smem, int kt, int h, int u, int y, int area) const {
         if (y < C::V::LPH) {
-            v3_load<typename C::V>(smem, T, W, tbytes, wbytes, voff, wave, kt, h, u, y);
+            v3_load<typename C::V, APAIR>(smem, T, W, tbytes, wbytes, voff, wave, kt, h, u, y);
         } else if (C::scales_with(kt)) {
             const int j = y - C::V::LPH;
             const int s = (wave + 4 * j) % C::NSC;
@@ -458,11 +463,11 @@ struct MxLoad {
 // sd into tsr / wsr, and with do_load the loads of half h of step lkt into
 // half-stage u (h = SEL1: LPH0 loads in sub-step 0, LPH1 in sub-step 1).
 // FIRST: the accumulators start from zero.
-template <int BW, int SS, bool FIRST, bool SEL1, bool SREADS>
+template <int BW, int SS, bool FIRST, bool SEL1, bool SREADS, class LD>
 __device__ __forceinline__ void mx_substep(f32x16_t (&acc)[4][BW / 64], const MxFrag<BW / 64>& cur,
                                            const int* tsc, const int* wsc, MxFrag<BW / 64>& nxt,
                                            const MxAddr& rd, const MxAddr& sd, int* tsr, int* wsr,
-                                           unsigned char* smem, const MxLoad<BW, SS>& ld, int lkt, int h, int u,
+                                           unsigned char* smem, const LD& ld, int lkt, int h, int u,
                                            int area, bool do_load) {
     using C = MxCfg<BW, SS>;
     constexpr int NJ = C::NJ;
@@ -535,7 +540,7 @@ __device__ __forceinline__ f32x16_t mx_acc_read(const f32x16_t& a) {
 // with every fourth step, into two areas taken in turn by the workgroup's
 // successive groups of four steps (tile after tile), so that a group's area
 // is rewritten only after its last step's scales were read.
-template <int BW, int SS>
+template <int BW, int SS, int APAIR = 0>
 __global__ __launch_bounds__(256, 1)
 void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
     using C = MxCfg<BW, SS>;
@@ -550,10 +555,10 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
     const int wcol0 = (wave & 1) * (BW / 2);          // its output columns
     const bool ahead_ok = (a.C & 7) == 0 && ktiles >= 2;
 
-    MxLoad<BW, SS> ld;
+    MxLoad<BW, SS, APAIR != 0> ld;
     ld.T = reinterpret_cast<const uint16_t*>(a.T);
     ld.W = reinterpret_cast<const uint16_t*>(a.W);
-    ld.tbytes = (unsigned)((uint64_t)a.R * a.ldt);
+    ld.tbytes = (unsigned)((uint64_t)(APAIR ? (a.R + 1) / 2 : a.R) * a.ldt);
     ld.wbytes = (unsigned)((uint64_t)a.C * a.ldw);
     ld.Ts = a.Ts;
     ld.Ws = a.Ws;
@@ -635,7 +640,7 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
         } else {
             // the half-stages may still be read by a wave finishing the previous tile
             if (item != (int)blockIdx.x) __syncthreads();
-            v3_offsets<V, 2>(ld.voff, row0, col0, a.R, a.C, a.ldt / 2, a.ldw / 2, wave, lane);
+            v3_offsets<V, 2, APAIR != 0>(ld.voff, row0, col0, a.R, a.C, a.ldt / 2, a.ldw / 2, wave, lane);
             ld.scale_offsets(a, row0, col0, lane);
 #pragma unroll
             for (int y = 0; y < C::LPH0; ++y) ld.load(smem, 0, 0, hs(0, 0), y, gb & 1);
@@ -676,7 +681,7 @@ void gemm_mx_kernel(MxGemmArgs a, int tiles_c, int ntiles) {
             larea = (gb_next + (lkt >> 2)) & 1;
             if (!ahead_next) return false;
             if (kt + 2 == ktiles && h == 0) {
-                v3_offsets<V, 2>(ld.voff, ntr * V3_BM, ntc * BW, a.R, a.C, a.ldt / 2, a.ldw / 2, wave, lane);
+                v3_offsets<V, 2, APAIR != 0>(ld.voff, ntr * V3_BM, ntc * BW, a.R, a.C, a.ldt / 2, a.ldw / 2, wave, lane);
                 ld.scale_offsets(a, ntr * V3_BM, ntc * BW, lane);
             }
             return true;
@@ -884,10 +889,17 @@ hipError_t launch_pipelined(const MxGemmArgs& a, int cus, hipStream_t stream) {
     const int ntiles = tiles_c * ((a.R + 255) / 256);
     const int grid = ntiles < cus ? ntiles : cus;
     // four steps' scales per 16-byte load where every scale row starts on 16 bytes
-    if (scale_rows_16(a))
-        hipLaunchKernelGGL((gemm_mx_kernel<BW, 4>), dim3(grid), dim3(256), 0, stream, a, tiles_c, ntiles);
-    else
-        hipLaunchKernelGGL((gemm_mx_kernel<BW, 1>), dim3(grid), dim3(256), 0, stream, a, tiles_c, ntiles);
+    if (scale_rows_16(a)) {
+        if (a.t_pairs)
+            hipLaunchKernelGGL((gemm_mx_kernel<BW, 4, 1>), dim3(grid), dim3(256), 0, stream, a, tiles_c, ntiles);
+        else
+            hipLaunchKernelGGL((gemm_mx_kernel<BW, 4>), dim3(grid), dim3(256), 0, stream, a, tiles_c, ntiles);
+    } else {
+        if (a.t_pairs)
+            hipLaunchKernelGGL((gemm_mx_kernel<BW, 1, 1>), dim3(grid), dim3(256), 0, stream, a, tiles_c, ntiles);
+        else
+            hipLaunchKernelGGL((gemm_mx_kernel<BW, 1>), dim3(grid), dim3(256), 0, stream, a, tiles_c, ntiles);
+    }
     return hipGetLastError();
 }
 
@@ -927,6 +939,10 @@ hipError_t launch_gemm_mx(const MxGemmArgs& a, int out_mx, int cus, hipStream_t 
         a.C * a.ldws >= lim || a.ldt % 16 || a.ldw % 16 || a.ldts % 4 || a.ldws % 4 ||
         (!out_mx && (int64_t)a.R * a.ldo * 2 >= lim))
         return hipErrorInvalidValue;
+    // row pairs: token codes read by the expansion, codes written by the
+    // projection; pair pitches of whole 128-byte blocks
+    if ((a.t_pairs && (out_mx || a.ldt % 128)) || (a.out_pairs && (!out_mx || a.ldo % 128)))
+        return hipErrorNotSupported;
     const int tile = mx_gemm_tile(a.R, a.C, cus, out_mx);
     if (out_mx) {
         switch (tile) {

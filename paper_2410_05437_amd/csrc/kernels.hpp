@@ -141,6 +141,11 @@ struct MxGemmArgs {
     uint8_t* outs;     int64_t ldos;    // MX-FP8 output: scale bytes [R][ldos]
     int R, C, D;
     int cpad;                           // MX-FP8 output: columns written, round_up(C, 128)
+    // Row pairs (the MX-FP8 layer's Z in its workspace): code (r, c) at
+    // (r / 2) * ld + (c / 64) * 128 + (r % 2) * 64 + c % 64, ld (bytes per
+    // row pair) a multiple of 128; the scale bytes stay one row per token.
+    int t_pairs = 0;                    // the token codes T (bf16 output only)
+    int out_pairs = 0;                  // the MX-FP8 output codes
 };
 // Tile of the MX GEMM for R x C outputs (0: 256 x 256, 1: 256 x 128, 2: 128 x 128;
 // 2 only for MX-FP8 output).
