@@ -131,6 +131,67 @@ def time_each(fn, n_args, steps, stream):
     return float(np.mean([a.elapsed_time(b) for a, b in evs]))
 
 
+def layer_percentiles(fn, n_args, calls, stream):
+    """p10, median and p90 (us) of `calls` single calls, each bracketed by its
+    own pair of events on the launch stream."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(calls)]
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(evs):
+        a.record(stream)
+        fn(i % n_args)
+        b.record(stream)
+    torch.cuda.synchronize()
+    d = np.sort([a.elapsed_time(b) * 1e3 for a, b in evs])
+    return [round(float(np.percentile(d, q)), 2) for q in (10, 50, 90)]
+
+
+def clock_under_load(fn, n_args, seconds):
+    """Median and range of the gfx clock (MHz, mean over the XCDs) that
+    `amd-smi metric -c` reports while `fn` runs back to back for `seconds`;
+    None where amd-smi is missing or lists more than this one GPU."""
+    import shutil
+    import subprocess
+    import threading
+    import torch
+    exe = shutil.which("amd-smi")
+    if not exe:
+        return None
+    samples, gpus = [], []
+    stop = threading.Event()
+
+    def sample():
+        while not stop.is_set():
+            try:
+                out = subprocess.run([exe, "metric", "-c", "--json"], capture_output=True, text=True,
+                                     timeout=10).stdout
+                data = json.loads(out)
+                data = data.get("gpu_data", data) if isinstance(data, dict) else data
+                gpus.append(len(data))
+                clk = [v["clk"]["value"] for k, v in data[0]["clock"].items()
+                       if k.startswith("gfx_") and isinstance(v, dict) and isinstance(v.get("clk"), dict)]
+                if clk:
+                    samples.append(sum(clk) / len(clk))
+            except Exception:
+                return
+
+    th = threading.Thread(target=sample, daemon=True)
+    th.start()
+    t0 = time.time()
+    i = 0
+    while time.time() - t0 < seconds:
+        for _ in range(20):
+            fn(i % n_args)
+            i += 1
+        torch.cuda.synchronize()
+    stop.set()
+    th.join(timeout=15)
+    if not samples or max(gpus) != 1:
+        return None
+    return {"median": round(float(np.median(samples)), 0), "min": round(min(samples), 0),
+            "max": round(max(samples), 0), "samples": len(samples)}
+
+
 def copy_probe(dev):
     """One elementwise copy of COPY_PROBE_BYTES (read that many bytes, write
     that many): the reference the traffic counters are scaled by."""
@@ -403,10 +464,17 @@ def main():
     ms_fold = time_calls(lambda i: E.espace_fold_weights(Ws, Pts, Wf_tmp, wsf), 1,
                          max(5, args.steps // 5), 2, stream)
 
+    # spread of single layer calls (each between its own two events, after
+    # the clocks are up) and the gfx clock while the layer runs
+    pct = layer_percentiles(step, R, 50, stream)
+    clk = clock_under_load(step, R, 1.0)
+
     # parity of the benchmarked output on sampled entries (oracle not needed:
     # the parity tests cover this launch configuration against the oracle)
     detail = {
         "us_per_layer": round(ms * 1e3, 2),
+        "layer_us_p10_median_p90": pct,
+        "gfx_clock_mhz_under_load": clk,
         "cold_us_per_layer": round(ms_cold * 1e3, 2),
         "clock_warmup_s": args.clock_warmup,
         "dense_us": round(ms_dense * 1e3, 2),
