@@ -538,7 +538,13 @@ def main():
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic if dom == "expand" else None,
                      "layer_achieved": round(tflops, 1),
-                     "layer_frac": round(tflops / PEAK_BF16_TFLOPS, 4)},
+                     "layer_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                     # the expand GEMM as it runs inside the layer (on Z in the
+                     # workspace's row-pair layout, which no public call takes):
+                     # the layer's time less the projection's, both timed above
+                     "expand_in_layer_us_derived": round((ms - ms_proj) * 1e3, 2),
+                     "expand_in_layer_frac_derived": round(
+                         kern["expand"]["flops"] / ((ms - ms_proj) * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)},
         "cpu_baseline": cpu,
         "detail": detail,
     }
