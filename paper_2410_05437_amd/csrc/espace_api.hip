@@ -585,7 +585,7 @@ espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, voi
         g.a_pairs = a_pairs;
         g.c_pairs = c_pairs;
         if (p.pair) g.epoch = next_epoch();
-        if ((a_pairs || c_pairs) && (p.kind != KIND_TILED || p.rows1 > 0))
+        if ((a_pairs || c_pairs) && p.kind != KIND_TILED)
             return fail(ESPACE_ERR_HIP, "row-pair layout on a plan that does not take it");
         if (p.kind == KIND_TILED && p.rows1 > 0) {
             // rows [0, rows1), then the rest with its own tile plan (and its
@@ -593,8 +593,9 @@ espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, voi
             g.R = p.rows1;
             e = launch_tiled(g, stream);
             if (e == hipSuccess) {
-                g.A = (const uint16_t*)A + (int64_t)p.rows1 * lda;
-                g.C = (uint16_t*)C + (int64_t)p.rows1 * ldc;
+                // rows1 is a multiple of 256: row pairs start on a pair
+                g.A = (const uint16_t*)A + (int64_t)(a_pairs ? p.rows1 / 2 : p.rows1) * lda;
+                g.C = (uint16_t*)C + (int64_t)(c_pairs ? p.rows1 / 2 : p.rows1) * ldc;
                 g.R = (int)(R - p.rows1);
                 g.tile = p.tile2;
                 g.splits = p.splits2;
@@ -621,17 +622,20 @@ espace_status run_tn(const void* A, int64_t lda, const void* B, int64_t ldb, voi
 // 64-byte half-rows of Z arrive as whole lines, half the L2 requests for
 // that operand (the load path of the CUs bounds these GEMMs; in a probe of
 // the expand's operand stream with the fragment reads, 121 -> 114 µs).
-// Taken for prefill when the projection is one tiled launch whose kernel
-// writes bf16 itself (one depth range or the pair combine) and the expand
-// GEMM is one single-range launch of the four-wave kernel.
+// Taken for prefill when the projection is tiled (any depth split; its
+// output is written by the GEMM kernel, the pair combine or the reduction
+// pass) and every launch of the expand GEMM is a single-range launch of the
+// four-wave kernel.
 bool z_pairs(int64_t N, int64_t L, int64_t K, int64_t M, int64_t ldx, int64_t ldp, int64_t ldwf, int64_t ldy,
              espace_dtype dt) {
     if (dt != ESPACE_BF16 || N <= 32) return false;
     const Plan a = plan_tn(N, L, K, dt);
     const Plan b = plan_tn(N, M, L, dt);
-    if (a.kind != KIND_TILED || a.rows1 > 0 || (a.splits > 1 && !(a.pair && a.splits == 2))) return false;
-    if (b.kind != KIND_TILED || b.rows1 > 0 || b.splits != 1) return false;
-    if (b.tile != espace::TILE_256x256_W8T && b.tile != espace::TILE_256x192_W8) return false;
+    auto v3_single = [](int tile, int splits) {
+        return splits == 1 && (tile == espace::TILE_256x256_W8T || tile == espace::TILE_256x192_W8);
+    };
+    if (a.kind != KIND_TILED || b.kind != KIND_TILED) return false;
+    if (!v3_single(b.tile, b.splits) || (b.rows1 > 0 && !v3_single(b.tile2, b.splits2))) return false;
     // the kernels' 32-bit offsets (the register-staged fallback keeps plain layouts)
     const int64_t lim = (int64_t)1 << 31;
     const int64_t ldzp = 2 * z_ld(L, N, dt);

@@ -206,7 +206,8 @@ void gemm_tn_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda,
     }
 }
 
-// Sum of S fp32 partial results -> bf16 or fp32 output.
+// Sum of S fp32 partial results -> bf16 or fp32 output (out_bf16: 0 fp32,
+// 1 bf16, 2 bf16 in the row-pair layout, ldc its pair pitch).
 __global__ __launch_bounds__(256)
 void splitk_reduce_kernel(const float* __restrict__ P, int S, int64_t split_stride, int64_t ldp,
                           void* __restrict__ Cout, int64_t ldc, int R, int Cc, int out_bf16) {
@@ -217,7 +218,9 @@ void splitk_reduce_kernel(const float* __restrict__ P, int S, int64_t split_stri
         const int64_t c = e - r * Cc;
         float s = 0.f;
         for (int i = 0; i < S; ++i) s += P[i * split_stride + r * ldp + c];
-        if (out_bf16)
+        if (out_bf16 == 2)
+            reinterpret_cast<uint16_t*>(Cout)[pair_offset(r, c, ldc)] = (uint16_t)bf16_rne(s);
+        else if (out_bf16)
             reinterpret_cast<uint16_t*>(Cout)[r * ldc + c] = (uint16_t)bf16_rne(s);
         else
             reinterpret_cast<float*>(Cout)[r * ldc + c] = s;

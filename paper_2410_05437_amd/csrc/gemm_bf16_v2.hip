@@ -509,7 +509,7 @@ hipError_t launch_v2(const GemmArgs& g, hipStream_t stream) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_splitk_reduce(g.partial, S, split_stride, ldp, g.C, g.ldc, g.R, g.Cc,
-                                g.c_f32 ? 0 : 1, stream);
+                                g.c_f32 ? 0 : (g.c_pairs ? 2 : 1), stream);
 }
 
 }  // namespace
@@ -536,9 +536,9 @@ void tile_dims(int tile, int* bm, int* bn) {
 // offsets).
 hipError_t launch_gemm_tn_bf16_v2(const GemmArgs& g, hipStream_t stream) {
     const int64_t lim = (int64_t)1 << 31;
-    // a row-pair output: one depth range or the pair combine, whole 64-element
-    // blocks per pair; A is always plain here
-    if (g.a_pairs || (g.c_pairs && ((g.splits > 1 && !(g.pair && g.splits == 2)) || g.ldc % 64 || g.c_f32)))
+    // a row-pair output: bf16, whole 64-element blocks per pair; A is always
+    // plain here
+    if (g.a_pairs || (g.c_pairs && (g.ldc % 64 || g.c_f32)))
         return hipErrorNotSupported;
     if ((int64_t)g.R * g.lda >= lim || (int64_t)g.Cc * g.ldb >= lim || g.c_f32) {
         if (g.c_pairs) return hipErrorNotSupported;

@@ -417,7 +417,7 @@ hipError_t launch_v3(const GemmArgs& g, hipStream_t stream) {
                        map, nullptr, nullptr, 0ull, g.wait, 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    return launch_splitk_reduce(g.partial, S, split_stride, ldp, g.C, g.ldc, g.R, g.Cc, 1, stream);
+    return launch_splitk_reduce(g.partial, S, split_stride, ldp, g.C, g.ldc, g.R, g.Cc, g.c_pairs ? 2 : 1, stream);
 }
 
 template <int BN>
@@ -462,14 +462,12 @@ hipError_t launch_gemm_tn_bf16_v3(const GemmArgs& g, hipStream_t stream) {
     if ((int64_t)g.R * g.lda >= lim || (int64_t)g.Cc * g.ldb >= lim || (int64_t)g.R * g.ldc >= lim ||
         g.c_f32)
         return hipErrorInvalidValue;
-    // row-pair A only on the single-range kernel; a row-pair output only where
-    // the kernel writes bf16 itself (one range or the pair combine); pair
-    // pitches are whole 64-element blocks
+    // row-pair A only on the single-range kernel; pair pitches are whole
+    // 64-element blocks
     const int ktiles = (g.D + V3_BK - 1) / V3_BK;
     const int S = g.splits < 1 ? 1 : g.splits;
     const int nranges = (ktiles + (ktiles + S - 1) / S - 1) / ((ktiles + S - 1) / S);
-    if ((g.a_pairs && (nranges != 1 || g.lda % 64)) ||
-        (g.c_pairs && ((nranges != 1 && !(g.pair && nranges == 2)) || g.ldc % 64)))
+    if ((g.a_pairs && (nranges != 1 || g.lda % 64)) || (g.c_pairs && g.ldc % 64))
         return hipErrorNotSupported;
     switch (g.tile) {
         case TILE_256x256:

@@ -97,6 +97,7 @@ hipError_t launch_gemv_tn_bf16(const GemmArgs& g, hipStream_t stream);
 // says whether the tokens and depth fit (depth up to 6144).
 bool stream_supported(int R, int D);
 hipError_t launch_stream_tn_bf16(const GemmArgs& g, hipStream_t stream);
+// out_bf16: 0 fp32 output, 1 bf16, 2 bf16 in the row-pair layout
 hipError_t launch_splitk_reduce(const float* P, int S, int64_t split_stride, int64_t ldp,
                                 void* C, int64_t ldc, int R, int Cc, int out_bf16,
                                 hipStream_t stream);

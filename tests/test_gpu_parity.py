@@ -591,10 +591,12 @@ def test_prefill_layer_shapes(E, shape):
 # (K, M, L, N) of prefill layers that keep Z in the row-pair layout (an odd
 # token count, whose last pair has one token; a component count that is not a
 # multiple of 64, or of 8, with the expand GEMM's masked depth tail on row
-# pairs; the projection on the 128 x 192 tile and, at depth 11008, on the
-# four-wave 256 x 192 tile in two depth halves; a projection depth tail)
+# pairs; projections on the 128 x 192 tile, on the four-wave 256 x 192 tile
+# in two depth halves (depth 11008), with a projection depth tail, in two
+# launches split by rows (the first in two depth halves; the GPT3-22B FFN-up
+# class at L = 2458), and in four depth ranges summed by the reduction pass)
 ROW_PAIR_SHAPES = [(4096, 12288, 1536, 4095), (4096, 6000, 1500, 4095), (4100, 12288, 1300, 4095),
-                   (11008, 4096, 1536, 4095)]
+                   (11008, 4096, 1536, 4095), (6144, 2048, 2458, 8191), (8192, 12288, 1000, 2047)]
 
 
 def _row_pairs(Z, ldp):
