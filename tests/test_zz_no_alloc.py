@@ -28,9 +28,11 @@ def _case(E, dev, K, M, L, N, seed):
 def test_noalloc_matches_workspace_call():
     dev = need_gpu()
     import paper_2410_05437_amd as E
-    # a prefill layer (tiled GEMMs, Z in the scratch), then a smaller one with
+    # a prefill layer whose Z sits in the scratch in row pairs (an odd token
+    # count, components not a multiple of 64), then smaller ones: tiled GEMMs,
     # a pair-combined projection, then a decode call
-    cases = [(2048, 3000, 512, 1500, 1), (1100, 600, 700, 1000, 2), (1003, 1500, 200, 16, 3)]
+    cases = [(4096, 6000, 1500, 4095, 4), (2048, 3000, 512, 1500, 1), (1100, 600, 700, 1000, 2),
+             (1003, 1500, 200, 16, 3)]
     for K, M, L, N, seed in cases:
         inp, X, Pt, Wf = _case(E, dev, K, M, L, N, seed)
         Y_na = E.espace_projected_linear_noalloc(X, Pt, Wf, out_mat(N, M, "bf16", dev))
